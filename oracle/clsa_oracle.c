@@ -1,0 +1,227 @@
+/*
+ * CPU oracle for the CLSA shared-routing sparse attention path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
+ * loads this file; only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg do.  It shares no code, header, table or helper with the GPU
+ * kernels.
+ *
+ * Plain, slow and meant to be checked by eye against the paper
+ * ("You Only Index Once: Cross-Layer Sparse Attention with Shared Routing"):
+ *   - every bfloat16 input is widened exactly to double;
+ *   - every sum is accumulated in double, in plain loop order;
+ *   - the top-k is a full sort, not a selection algorithm.
+ *
+ * Functions and the passage each follows:
+ *   oracle_index_scores  Section 2.1, Eq. (3): I = Q_idx K_idx^T, one indexing
+ *                        head of width d_idx = idx_heads * idx_dim (the per-token
+ *                        index key is stored as idx_heads blocks of idx_dim).
+ *   oracle_topk          Section 2.1, Eq. (3): S_t = TopK(I_t, k).
+ *   oracle_sparse_attn   Section 2.1, Eq. (4): O_t = Attn(Q_t, K_{S_t}, V_{S_t}),
+ *                        softmax attention of Eq. (1) restricted to S_t, with GQA.
+ *   oracle_decode_step   Section 2.1 last paragraph and Section 2.3 ("compute
+ *                        top-k once"): one index pass, one top-k, then every
+ *                        layer reuses the same S_t.
+ *
+ * Readings where the paper is silent (each is listed with its reason in the
+ * design notes):
+ *   - valid keys of row (b,t) are j < seq_lens[b], and also j <= q_pos[b,t]
+ *     when causal (inclusive: the current token's cache entry exists);
+ *   - the selection order is (score descending, token index ascending), so ties
+ *     at the k-th score go to the lowest token index; S is written ascending,
+ *     padded with -1, n_sel = min(k, |valid|);
+ *   - the selection is decided on scores rounded to float32 (the precision the
+ *     GPU path decides in); -0.0 and +0.0 compare equal;
+ *   - query head h uses key/value head floor(h / (q_heads / kv_heads));
+ *   - no positional encoding on this path; scale = softmax_scale;
+ *   - an empty index set (n_sel = 0) gives output 0 and lse = -inf.
+ */
+#include "clsa_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+double oracle_bf16_to_double(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* Element offset of token j of sequence b in a cache whose token rows hold
+ * row_elems elements: contiguous [B, max_len, ...] or paged [P, page, ...]. */
+static size_t token_row(const oracle_shape *s, const int32_t *page_table, int b, int j,
+                        size_t row_elems)
+{
+    if (s->page_size == 0)
+        return ((size_t)b * (size_t)s->max_len + (size_t)j) * row_elems;
+    int32_t page = page_table[(size_t)b * (size_t)s->max_pages + (size_t)(j / s->page_size)];
+    return ((size_t)page * (size_t)s->page_size + (size_t)(j % s->page_size)) * row_elems;
+}
+
+/* Number of valid keys of query row (b,t); the valid keys are 0..n-1. */
+int oracle_valid_len(const oracle_shape *s, const int32_t *seq_lens, const int32_t *q_pos,
+                     int b, int t)
+{
+    int n = seq_lens[b];
+    if (s->causal) {
+        int lim = q_pos[(size_t)b * s->n_q + t] + 1;
+        if (lim < n)
+            n = lim;
+    }
+    return n < 0 ? 0 : n;
+}
+
+/* Eq. (3), first half: s[b,t,j] = sum_i q_idx[b,t,i] * k_idx[b,j,i], i over the
+ * d_idx = idx_heads*idx_dim components of the single indexing head. */
+void oracle_index_scores(const oracle_shape *s, const uint16_t *q_idx, const uint16_t *k_idx,
+                         const int32_t *page_table, const int32_t *seq_lens,
+                         const int32_t *q_pos, double *scores)
+{
+    const int d_idx = s->idx_heads * s->idx_dim;
+    for (int b = 0; b < s->batch; b++) {
+        for (int t = 0; t < s->n_q; t++) {
+            const uint16_t *q = q_idx + ((size_t)b * s->n_q + t) * d_idx;
+            double *row = scores + ((size_t)b * s->n_q + t) * (size_t)s->max_len;
+            int n = oracle_valid_len(s, seq_lens, q_pos, b, t);
+            for (int j = 0; j < n; j++) {
+                const uint16_t *k = k_idx + token_row(s, page_table, b, j, (size_t)d_idx);
+                double acc = 0.0;
+                for (int i = 0; i < d_idx; i++)
+                    acc += oracle_bf16_to_double(q[i]) * oracle_bf16_to_double(k[i]);
+                row[j] = acc;
+            }
+        }
+    }
+}
+
+typedef struct {
+    float s;
+    int32_t j;
+} scored_token;
+
+/* Selection order: higher score first; equal scores: lower token index first. */
+static int by_score_then_index(const void *pa, const void *pb)
+{
+    const scored_token *a = (const scored_token *)pa, *b = (const scored_token *)pb;
+    if (a->s > b->s) return -1;
+    if (a->s < b->s) return 1;
+    return (a->j > b->j) - (a->j < b->j);
+}
+
+static int by_int(const void *pa, const void *pb)
+{
+    int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    return (a > b) - (a < b);
+}
+
+/* Eq. (3), second half: S = the first min(k, n) valid tokens in selection order,
+ * written in ascending token order and padded with -1. */
+void oracle_topk(const oracle_shape *s, const float *scores, const int32_t *seq_lens,
+                 const int32_t *q_pos, int32_t *idx, int32_t *n_sel)
+{
+    const int k = s->top_k;
+    scored_token *buf = (scored_token *)malloc(sizeof(scored_token) * (size_t)(s->max_len > 0 ? s->max_len : 1));
+    for (int b = 0; b < s->batch; b++) {
+        for (int t = 0; t < s->n_q; t++) {
+            const size_t r = (size_t)b * s->n_q + t;
+            const float *row = scores + r * (size_t)s->max_len;
+            int n = oracle_valid_len(s, seq_lens, q_pos, b, t);
+            for (int j = 0; j < n; j++) {
+                buf[j].s = row[j];
+                buf[j].j = j;
+            }
+            qsort(buf, (size_t)n, sizeof *buf, by_score_then_index);
+            int m = n < k ? n : k;
+            int32_t *out = idx + r * (size_t)k;
+            for (int i = 0; i < m; i++)
+                out[i] = buf[i].j;
+            qsort(out, (size_t)m, sizeof *out, by_int);
+            for (int i = m; i < k; i++)
+                out[i] = -1;
+            n_sel[r] = m;
+        }
+    }
+    free(buf);
+}
+
+/* Eq. (4) with the softmax attention of Eq. (1), one layer:
+ *   z_i = scale * <q[b,t,h], K[b, S_i, g]>,  w = softmax(z),
+ *   out[b,t,h] = sum_i w_i V[b, S_i, g],     lse[b,t,h] = log sum_i exp(z_i),
+ * with g = floor(h / (q_heads / kv_heads)). */
+void oracle_sparse_attn(const oracle_shape *s, const uint16_t *q, const uint16_t *k_cache,
+                        const uint16_t *v_cache, const int32_t *page_table, const int32_t *idx,
+                        const int32_t *n_sel, double *out, double *lse)
+{
+    const int D = s->head_dim, Hq = s->q_heads, Hkv = s->kv_heads, k = s->top_k;
+    const int group = Hq / Hkv;
+    const size_t kv_row = (size_t)Hkv * D;
+    double *z = (double *)malloc(sizeof(double) * (size_t)(k > 0 ? k : 1));
+    for (int b = 0; b < s->batch; b++) {
+        for (int t = 0; t < s->n_q; t++) {
+            const size_t r = (size_t)b * s->n_q + t;
+            const int32_t *S = idx + r * (size_t)k;
+            const int m = n_sel[r];
+            for (int h = 0; h < Hq; h++) {
+                const int g = h / group;
+                const uint16_t *qh = q + (r * Hq + h) * D;
+                double *o = out + (r * Hq + h) * D;
+                for (int e = 0; e < D; e++)
+                    o[e] = 0.0;
+                if (m == 0) {
+                    if (lse) lse[r * Hq + h] = -INFINITY;
+                    continue;
+                }
+                double zmax = -INFINITY;
+                for (int i = 0; i < m; i++) {
+                    const uint16_t *kr = k_cache + token_row(s, page_table, b, S[i], kv_row) + (size_t)g * D;
+                    double acc = 0.0;
+                    for (int e = 0; e < D; e++)
+                        acc += oracle_bf16_to_double(qh[e]) * oracle_bf16_to_double(kr[e]);
+                    z[i] = s->softmax_scale * acc;
+                    if (z[i] > zmax)
+                        zmax = z[i];
+                }
+                double denom = 0.0;
+                for (int i = 0; i < m; i++)
+                    denom += exp(z[i] - zmax);
+                for (int i = 0; i < m; i++) {
+                    const double w = exp(z[i] - zmax) / denom;
+                    const uint16_t *vr = v_cache + token_row(s, page_table, b, S[i], kv_row) + (size_t)g * D;
+                    for (int e = 0; e < D; e++)
+                        o[e] += w * oracle_bf16_to_double(vr[e]);
+                }
+                if (lse) lse[r * Hq + h] = zmax + log(denom);
+            }
+        }
+    }
+    free(z);
+}
+
+/* One decode (or chunked-prefill) step: index once, select once, then every one
+ * of the n_layers layers attends over the same S with its own query. */
+void oracle_decode_step(const oracle_shape *s, const uint16_t *q_idx, const uint16_t *k_idx,
+                        const uint16_t *k_cache, const uint16_t *v_cache,
+                        const int32_t *page_table, const int32_t *seq_lens, const int32_t *q_pos,
+                        int n_layers, const uint16_t *q_layers, double *out_layers,
+                        double *lse_layers, int32_t *idx, int32_t *n_sel, double *scores)
+{
+    const size_t rows = (size_t)s->batch * s->n_q;
+    const size_t nsc = rows * (size_t)s->max_len;
+    float *s32 = (float *)malloc(sizeof(float) * (nsc > 0 ? nsc : 1));
+    for (size_t i = 0; i < nsc; i++)
+        scores[i] = 0.0;
+    oracle_index_scores(s, q_idx, k_idx, page_table, seq_lens, q_pos, scores);
+    for (size_t i = 0; i < nsc; i++)
+        s32[i] = (float)scores[i];
+    oracle_topk(s, s32, seq_lens, q_pos, idx, n_sel);
+    free(s32);
+    const size_t per_layer_q = rows * (size_t)s->q_heads * s->head_dim;
+    const size_t per_layer_lse = rows * (size_t)s->q_heads;
+    for (int l = 0; l < n_layers; l++)
+        oracle_sparse_attn(s, q_layers + l * per_layer_q, k_cache, v_cache, page_table, idx, n_sel,
+                           out_layers + l * per_layer_q,
+                           lse_layers ? lse_layers + l * per_layer_lse : NULL);
+}
