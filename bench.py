@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Benchmark of the CLSA decode step on one MI355X.
+
+One step = one clsa_decode_step call: the indexer over every cached token, one
+top-k, then L sparse-attention layers that share the index set.  Workload (by
+default): batch 4, 131072-token contexts, top-k 2048, 32 query / 8 KV heads of
+128, 16 layers, 64 planted aligned index keys per sequence; synthetic seeded
+bf16 inputs.
+
+Prints ONE JSON line: metric, value (us per decode step), roofline of the
+dominant kernel (the indexer, HBM-bound) measured with HIP events on the
+library's stream over the timed region, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "CLSA decode-step µs + HBM GB/s (index+top-k+L sparse attn), 128K ctx"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w):
+    """Bytes the step must move at least once (unique): index keys + scores out,
+    the selected K/V rows once, per-layer queries and outputs, the index set."""
+    toks = sum(w.lens)
+    index_keys = toks * w.idx_heads * w.idx_dim * 2
+    scores = toks * 4
+    sel = sum(min(w.top_k, n) for n in w.lens) * w.n_q
+    kv_rows = sel * w.kv_heads * w.head_dim * 2 * 2
+    qo = w.n_layers * w.batch * w.n_q * w.q_heads * w.head_dim * 2 * 2
+    idx = w.batch * w.n_q * w.top_k * 4
+    return dict(index=index_keys + scores, step=index_keys + scores + kv_rows + qo + idx,
+                kv_rows=kv_rows)
+
+
+def cpu_baseline(w, x, budget_s: float):
+    """Time the CPU oracle on the same workload, repeating whole steps until
+    ``budget_s`` seconds have passed (at least one)."""
+    import oracle as orc
+    sh = orc.shape_of(w)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        orc.decode_step(sh, x["q_idx"], x["k_idx"], x["k_cache"], x["v_cache"], x["seq_lens"],
+                        x["q_layers"], x["q_pos"], x["page_table"])
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
+            break
+    us = el / reps * 1e6
+    return {"value": round(us, 1), "unit": "us/step", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} full decode step(s) of {w.name} (B={w.batch}, L={w.n_layers}), "
+                      f"single-threaded C, {el:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="decode_b4_n128k_planted")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle time for the CPU baseline (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the decode path "
+                                   "shards by sequence with no communication, so --gpus N>1 "
+                                   "is not measured here"}))
+        return 2
+
+    import torch
+    from paper_2606_06467_amd import binding as B
+    from paper_2606_06467_amd import inputs
+
+    w = inputs.workload(args.workload)
+    if w.n_q != 1:
+        log("note: chunked-prefill workload timed through the decode-step entry point")
+    log(f"[bench] generating {w.name} ...")
+    t = time.time()
+    x = inputs.make_inputs(w)
+    log(f"[bench] inputs ready in {time.time() - t:.1f} s")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def bf(a):
+        return B.bf16_from_bits(a, dev)
+
+    # Several copies of the caches so that consecutive steps read different HBM
+    # (no cache reuse across steps: each step starts cold like a new batch).
+    per_copy = x["k_idx"].nbytes + x["k_cache"].nbytes + x["v_cache"].nbytes
+    copies = int(min(16, max(2, math.ceil(768e6 / per_copy))))
+    caches = []
+    for c in range(copies):
+        caches.append((bf(x["k_idx"]), bf(x["k_cache"]), bf(x["v_cache"])))
+    q_idx = bf(x["q_idx"])
+    q_layers = bf(x["q_layers"])
+    seq_lens = torch.from_numpy(x["seq_lens"]).to(dev)
+    q_pos = None if x["q_pos"] is None else torch.from_numpy(x["q_pos"]).to(dev)
+    pt = None if x["page_table"] is None else torch.from_numpy(x["page_table"]).to(dev)
+    sh = B.make_shape(batch=w.batch, n_q=w.n_q, max_len=w.max_len, top_k=w.top_k,
+                      q_heads=w.q_heads, kv_heads=w.kv_heads, page_size=w.page_size,
+                      max_pages=w.max_pages, causal=w.causal)
+    L = w.n_layers
+    out = torch.empty((L, w.batch, w.n_q, w.q_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((L, w.batch, w.n_q, w.q_heads), dtype=torch.float32, device=dev)
+    idx = torch.empty((w.batch, w.n_q, w.top_k), dtype=torch.int32, device=dev)
+    ns = torch.empty((w.batch, w.n_q), dtype=torch.int32, device=dev)
+    ws = B.workspace(sh, B.CLSA_OP_DECODE, L, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i):
+        ki, kc, vc = caches[i % copies]
+        B.clsa_decode_step(sh, q_idx, ki, kc, vc, pt, seq_lens, q_pos, q_layers, out, lse, idx,
+                           ns, ws, stream)
+
+    log(f"[bench] {copies} cache copies, warmup {args.warmup} ...")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps ----
+    log(f"[bench] timing {args.steps} steps ...")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    # ---- the same K steps again with phase events (kernel times on this stream) ----
+    ev = B.HipEvents(4 * args.steps)
+    for i in range(args.steps):
+        B.clsa_set_phase_events(ev.handles[4 * i: 4 * i + 4])
+        step(i)
+    B.clsa_set_phase_events(None)
+    torch.cuda.synchronize()
+    ph = np.array([[ev.elapsed_ms(4 * i + a, 4 * i + a + 1) for a in range(3)]
+                   for i in range(args.steps)])
+    ev.close()
+    index_ms, topk_ms, layers_ms = (float(v) for v in ph.mean(axis=0))
+
+    ab = algorithmic_bytes(w)
+    step_us = ms_per_step * 1e3
+    achieved = ab["index"] / (index_ms * 1e-3) / 1e9
+    res = {
+        "metric": METRIC,
+        "value": round(step_us, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "context": max(w.lens),
+                   "top_k": w.top_k, "layers": L, "q_heads": w.q_heads, "kv_heads": w.kv_heads,
+                   "head_dim": w.head_dim, "index_dim": w.idx_heads * w.idx_dim,
+                   "paged": bool(w.page_size), "planted": w.planted},
+        "tokens_per_s": round(w.batch * w.n_q / (ms_per_step * 1e-3), 1),
+        "hbm_GBps": round(ab["step"] / (ms_per_step * 1e-3) / 1e9, 1),
+        "phases_us": {"index": round(index_ms * 1e3, 2), "topk": round(topk_ms * 1e3, 2),
+                      "layers": round(layers_ms * 1e3, 2),
+                      "per_layer": round(layers_ms * 1e3 / max(L, 1), 2)},
+        "roofline": {"bound": "hbm", "kernel": "index_decode_kernel<true>",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": ab["index"]},
+    }
+    if args.cpu_budget > 0:
+        log("[bench] CPU oracle baseline ...")
+        res["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

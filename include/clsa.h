@@ -1,0 +1,166 @@
+/*
+ * libclsa -- MI355X (gfx950) kernels for the decode hot path of Cross-Layer
+ * Sparse Attention ("You Only Index Once: Cross-Layer Sparse Attention with
+ * Shared Routing").
+ *
+ * The path: one indexer pass scores the current query against every cached
+ * token's index key (Section 2.1, Eq. 3, I = Q_idx K_idx^T), one token-level
+ * top-k is taken (Eq. 3, S_t = TopK(I_t, k)), and every cross-decoder layer
+ * attends only to the selected rows of the one shared KV cache (Eq. 4,
+ * O_t = Attn(Q_t, K_{S_t}, V_{S_t})), reusing the same S_t (Section 2.1, last
+ * paragraph; Section 2.3: top-k is computed once per step).
+ *
+ * Conventions for every entry point
+ *   - All tensor arguments are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or retains them.  bfloat16 tensors are passed as
+ *     void* and must be 16-byte aligned; int32/float tensors 4-byte aligned.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Every call only
+ *     enqueues work on that stream and returns without synchronising; errors
+ *     inside kernels are not reported back.
+ *   - `ws` is caller-owned device scratch of at least clsa_workspace_bytes()
+ *     bytes, 256-byte aligned.  Its contents need not be initialised and are
+ *     undefined afterwards.  Two calls that overlap in time must not share one
+ *     workspace.
+ *   - Arguments are validated on the host before anything is enqueued; on any
+ *     error nothing is enqueued.  No C++ exception crosses this interface.
+ *   - Device-side values are trusted within documented ranges: seq_lens[b] is
+ *     clamped to [0, max_len]; q_pos (causal) limits row (b,t) to keys
+ *     j <= q_pos[b,t]; page_table entries for pages that hold valid tokens
+ *     must be valid physical page numbers (they are not range-checked).
+ *
+ * Tensor layouts (row-major, R = batch * n_q query rows, row r = b * n_q + t):
+ *   q_idx       bf16 [batch, n_q, idx_heads, idx_dim]   index query (Eq. 2)
+ *   k_idx       bf16 [batch, max_len, idx_heads, idx_dim]          contiguous
+ *               bf16 [num_pages, page_size, idx_heads, idx_dim]    paged
+ *   k_cache,    bf16 [batch, max_len, kv_heads, head_dim]          contiguous
+ *   v_cache     bf16 [num_pages, page_size, kv_heads, head_dim]    paged
+ *   page_table  int32 [batch, max_pages]: physical page of logical page p of
+ *               sequence b; shared by k_idx, k_cache and v_cache (the routing
+ *               index is bound to the shared KV cache, Section 2.1)
+ *   seq_lens    int32 [batch]: cached tokens per sequence (incl. the current one)
+ *   q_pos       int32 [batch, n_q]: absolute position of each query (causal only)
+ *   scores      fp32 [batch, n_q, max_len]: only valid positions are written
+ *   idx         int32 [batch, n_q, top_k]: selected token positions, ascending,
+ *               padded with -1
+ *   n_sel       int32 [batch, n_q]: min(top_k, number of valid keys)
+ *   q, out      bf16 [batch, n_q, q_heads, head_dim]
+ *   lse         fp32 [batch, n_q, q_heads] natural-log sum of exp of the scaled
+ *               logits over S (-inf for an empty S), or NULL
+ *   q_layers,   bf16 [n_layers, batch, n_q, q_heads, head_dim]
+ *   out_layers
+ *   lse_layers  fp32 [n_layers, batch, n_q, q_heads] or NULL
+ *
+ * Semantics fixed where the paper is silent
+ *   - valid keys of row (b,t): j < seq_lens[b] and, when causal, j <= q_pos[b,t];
+ *   - selection order: score descending, then token index ascending, i.e. ties
+ *     at the k-th score go to the lowest index; -0.0 and +0.0 are equal; NaN
+ *     scores are not supported;
+ *   - query head h reads key/value head h / (q_heads / kv_heads) (GQA);
+ *   - no positional encoding is applied on this path;
+ *   - an empty S (no valid key) yields out = 0 and lse = -inf.
+ *
+ * Supported shapes (CLSA_ERR_UNSUPPORTED otherwise; there is no fallback):
+ *   idx_heads * idx_dim == 256, head_dim == 128,
+ *   q_heads / kv_heads in {1, 2, 4, 5, 8}, 1 <= top_k <= 8192,
+ *   max_len <= 262144, page_size 0 or a power of two in [16, 4096].
+ */
+#ifndef CLSA_H
+#define CLSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CLSA_OK = 0,
+    CLSA_ERR_INVALID_ARG = -1, /* null/misaligned pointer, non-positive size, ... */
+    CLSA_ERR_UNSUPPORTED = -2, /* a shape outside the compiled set               */
+    CLSA_ERR_WORKSPACE = -3,   /* ws NULL or smaller than clsa_workspace_bytes()  */
+    CLSA_ERR_HIP = -4          /* the HIP runtime reported an error on enqueue   */
+} clsa_status;
+
+typedef enum {
+    CLSA_OP_INDEX = 0,  /* clsa_index_scores (needs no workspace) */
+    CLSA_OP_TOPK = 1,   /* clsa_topk */
+    CLSA_OP_ATTN = 2,   /* clsa_sparse_attn */
+    CLSA_OP_DECODE = 3  /* clsa_decode_step */
+} clsa_op;
+
+typedef struct clsa_shape {
+    int32_t batch;       /* B sequences                                          */
+    int32_t n_q;         /* T query tokens per sequence (1 = decode)              */
+    int32_t idx_heads;   /* index key stored as idx_heads blocks of idx_dim: one  */
+    int32_t idx_dim;     /*   indexing head of width d_idx = idx_heads * idx_dim  */
+    int32_t q_heads;     /* attention query heads                                 */
+    int32_t kv_heads;    /* key/value heads of the shared cache                   */
+    int32_t head_dim;    /* D                                                     */
+    int32_t max_len;     /* capacity per sequence; row stride of scores and of    */
+                         /*   contiguous caches; a multiple of page_size if paged */
+    int32_t page_size;   /* 0 = contiguous caches, else tokens per page           */
+    int32_t max_pages;   /* columns of page_table (>= max_len / page_size)        */
+    int32_t top_k;       /* k                                                     */
+    int32_t causal;      /* 1: row (b,t) also limited to keys j <= q_pos[b,t]     */
+    float softmax_scale; /* logit scale of Eq. 4's softmax (1/sqrt(head_dim))     */
+} clsa_shape;
+
+/* Bytes of workspace `op` needs for `shape` (n_layers only matters for
+ * CLSA_OP_DECODE).  Returns 0 for CLSA_OP_INDEX, and also 0 when the shape is
+ * invalid or unsupported (the entry point then reports the reason). */
+size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layers);
+
+/* Eq. 3, first half: scores[b,t,j] = sum_i q_idx[b,t,i] * k_idx[b,j,i] over the
+ * d_idx components of the single indexing head, for every valid j; bf16 inputs,
+ * fp32 products and accumulation; no scale and no nonlinearity.  page_table
+ * may be NULL when page_size == 0; q_pos may be NULL unless causal. */
+clsa_status clsa_index_scores(const clsa_shape *shape, const void *q_idx, const void *k_idx,
+                              const int32_t *page_table, const int32_t *seq_lens,
+                              const int32_t *q_pos, float *scores, void *stream);
+
+/* Eq. 3, second half: for every row (b,t), the min(top_k, n_valid) valid
+ * positions with the largest scores (ties to the lowest index), written in
+ * ascending order to idx[b,t,:], padded with -1; n_sel[b,t] = their count.
+ * Exact: the set is decided on the given fp32 scores with no approximation. */
+clsa_status clsa_topk(const clsa_shape *shape, const float *scores, const int32_t *seq_lens,
+                      const int32_t *q_pos, int32_t *idx, int32_t *n_sel, void *ws,
+                      size_t ws_bytes, void *stream);
+
+/* Eq. 4, one layer: for every row (b,t) and query head h, softmax attention of
+ * q[b,t,h] over the rows idx[b,t,0..n_sel-1] of head g = h/(q_heads/kv_heads)
+ * of the shared K/V cache, logits scaled by softmax_scale; fp32 math, bf16
+ * out, optional fp32 lse.  idx entries beyond n_sel are ignored; entries below
+ * n_sel must be valid positions (< seq_lens[b]) of sequence b. */
+clsa_status clsa_sparse_attn(const clsa_shape *shape, const void *q, const void *k_cache,
+                             const void *v_cache, const int32_t *page_table, const int32_t *idx,
+                             const int32_t *n_sel, void *out, float *lse, void *ws,
+                             size_t ws_bytes, void *stream);
+
+/* One step of the shared-routing path (Section 2.1; Section 2.3): one indexer
+ * pass and one top-k over the whole cache, then n_layers attention passes
+ * in layer order, layer l using q_layers[l] and the same index set.  The index
+ * set is also returned in idx / n_sel.  The scores live in the workspace. */
+clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const void *k_idx,
+                             const void *k_cache, const void *v_cache,
+                             const int32_t *page_table, const int32_t *seq_lens,
+                             const int32_t *q_pos, int32_t n_layers, const void *q_layers,
+                             void *out_layers, float *lse_layers, int32_t *idx, int32_t *n_sel,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/* Static, human-readable name of a status code. */
+const char *clsa_status_string(clsa_status status);
+
+/* Profiling hook (not thread-safe; set and use from one thread).  With n == 4
+ * and four hipEvent_t handles, the next clsa_decode_step calls record
+ * events[0] right before the indexer kernel, events[1] after it, events[2]
+ * after the top-k and events[3] after the last layer, on the call's stream.
+ * n == 0 (events may be NULL) switches the hook off.  Any other n is
+ * CLSA_ERR_INVALID_ARG. */
+clsa_status clsa_set_phase_events(void *const *events, int32_t n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLSA_H */

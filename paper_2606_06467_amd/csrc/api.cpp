@@ -1,0 +1,282 @@
+// C-ABI entry points of libclsa: host-side validation, workspace carving and
+// kernel dispatch.  Nothing here allocates device memory or synchronises.
+#include "clsa.h"
+
+#include <math.h>
+#include <stdint.h>
+
+#include "clsa_internal.h"
+
+namespace {
+
+using clsa::Geometry;
+
+constexpr int kMaxTopK = 8192;
+constexpr int kMaxLen = 262144;
+constexpr size_t kAlign = 256;
+
+struct PhaseHook {
+    hipEvent_t ev[4];
+    bool on = false;
+} g_hook;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int log2i(int x) {
+    int s = 0;
+    while ((1 << s) < x) ++s;
+    return s;
+}
+
+enum Needs : unsigned { kIndex = 1u, kTopk = 2u, kAttn = 4u };
+
+// Checks the shape for the operations in `needs` and fills the kernel geometry.
+clsa_status check_shape(const clsa_shape *s, unsigned needs, Geometry *g) {
+    if (!s) return CLSA_ERR_INVALID_ARG;
+    if (s->batch < 1 || s->n_q < 1 || s->max_len < 1 || s->top_k < 1) return CLSA_ERR_INVALID_ARG;
+    if (s->idx_heads < 1 || s->idx_dim < 1 || s->q_heads < 1 || s->kv_heads < 1 || s->head_dim < 1)
+        return CLSA_ERR_INVALID_ARG;
+    if ((int64_t)s->batch * s->n_q > 0x7fffffff) return CLSA_ERR_INVALID_ARG;
+    if (s->causal != 0 && s->causal != 1) return CLSA_ERR_INVALID_ARG;
+    if (s->page_size != 0) {
+        if (!is_pow2(s->page_size)) return CLSA_ERR_INVALID_ARG;
+        if (s->max_len % s->page_size != 0) return CLSA_ERR_INVALID_ARG;
+        if ((int64_t)s->max_pages * s->page_size < s->max_len) return CLSA_ERR_INVALID_ARG;
+        if (s->page_size < 16 || s->page_size > 4096) return CLSA_ERR_UNSUPPORTED;
+    }
+    if ((needs & kAttn) && !isfinite(s->softmax_scale)) return CLSA_ERR_INVALID_ARG;
+    if ((needs & kAttn) && s->q_heads % s->kv_heads != 0) return CLSA_ERR_INVALID_ARG;
+    if ((needs & kIndex) && s->idx_heads * s->idx_dim != 256) return CLSA_ERR_UNSUPPORTED;
+    if (needs & kAttn) {
+        const int grp = s->q_heads / s->kv_heads;
+        if (s->head_dim != 128) return CLSA_ERR_UNSUPPORTED;
+        if (grp != 1 && grp != 2 && grp != 4 && grp != 5 && grp != 8) return CLSA_ERR_UNSUPPORTED;
+    }
+    if (s->top_k > kMaxTopK) return CLSA_ERR_UNSUPPORTED;
+    if ((needs & (kIndex | kTopk)) && s->max_len > kMaxLen) return CLSA_ERR_UNSUPPORTED;
+    g->batch = s->batch;
+    g->n_q = s->n_q;
+    g->rows = s->batch * s->n_q;
+    g->max_len = s->max_len;
+    g->page_shift = s->page_size ? log2i(s->page_size) : -1;
+    g->max_pages = s->page_size ? s->max_pages : 0;
+    g->top_k = s->top_k;
+    g->causal = s->causal;
+    g->q_heads = s->q_heads;
+    g->kv_heads = s->kv_heads;
+    g->group = s->q_heads / s->kv_heads;
+    g->softmax_scale = s->softmax_scale;
+    return CLSA_OK;
+}
+
+clsa_status check_ptr(const void *p, uintptr_t align) {
+    if (!p || !aligned(p, align)) return CLSA_ERR_INVALID_ARG;
+    return CLSA_OK;
+}
+
+#define CLSA_TRY(expr)                        \
+    do {                                      \
+        const clsa_status st_ = (expr);       \
+        if (st_ != CLSA_OK) return st_;       \
+    } while (0)
+
+clsa_status check_common(const clsa_shape *s, const int32_t *page_table, const int32_t *q_pos,
+                         bool uses_q_pos, bool uses_pages) {
+    if (uses_pages && s->page_size) CLSA_TRY(check_ptr(page_table, 4));
+    if (uses_q_pos && s->causal) CLSA_TRY(check_ptr(q_pos, 4));
+    return CLSA_OK;
+}
+
+// Device limit on dynamic LDS per workgroup, cached per device.
+clsa_status check_topk_lds(int max_len) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return CLSA_ERR_HIP;
+    static int cached_dev = -1, cached_lds = 0;
+    if (cached_dev != dev) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+            return CLSA_ERR_HIP;
+        cached_lds = v;
+        cached_dev = dev;
+    }
+    return clsa::topk_lds_bytes(max_len) + 1024 <= (size_t)cached_lds ? CLSA_OK
+                                                                        : CLSA_ERR_UNSUPPORTED;
+}
+
+struct DecodeWs {
+    float *scores;
+    uint32_t *hist;
+    float *partials;
+};
+
+size_t decode_ws_layout(const Geometry &g, void *base, DecodeWs *out) {
+    size_t off = 0;
+    const size_t scores = align_up(sizeof(float) * (size_t)g.rows * g.max_len);
+    const size_t hist = align_up(sizeof(uint32_t) * (size_t)g.rows * clsa::kCoarseBins);
+    const size_t part = align_up(sizeof(float) * clsa::attn_partial_floats(g));
+    if (out) {
+        char *p = static_cast<char *>(base);
+        out->scores = reinterpret_cast<float *>(p + off);
+        out->hist = reinterpret_cast<uint32_t *>(p + off + scores);
+        out->partials = part ? reinterpret_cast<float *>(p + off + scores + hist) : nullptr;
+    }
+    return scores + hist + part;
+}
+
+clsa_status from_hip(hipError_t e) { return e == hipSuccess ? CLSA_OK : CLSA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layers) {
+    Geometry g;
+    switch (op) {
+        case CLSA_OP_INDEX:
+            return 0;
+        case CLSA_OP_TOPK:
+            return 0;
+        case CLSA_OP_ATTN:
+            if (check_shape(shape, kAttn, &g) != CLSA_OK) return 0;
+            return align_up(sizeof(float) * clsa::attn_partial_floats(g));
+        case CLSA_OP_DECODE:
+            (void)n_layers;
+            if (check_shape(shape, kIndex | kTopk | kAttn, &g) != CLSA_OK) return 0;
+            return decode_ws_layout(g, nullptr, nullptr);
+        default:
+            return 0;
+    }
+}
+
+clsa_status clsa_index_scores(const clsa_shape *shape, const void *q_idx, const void *k_idx,
+                              const int32_t *page_table, const int32_t *seq_lens,
+                              const int32_t *q_pos, float *scores, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kIndex, &g));
+    CLSA_TRY(check_ptr(q_idx, 16));
+    CLSA_TRY(check_ptr(k_idx, 16));
+    CLSA_TRY(check_ptr(seq_lens, 4));
+    CLSA_TRY(check_ptr(scores, 4));
+    CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
+    return from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, scores,
+                                              nullptr, static_cast<hipStream_t>(stream)));
+}
+
+clsa_status clsa_topk(const clsa_shape *shape, const float *scores, const int32_t *seq_lens,
+                      const int32_t *q_pos, int32_t *idx, int32_t *n_sel, void *ws,
+                      size_t ws_bytes, void *stream) {
+    (void)ws;
+    (void)ws_bytes;
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kTopk, &g));
+    CLSA_TRY(check_ptr(scores, 4));
+    CLSA_TRY(check_ptr(seq_lens, 4));
+    CLSA_TRY(check_ptr(idx, 4));
+    CLSA_TRY(check_ptr(n_sel, 4));
+    CLSA_TRY(check_common(shape, nullptr, q_pos, true, false));
+    CLSA_TRY(check_topk_lds(g.max_len));
+    return from_hip(clsa::launch_topk(g, scores, seq_lens, q_pos, nullptr, idx, n_sel,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+clsa_status clsa_sparse_attn(const clsa_shape *shape, const void *q, const void *k_cache,
+                             const void *v_cache, const int32_t *page_table, const int32_t *idx,
+                             const int32_t *n_sel, void *out, float *lse, void *ws,
+                             size_t ws_bytes, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kAttn, &g));
+    CLSA_TRY(check_ptr(q, 16));
+    CLSA_TRY(check_ptr(k_cache, 16));
+    CLSA_TRY(check_ptr(v_cache, 16));
+    CLSA_TRY(check_ptr(idx, 4));
+    CLSA_TRY(check_ptr(n_sel, 4));
+    CLSA_TRY(check_ptr(out, 16));
+    if (lse) CLSA_TRY(check_ptr(lse, 4));
+    CLSA_TRY(check_common(shape, page_table, nullptr, false, true));
+    const size_t need = align_up(sizeof(float) * clsa::attn_partial_floats(g));
+    if (need && (!ws || ws_bytes < need || !aligned(ws, kAlign))) return CLSA_ERR_WORKSPACE;
+    return from_hip(clsa::launch_sparse_attn(g, q, k_cache, v_cache, page_table, idx, n_sel, out,
+                                             lse, static_cast<float *>(ws),
+                                             static_cast<hipStream_t>(stream)));
+}
+
+clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const void *k_idx,
+                             const void *k_cache, const void *v_cache,
+                             const int32_t *page_table, const int32_t *seq_lens,
+                             const int32_t *q_pos, int32_t n_layers, const void *q_layers,
+                             void *out_layers, float *lse_layers, int32_t *idx, int32_t *n_sel,
+                             void *ws, size_t ws_bytes, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kIndex | kTopk | kAttn, &g));
+    if (n_layers < 0) return CLSA_ERR_INVALID_ARG;
+    CLSA_TRY(check_ptr(q_idx, 16));
+    CLSA_TRY(check_ptr(k_idx, 16));
+    CLSA_TRY(check_ptr(seq_lens, 4));
+    CLSA_TRY(check_ptr(idx, 4));
+    CLSA_TRY(check_ptr(n_sel, 4));
+    if (n_layers > 0) {
+        CLSA_TRY(check_ptr(k_cache, 16));
+        CLSA_TRY(check_ptr(v_cache, 16));
+        CLSA_TRY(check_ptr(q_layers, 16));
+        CLSA_TRY(check_ptr(out_layers, 16));
+        if (lse_layers) CLSA_TRY(check_ptr(lse_layers, 4));
+    }
+    CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
+    const size_t need = decode_ws_layout(g, nullptr, nullptr);
+    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
+    CLSA_TRY(check_topk_lds(g.max_len));
+
+    DecodeWs w;
+    decode_ws_layout(g, ws, &w);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool hook = g_hook.on;
+    CLSA_TRY(from_hip(clsa::launch_zero_u32(w.hist, (size_t)g.rows * clsa::kCoarseBins, st)));
+    if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+    CLSA_TRY(from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos,
+                                                w.scores, w.hist, st)));
+    if (hook && hipEventRecord(g_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
+    CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.hist, idx, n_sel, st)));
+    if (hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
+    const size_t q_stride = (size_t)g.rows * g.q_heads * 128;  // bf16 elements per layer
+    const size_t lse_stride = (size_t)g.rows * g.q_heads;
+    for (int l = 0; l < n_layers; ++l) {
+        const uint16_t *ql = static_cast<const uint16_t *>(q_layers) + l * q_stride;
+        uint16_t *ol = static_cast<uint16_t *>(out_layers) + l * q_stride;
+        float *lsel = lse_layers ? lse_layers + l * lse_stride : nullptr;
+        CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, idx, n_sel,
+                                                   ol, lsel, w.partials, st)));
+    }
+    if (hook && hipEventRecord(g_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
+    return CLSA_OK;
+}
+
+const char *clsa_status_string(clsa_status status) {
+    switch (status) {
+        case CLSA_OK: return "CLSA_OK";
+        case CLSA_ERR_INVALID_ARG: return "CLSA_ERR_INVALID_ARG";
+        case CLSA_ERR_UNSUPPORTED: return "CLSA_ERR_UNSUPPORTED";
+        case CLSA_ERR_WORKSPACE: return "CLSA_ERR_WORKSPACE";
+        case CLSA_ERR_HIP: return "CLSA_ERR_HIP";
+    }
+    return "CLSA_ERR_UNKNOWN";
+}
+
+clsa_status clsa_set_phase_events(void *const *events, int32_t n) {
+    if (n == 0) {
+        g_hook.on = false;
+        return CLSA_OK;
+    }
+    if (n != 4 || !events) return CLSA_ERR_INVALID_ARG;
+    for (int i = 0; i < 4; ++i) {
+        if (!events[i]) return CLSA_ERR_INVALID_ARG;
+        g_hook.ev[i] = static_cast<hipEvent_t>(events[i]);
+    }
+    g_hook.on = true;
+    return CLSA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Device helpers shared by the gfx950 kernels of libclsa.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace clsa {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load with the non-temporal hint (streamed once; keep it out of the caches).
+__device__ __forceinline__ uint4 load16_nt(const void *p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Four packed bf16 pairs (16 bytes) -> dot with four other pairs, fp32 accumulate.
+// v_dot2_f32_bf16: the two bf16 x bf16 products are exact in fp32.
+__device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float acc) {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.x),
+                                          __builtin_bit_cast(bf16x2, b.x), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.y),
+                                          __builtin_bit_cast(bf16x2, b.y), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.z),
+                                          __builtin_bit_cast(bf16x2, b.z), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.w),
+                                          __builtin_bit_cast(bf16x2, b.w), acc, false);
+    return acc;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (inputs here are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
+// -0.0 is mapped like +0.0 so that the two compare equal.
+__device__ __forceinline__ uint32_t score_key(float s) {
+    uint32_t u = __float_as_uint(s);
+    if ((u << 1) == 0u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ int clamp_len(int n, int max_len) {
+    return n < 0 ? 0 : (n > max_len ? max_len : n);
+}
+
+// Number of valid keys of query row (b, t).
+__device__ __forceinline__ int valid_keys(const int32_t *seq_lens, const int32_t *q_pos,
+                                          int causal, int b, int row, int max_len) {
+    int n = clamp_len(seq_lens[b], max_len);
+    if (causal) {
+        int lim = q_pos[row] + 1;
+        n = lim < n ? (lim < 0 ? 0 : lim) : n;
+    }
+    return n;
+}
+
+// Element offset of token j of sequence b in a cache with `row_elems` elements
+// per token: contiguous [B, max_len, ...] or paged [P, page, ...].
+__device__ __forceinline__ size_t token_offset(const int32_t *page_table, int page_shift,
+                                               int max_pages, int max_len, int b, int j,
+                                               int row_elems) {
+    if (page_shift < 0) return ((size_t)b * max_len + j) * row_elems;
+    const int page = page_table[(size_t)b * max_pages + (j >> page_shift)];
+    return (((size_t)page << page_shift) + (j & ((1 << page_shift) - 1))) * row_elems;
+}
+
+}  // namespace clsa

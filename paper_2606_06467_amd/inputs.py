@@ -170,15 +170,16 @@ def page_table_for(w: Workload, seed: int) -> np.ndarray:
     return pt
 
 
-def make_inputs(w: Workload, layers: Optional[List[int]] = None, seed_base: Optional[int] = None
-                ) -> Dict[str, np.ndarray]:
+def make_inputs(w: Workload, layers: Optional[List[int]] = None, seed_base: Optional[int] = None,
+                index_only: bool = False) -> Dict[str, np.ndarray]:
     """Host arrays for workload ``w``.
 
     Returns uint16 bfloat16 bits for ``q_idx [B,T,Hi,Di]``, ``k_idx``, ``k_cache``,
     ``v_cache`` (contiguous ``[B,max_len,H,D]`` or paged ``[P,page,H,D]``),
     ``q_layers [L,B,T,Hq,D]`` and int32 ``seq_lens [B]``, ``q_pos [B,T]`` (or
     None), ``page_table [B,max_pages]`` (or None).  ``layers`` restricts which
-    layer queries are generated (default: all ``n_layers``)."""
+    layer queries are generated (default: all ``n_layers``); ``index_only`` skips
+    K, V and the layer queries (they are then None)."""
     base = 1000 * w.wid if seed_base is None else seed_base
     B, T = w.batch, w.n_q
     out: Dict[str, np.ndarray] = {}
@@ -192,15 +193,18 @@ def make_inputs(w: Workload, layers: Optional[List[int]] = None, seed_base: Opti
         rows_shape = (B, w.max_len)
         out["page_table"] = None
     out["k_idx"] = normal_bf16(base + 2, rows_shape + (w.idx_heads, w.idx_dim), 1.0 / 8.0)
-    out["k_cache"] = normal_bf16(base + 3, rows_shape + (w.kv_heads, w.head_dim), 1.0)
-    out["v_cache"] = normal_bf16(base + 4, rows_shape + (w.kv_heads, w.head_dim), 1.0)
     if w.planted:
         _plant(w, out, base + 5)
-    ls = list(range(w.n_layers)) if layers is None else list(layers)
-    ql = np.empty((len(ls), B, T, w.q_heads, w.head_dim), dtype=np.uint16)
-    for i, l in enumerate(ls):
-        ql[i] = normal_bf16(base + 100 + l, (B, T, w.q_heads, w.head_dim), 1.0)
-    out["q_layers"] = ql
+    if index_only:
+        out["k_cache"] = out["v_cache"] = out["q_layers"] = None
+    else:
+        out["k_cache"] = normal_bf16(base + 3, rows_shape + (w.kv_heads, w.head_dim), 1.0)
+        out["v_cache"] = normal_bf16(base + 4, rows_shape + (w.kv_heads, w.head_dim), 1.0)
+        ls = list(range(w.n_layers)) if layers is None else list(layers)
+        ql = np.empty((len(ls), B, T, w.q_heads, w.head_dim), dtype=np.uint16)
+        for i, l in enumerate(ls):
+            ql[i] = normal_bf16(base + 100 + l, (B, T, w.q_heads, w.head_dim), 1.0)
+        out["q_layers"] = ql
     out["seq_lens"] = np.asarray(w.lens, dtype=np.int32)
     if w.causal:
         p0 = w.q_pos0 if w.q_pos0 is not None else [n - T for n in w.lens]

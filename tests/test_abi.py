@@ -1,0 +1,193 @@
+"""Host-only checks of the C-ABI library: it loads, exports every entry point that
+include/clsa.h declares, and rejects bad arguments before touching the GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "clsa.h")
+LIB = os.path.join(ROOT, "paper_2606_06467_amd", "libclsa.so")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2606_06467_amd import _build
+        _build.build()
+    from paper_2606_06467_amd import binding
+    return binding.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(clsa_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("clsa_index_scores", "clsa_topk", "clsa_sparse_attn", "clsa_decode_step",
+              "clsa_workspace_bytes", "clsa_status_string", "clsa_set_phase_events"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (clsa_\w+)", out))
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    for n in declared_functions():
+        assert hasattr(lib, n)
+
+
+def test_library_is_gfx950_only(lib, tmp_path):
+    """The device code bundled into the library targets gfx950 and nothing else."""
+    fb = tmp_path / "fatbin"
+    subprocess.run(["objcopy", f"--dump-section=.hip_fatbin={fb}", LIB, str(tmp_path / "x.so")],
+                   check=True)
+    out = subprocess.run(["/opt/rocm/llvm/bin/clang-offload-bundler", "--list", "--type=o",
+                          f"--input={fb}"], capture_output=True, text=True, check=True)
+    targets = [t for t in out.stdout.split() if "amdgcn" in t]
+    assert targets and all(t.endswith("gfx950") for t in targets), targets
+
+
+def test_status_strings(lib):
+    from paper_2606_06467_amd import binding as B
+    assert B.clsa_status_string(0) == "CLSA_OK"
+    assert B.clsa_status_string(-1) == "CLSA_ERR_INVALID_ARG"
+    assert B.clsa_status_string(-2) == "CLSA_ERR_UNSUPPORTED"
+    assert B.clsa_status_string(-3) == "CLSA_ERR_WORKSPACE"
+    assert B.clsa_status_string(-4) == "CLSA_ERR_HIP"
+    assert B.clsa_status_string(7) == "CLSA_ERR_UNKNOWN"
+
+
+# Fake, aligned, never-dereferenced device addresses: every call below must be
+# rejected by host validation before anything is enqueued.
+A = ctypes.c_void_p(0x10000)
+MIS = ctypes.c_void_p(0x10002)
+
+
+def _shape(**kw):
+    from paper_2606_06467_amd import binding as B
+    base = dict(batch=2, n_q=1, max_len=1024, top_k=64)
+    base.update(kw)
+    return B.make_shape(**base)
+
+
+def _index(lib, sh, q=A, k=A, pt=None, sl=A, qp=None, sc=A):
+    return lib.clsa_index_scores(ctypes.byref(sh), q, k, pt, sl, qp, sc, None)
+
+
+def _attn(lib, sh, q=A, k=A, v=A, pt=None, idx=A, ns=A, out=A, lse=None, ws=None, wsb=0):
+    return lib.clsa_sparse_attn(ctypes.byref(sh), q, k, v, pt, idx, ns, out, lse, ws, wsb, None)
+
+
+def _step(lib, sh, ws=None, wsb=0, L=2, **kw):
+    a = dict(q_idx=A, k_idx=A, k=A, v=A, pt=None, sl=A, qp=None, ql=A, ol=A, lse=None, idx=A, ns=A)
+    a.update(kw)
+    return lib.clsa_decode_step(ctypes.byref(sh), a["q_idx"], a["k_idx"], a["k"], a["v"], a["pt"],
+                                a["sl"], a["qp"], L, a["ql"], a["ol"], a["lse"], a["idx"], a["ns"],
+                                ws, wsb, None)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("batch", 0, -1), ("n_q", 0, -1), ("max_len", 0, -1), ("top_k", 0, -1), ("top_k", -5, -1),
+    ("idx_heads", 0, -1), ("causal", 2, -1), ("page_size", 48, -1), ("page_size", -64, -1),
+    ("idx_dim", 32, -2), ("top_k", 8193, -2), ("max_len", 262144 * 2, -2),
+])
+def test_index_rejects_bad_shapes(lib, field, value, code):
+    sh = _shape(**{field: value})
+    assert _index(lib, sh) == code
+
+
+def test_index_rejects_bad_pointers(lib):
+    sh = _shape()
+    assert _index(lib, sh, q=None) == -1
+    assert _index(lib, sh, q=MIS) == -1       # bf16 tensors need 16-byte alignment
+    assert _index(lib, sh, k=None) == -1
+    assert _index(lib, sh, sl=None) == -1
+    assert _index(lib, sh, sc=None) == -1
+    assert _index(lib, _shape(causal=True), qp=None) == -1              # causal needs q_pos
+    assert _index(lib, _shape(page_size=64, max_pages=16), pt=None) == -1
+    assert _index(lib, _shape(page_size=64, max_pages=15), pt=A) == -1  # table too narrow
+    assert _index(lib, _shape(page_size=64, max_pages=16, max_len=1000), pt=A) == -1
+    assert _index(lib, _shape(page_size=8, max_pages=128), pt=A) == -2
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=64), -2), (dict(q_heads=32, kv_heads=5), -1), (dict(q_heads=48, kv_heads=8), -2),
+    (dict(q_heads=20, kv_heads=4), None), (dict(softmax_scale=float("nan")), -1),
+    (dict(softmax_scale=float("inf")), -1),
+])
+def test_attn_rejects_bad_shapes(lib, kw, code):
+    from paper_2606_06467_amd import binding as B
+    sh = _shape(top_k=2048, **kw)
+    if code is None:
+        # supported shape: it needs a workspace (so the call below cannot reach a
+        # launch with the fake pointers) and fails only on the missing workspace
+        assert B.clsa_workspace_bytes(sh, B.CLSA_OP_ATTN) > 0
+        assert _attn(lib, sh, ws=None, wsb=0) == -3
+    else:
+        assert _attn(lib, sh, ws=None, wsb=0) == code
+
+
+def test_attn_pointer_and_workspace_checks(lib):
+    from paper_2606_06467_amd import binding as B
+    sh = _shape(top_k=2048)
+    need = B.clsa_workspace_bytes(sh, B.CLSA_OP_ATTN)
+    assert need > 0 and need % 256 == 0
+    assert _attn(lib, sh, q=MIS) == -1
+    assert _attn(lib, sh, out=None) == -1
+    assert _attn(lib, sh, lse=ctypes.c_void_p(0x10001)) == -1
+    assert _attn(lib, sh, ws=None, wsb=need) == -3
+    assert _attn(lib, sh, ws=A, wsb=need - 1) == -3
+    assert _attn(lib, sh, ws=ctypes.c_void_p(0x10010), wsb=need) == -3   # not 256-byte aligned
+
+
+def test_decode_step_checks(lib):
+    from paper_2606_06467_amd import binding as B
+    sh = _shape()
+    need = B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 2)
+    assert need >= 2 * 1024 * 4
+    assert _step(lib, sh, ws=None, wsb=need) == -3
+    assert _step(lib, sh, ws=A, wsb=need - 256) == -3
+    assert _step(lib, sh, ws=A, wsb=need, L=-1) == -1
+    assert _step(lib, sh, ws=A, wsb=need, q_idx=None) == -1
+    assert _step(lib, sh, ws=A, wsb=need, ql=None) == -1
+    assert _step(lib, sh, ws=A, wsb=need, idx=None) == -1
+    assert _step(lib, _shape(causal=True), ws=A, wsb=need) == -1
+    assert _step(lib, _shape(head_dim=96), ws=A, wsb=need) == -2
+
+
+def test_workspace_sizes(lib):
+    from paper_2606_06467_amd import binding as B
+    sh = _shape(batch=4, max_len=131072, top_k=2048)
+    assert B.clsa_workspace_bytes(sh, B.CLSA_OP_INDEX) == 0
+    assert B.clsa_workspace_bytes(sh, B.CLSA_OP_TOPK) == 0
+    dec = B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 16)
+    assert dec >= 4 * 131072 * 4 + 4 * 256 * 4
+    assert B.clsa_workspace_bytes(_shape(top_k=0), B.CLSA_OP_DECODE, 1) == 0
+    assert B.clsa_workspace_bytes(sh, 99) == 0
+
+
+def test_phase_event_hook_arguments(lib):
+    from paper_2606_06467_amd import binding as B
+    assert lib.clsa_set_phase_events(None, 0) == 0
+    assert lib.clsa_set_phase_events(None, 4) == -1
+    arr = (ctypes.c_void_p * 3)(A, A, A)
+    assert lib.clsa_set_phase_events(arr, 3) == -1
+    arr4 = (ctypes.c_void_p * 4)(A, A, None, A)
+    assert lib.clsa_set_phase_events(arr4, 4) == -1
+    assert lib.clsa_set_phase_events(None, 0) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    from paper_2606_06467_amd import binding as B
+    monkeypatch.setattr(B, "_lib_handle", None)
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        B.lib()

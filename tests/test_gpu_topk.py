@@ -1,0 +1,108 @@
+"""GPU parity of clsa_topk (Eq. 3, TopK) against the oracle.
+
+Both sides decide on the SAME float32 scores (from the seeded generator), so the
+index sets must agree bit for bit on every row, ties included (lowest index wins)."""
+import numpy as np
+import pytest
+
+import oracle as orc
+from paper_2606_06467_amd import inputs
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(scores, k, lens, q_pos=None):
+    import torch
+    from paper_2606_06467_amd import binding as B
+    Bt, T, N = scores.shape
+    sh = B.make_shape(batch=Bt, n_q=T, max_len=N, top_k=k, causal=q_pos is not None)
+    sc = torch.from_numpy(np.ascontiguousarray(scores)).cuda()
+    sl = torch.from_numpy(np.asarray(lens, np.int32)).cuda()
+    qp = None if q_pos is None else torch.from_numpy(np.asarray(q_pos, np.int32)).cuda()
+    idx = torch.full((Bt, T, k), -7, dtype=torch.int32, device="cuda")
+    ns = torch.full((Bt, T), -7, dtype=torch.int32, device="cuda")
+    B.clsa_topk(sh, sc, sl, qp, idx, ns)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), ns.cpu().numpy()
+
+
+def _check(scores, k, lens, q_pos=None, what=""):
+    Bt, T, N = scores.shape
+    sh = orc.shape(Bt, T, N, k, causal=q_pos is not None)
+    oi, on = orc.topk(sh, scores, np.asarray(lens, np.int32), q_pos)
+    gi, gn = _run(scores, k, lens, q_pos)
+    np.testing.assert_array_equal(gn, on)
+    bad = [r for r in np.ndindex(on.shape) if not np.array_equal(gi[r], oi[r])]
+    assert not bad, f"{what}: {len(bad)} rows differ, first {bad[:3]}"
+    U.log(f"  topk {what}: {Bt * T} rows bit-exact")
+
+
+def test_gaussian_rows_128k():
+    s = inputs.random_scores(71, 4, 131072)[:, None, :]
+    _check(s, 2048, [131072] * 4, what="gaussian 4x128K k=2048")
+
+
+@pytest.mark.parametrize("k", [1, 7, 64, 511, 2048, 8192])
+def test_various_k(k):
+    s = inputs.random_scores(72 + k, 3, 20000)[:, None, :]
+    _check(s, k, [20000, 8191, 3000], what=f"k={k}")
+
+
+def test_heavy_ties_quantised():
+    s = inputs.random_scores(73, 5, 50000, levels=8)[:, None, :]
+    _check(s, 1000, [50000] * 5, what="8 levels")
+
+
+def test_scattered_ties():
+    s = inputs.random_scores(74, 4, 70000, ties=0.5)[:, None, :]
+    _check(s, 2048, [70000, 69999, 12345, 2049], what="scattered ties")
+
+
+def test_all_equal_row_overflows_candidate_list():
+    """Every key falls in one coarse bin: the LDS candidate list overflows and the
+    kernel must fall back to re-reading the row."""
+    s = np.full((2, 1, 40000), 0.375, np.float32)
+    s[1, 0, ::3] = -0.0
+    s[1, 0, 1::3] = 0.0
+    _check(s, 2048, [40000, 40000], what="all equal / signed zeros")
+
+
+def test_narrow_band_many_candidates():
+    g = np.random.default_rng(75)
+    s = (1.0 + g.random((3, 1, 100000), dtype=np.float32) * 0.5).astype(np.float32)
+    _check(s, 4096, [100000] * 3, what="values in [1,1.5)")
+
+
+def test_infinities_and_extremes():
+    s = inputs.random_scores(76, 2, 9000)[:, None, :]
+    s[0, 0, 10] = np.inf
+    s[0, 0, 20] = -np.inf
+    s[1, 0, :100] = 3.4e38
+    s[1, 0, 100:200] = -3.4e38
+    s[1, 0, 200:300] = 1e-45
+    _check(s, 150, [9000, 9000], what="inf / extremes")
+
+
+def test_short_and_empty_rows():
+    s = inputs.random_scores(77, 4, 5000)[:, None, :]
+    _check(s, 2048, [0, 1, 2048, 2047], what="short rows")
+
+
+def test_causal_rows():
+    s = inputs.random_scores(78, 3, 6000)
+    q_pos = np.array([[0, 100, 2047, 2048, 2049, 5999]], np.int32)
+    s6 = np.stack([s[0]] * 6)[None]            # one sequence, 6 query rows
+    _check(s6, 2048, [6000], q_pos=q_pos, what="causal")
+
+
+def test_max_len_262144():
+    s = inputs.random_scores(79, 2, 262144)[:, None, :]
+    _check(s, 8192, [262144, 200000], what="262144 keys k=8192")
+
+
+def test_many_rows_prefill_like():
+    T = 256
+    s = inputs.random_scores(80, T, 16384)[None]
+    q_pos = (16384 - T + np.arange(T, dtype=np.int32))[None]
+    _check(s, 2048, [16384], q_pos=q_pos, what="256 causal rows")
