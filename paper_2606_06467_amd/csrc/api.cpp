@@ -92,7 +92,7 @@ clsa_status check_common(const clsa_shape *s, const int32_t *page_table, const i
 }
 
 // Device limit on dynamic LDS per workgroup, cached per device.
-clsa_status check_topk_lds(int max_len) {
+clsa_status check_topk_lds(const Geometry &g) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return CLSA_ERR_HIP;
     static int cached_dev = -1, cached_lds = 0;
@@ -103,28 +103,89 @@ clsa_status check_topk_lds(int max_len) {
         cached_lds = v;
         cached_dev = dev;
     }
-    return clsa::topk_lds_bytes(max_len) + 1024 <= (size_t)cached_lds ? CLSA_OK
+    return clsa::topk_lds_bytes(g) + 1024 <= (size_t)cached_lds ? CLSA_OK
                                                                         : CLSA_ERR_UNSUPPORTED;
 }
 
-struct DecodeWs {
-    float *scores;
-    uint32_t *hist;
-    float *partials;
+// Carves 256-byte aligned sub-buffers out of a workspace; with base == nullptr
+// it only adds up the sizes.
+struct Carver {
+    char *base;
+    size_t off = 0;
+    template <class T>
+    T *take(size_t count) {
+        T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += align_up(sizeof(T) * count);
+        return count ? p : nullptr;
+    }
 };
 
-size_t decode_ws_layout(const Geometry &g, void *base, DecodeWs *out) {
-    size_t off = 0;
-    const size_t scores = align_up(sizeof(float) * (size_t)g.rows * g.max_len);
-    const size_t hist = align_up(sizeof(uint32_t) * (size_t)g.rows * clsa::kCoarseBins);
-    const size_t part = align_up(sizeof(float) * clsa::attn_partial_floats(g));
-    if (out) {
-        char *p = static_cast<char *>(base);
-        out->scores = reinterpret_cast<float *>(p + off);
-        out->hist = reinterpret_cast<uint32_t *>(p + off + scores);
-        out->partials = part ? reinterpret_cast<float *>(p + off + scores + hist) : nullptr;
+struct TopkWs {
+    clsa::TopkBuffers buf{};
+    uint32_t *zero = nullptr;  // start of the region to clear before use
+    size_t zero_count = 0;
+};
+
+// Multi-workgroup top-k state: [hist | counters] (cleared per call), bitmaps, candidates.
+void carve_topk(const Geometry &g, Carver &c, TopkWs &t) {
+    if (!clsa::topk_uses_wide(g)) return;
+    const clsa::TopkWideLayout L = clsa::topk_wide_layout(g);
+    t.zero_count = L.hist_u32 + L.counters_u32;
+    t.zero = c.take<uint32_t>(t.zero_count);
+    t.buf.hist = t.zero;
+    t.buf.counters = t.zero ? t.zero + L.hist_u32 : nullptr;
+    t.buf.bitmaps = c.take<uint32_t>(2 * L.bitmap_u32);
+    t.buf.cands = c.take<uint32_t>(2 * L.cand_u32);
+}
+
+struct AttnWs {
+    float *partials = nullptr;
+};
+
+void carve_attn(const Geometry &g, Carver &c, AttnWs &w) {
+    w.partials = c.take<float>(clsa::attn_partial_floats(g));  // none with one split
+}
+
+struct DecodeWs {
+    float *scores = nullptr;
+    uint32_t *zero = nullptr;  // [coarse histogram | top-k counters], cleared per step
+    size_t zero_count = 0;
+    clsa::TopkBuffers topk{};
+    float *partials = nullptr;
+};
+
+size_t carve_decode(const Geometry &g, void *base, DecodeWs &w) {
+    Carver c{static_cast<char *>(base)};
+    w.scores = c.take<float>((size_t)g.rows * g.max_len);
+    const size_t hist = (size_t)g.rows * clsa::kCoarseBins;
+    const size_t counters = (size_t)g.rows * 2;
+    w.zero_count = hist + counters;
+    w.zero = c.take<uint32_t>(w.zero_count);
+    if (w.zero) {
+        w.topk.hist = w.zero;
+        w.topk.counters = w.zero + hist;
     }
-    return scores + hist + part;
+    if (clsa::topk_uses_wide(g)) {
+        const clsa::TopkWideLayout L = clsa::topk_wide_layout(g);
+        w.topk.bitmaps = c.take<uint32_t>(2 * L.bitmap_u32);
+        w.topk.cands = c.take<uint32_t>(2 * L.cand_u32);
+    }
+    w.partials = c.take<float>(clsa::attn_partial_floats(g));
+    return c.off;
+}
+
+size_t topk_ws_bytes(const Geometry &g) {
+    Carver c{nullptr};
+    TopkWs t;
+    carve_topk(g, c, t);
+    return c.off;
+}
+
+size_t attn_ws_bytes(const Geometry &g) {
+    Carver c{nullptr};
+    AttnWs w;
+    carve_attn(g, c, w);
+    return c.off;
 }
 
 clsa_status from_hip(hipError_t e) { return e == hipSuccess ? CLSA_OK : CLSA_ERR_HIP; }
@@ -134,19 +195,22 @@ clsa_status from_hip(hipError_t e) { return e == hipSuccess ? CLSA_OK : CLSA_ERR
 extern "C" {
 
 size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layers) {
+    (void)n_layers;  // layers run one after another and reuse the same buffers
     Geometry g;
     switch (op) {
         case CLSA_OP_INDEX:
             return 0;
         case CLSA_OP_TOPK:
-            return 0;
+            if (check_shape(shape, kTopk, &g) != CLSA_OK) return 0;
+            return topk_ws_bytes(g);
         case CLSA_OP_ATTN:
             if (check_shape(shape, kAttn, &g) != CLSA_OK) return 0;
-            return align_up(sizeof(float) * clsa::attn_partial_floats(g));
-        case CLSA_OP_DECODE:
-            (void)n_layers;
+            return attn_ws_bytes(g);
+        case CLSA_OP_DECODE: {
             if (check_shape(shape, kIndex | kTopk | kAttn, &g) != CLSA_OK) return 0;
-            return decode_ws_layout(g, nullptr, nullptr);
+            DecodeWs w;
+            return carve_decode(g, nullptr, w);
+        }
         default:
             return 0;
     }
@@ -169,8 +233,6 @@ clsa_status clsa_index_scores(const clsa_shape *shape, const void *q_idx, const 
 clsa_status clsa_topk(const clsa_shape *shape, const float *scores, const int32_t *seq_lens,
                       const int32_t *q_pos, int32_t *idx, int32_t *n_sel, void *ws,
                       size_t ws_bytes, void *stream) {
-    (void)ws;
-    (void)ws_bytes;
     Geometry g;
     CLSA_TRY(check_shape(shape, kTopk, &g));
     CLSA_TRY(check_ptr(scores, 4));
@@ -178,9 +240,15 @@ clsa_status clsa_topk(const clsa_shape *shape, const float *scores, const int32_
     CLSA_TRY(check_ptr(idx, 4));
     CLSA_TRY(check_ptr(n_sel, 4));
     CLSA_TRY(check_common(shape, nullptr, q_pos, true, false));
-    CLSA_TRY(check_topk_lds(g.max_len));
-    return from_hip(clsa::launch_topk(g, scores, seq_lens, q_pos, nullptr, idx, n_sel,
-                                      static_cast<hipStream_t>(stream)));
+    const size_t need = topk_ws_bytes(g);
+    if (need && (!ws || ws_bytes < need || !aligned(ws, kAlign))) return CLSA_ERR_WORKSPACE;
+    CLSA_TRY(check_topk_lds(g));
+    Carver c{static_cast<char *>(ws)};
+    TopkWs t;
+    carve_topk(g, c, t);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    CLSA_TRY(from_hip(clsa::launch_zero_u32(t.zero, t.zero_count, st)));
+    return from_hip(clsa::launch_topk(g, scores, seq_lens, q_pos, t.buf, false, idx, n_sel, st));
 }
 
 clsa_status clsa_sparse_attn(const clsa_shape *shape, const void *q, const void *k_cache,
@@ -197,11 +265,13 @@ clsa_status clsa_sparse_attn(const clsa_shape *shape, const void *q, const void 
     CLSA_TRY(check_ptr(out, 16));
     if (lse) CLSA_TRY(check_ptr(lse, 4));
     CLSA_TRY(check_common(shape, page_table, nullptr, false, true));
-    const size_t need = align_up(sizeof(float) * clsa::attn_partial_floats(g));
+    const size_t need = attn_ws_bytes(g);
     if (need && (!ws || ws_bytes < need || !aligned(ws, kAlign))) return CLSA_ERR_WORKSPACE;
+    Carver c{static_cast<char *>(ws)};
+    AttnWs w;
+    carve_attn(g, c, w);
     return from_hip(clsa::launch_sparse_attn(g, q, k_cache, v_cache, page_table, idx, n_sel, out,
-                                             lse, static_cast<float *>(ws),
-                                             static_cast<hipStream_t>(stream)));
+                                             lse, w.partials, static_cast<hipStream_t>(stream)));
 }
 
 clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const void *k_idx,
@@ -226,20 +296,21 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
         if (lse_layers) CLSA_TRY(check_ptr(lse_layers, 4));
     }
     CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
-    const size_t need = decode_ws_layout(g, nullptr, nullptr);
-    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
-    CLSA_TRY(check_topk_lds(g.max_len));
-
     DecodeWs w;
-    decode_ws_layout(g, ws, &w);
+    const size_t need = carve_decode(g, nullptr, w);
+    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
+    CLSA_TRY(check_topk_lds(g));
+
+    carve_decode(g, ws, w);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool hook = g_hook.on;
-    CLSA_TRY(from_hip(clsa::launch_zero_u32(w.hist, (size_t)g.rows * clsa::kCoarseBins, st)));
+    CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
     if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
     CLSA_TRY(from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos,
-                                                w.scores, w.hist, st)));
+                                                w.scores, w.topk.hist, st)));
     if (hook && hipEventRecord(g_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
-    CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.hist, idx, n_sel, st)));
+    CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, true, idx, n_sel,
+                                        st)));
     if (hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
     const size_t q_stride = (size_t)g.rows * g.q_heads * 128;  // bf16 elements per layer
     const size_t lse_stride = (size_t)g.rows * g.q_heads;

@@ -22,32 +22,48 @@ struct Geometry {
 
 // Tokens scored by one indexer workgroup (4 waves x 32 tokens).
 constexpr int kIndexTile = 128;
-// Bins of the coarse score histogram made by the indexer (top 8 key bits).
-constexpr int kCoarseBins = 256;
-// Selected tokens handled by one sparse-attention workgroup.
-constexpr int kAttnSplit = 64;
-// Candidate list capacity of the per-row top-k kernel (entries of 8 bytes).
+// Bins of the coarse score histogram made by the indexer (top 11 key bits,
+// i.e. quarter-octave bins of the score).
+constexpr int kCoarseShift = 21;  // top 11 key bits: sign, exponent, 2 mantissa bits
+constexpr int kCoarseBins = 1 << (32 - kCoarseShift);
+// Candidate list capacity of the per-row top-k kernel (LDS entries of 8 bytes).
 constexpr int kTopkCandCap = 8192;
+// Rows up to which the top-k splits each row over many workgroups.
+constexpr int kTopkWideMaxRows = 128;
+// Candidate list capacity per row of the multi-workgroup top-k (global memory).
+constexpr int kTopkWideCandCap = 16384;
 
 __host__ __device__ inline int div_up(int a, int b) { return (a + b - 1) / b; }
 
 // ---- index_decode.hip ----
+// coarse_hist: [rows, kCoarseBins], zero on entry, or NULL for no histogram.
 hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void *k_idx,
                                const int32_t *page_table, const int32_t *seq_lens,
                                const int32_t *q_pos, float *scores, uint32_t *coarse_hist,
                                hipStream_t stream);
 
 // ---- topk.hip ----
-// coarse_hist: [rows, kCoarseBins] made by launch_index_scores, or NULL to have
-// the top-k kernel build it itself.
+struct TopkWideLayout {
+    int words_max, cand_cap;
+    size_t hist_u32, counters_u32, bitmap_u32, cand_u32;  // per buffer, all rows
+};
+struct TopkBuffers {
+    uint32_t *hist;      // [rows, kCoarseBins]; zero on entry unless already filled
+    uint32_t *counters;  // [rows, 2]; zero on entry (wide path), left zero
+    uint32_t *bitmaps;   // 2 x bitmap_u32 (wide path)
+    uint32_t *cands;     // 2 x cand_u32 (wide path)
+};
+bool topk_uses_wide(const Geometry &g);
+TopkWideLayout topk_wide_layout(const Geometry &g);
+size_t topk_lds_bytes(const Geometry &g);  // LDS per workgroup of the largest top-k kernel
+// hist_ready: buf.hist already holds the coarse histogram of these scores.
 hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *seq_lens,
-                       const int32_t *q_pos, const uint32_t *coarse_hist, int32_t *idx,
-                       int32_t *n_sel, hipStream_t stream);
+                       const int32_t *q_pos, const TopkBuffers &buf, bool hist_ready,
+                       int32_t *idx, int32_t *n_sel, hipStream_t stream);
 hipError_t launch_zero_u32(uint32_t *p, size_t n, hipStream_t stream);
-size_t topk_lds_bytes(int max_len);
 
 // ---- sparse_attn.hip ----
-size_t attn_partial_floats(const Geometry &g);
+size_t attn_partial_floats(const Geometry &g);  // 0 when one split per (row, KV head)
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,

@@ -29,6 +29,33 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float acc) {
     return acc;
 }
 
+// Transpose-reduction across lanes.  Each lane holds CNT partial values; at the
+// exchange with lane ^ M it keeps the half selected by (lane & M) and adds the
+// partner's copy of that half, for M, M/2, ..., MSTOP.  Once a single value is
+// left the remaining exchanges are plain sums.  With CNT = 2^s values and s
+// halving steps, lane L ends with value index (L's step bits, high to low) of
+// the original CNT, summed over every lane the steps visited.  All sizes are
+// compile-time so that every register index stays static.
+template <int CNT, int M, int MSTOP, int NV>
+__device__ __forceinline__ void transpose_reduce(float (&p)[NV], int lane) {
+    if constexpr (M >= MSTOP) {
+        if constexpr (CNT > 1) {
+            constexpr int H = CNT / 2;
+            const bool up = (lane & M) != 0;
+#pragma unroll
+            for (int v = 0; v < H; ++v) {
+                const float keep = up ? p[v + H] : p[v];
+                const float send = up ? p[v] : p[v + H];
+                p[v] = keep + __shfl_xor(send, M);
+            }
+            transpose_reduce<H, M / 2, MSTOP, NV>(p, lane);
+        } else {
+            p[0] += __shfl_xor(p[0], M);
+            transpose_reduce<1, M / 2, MSTOP, NV>(p, lane);
+        }
+    }
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 

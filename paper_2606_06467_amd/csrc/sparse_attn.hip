@@ -5,8 +5,11 @@
 // One workgroup (4 waves) = one (query row, KV head g, split of S).  A split is
 // a run of 64-token chunks of the row's index list.  Per chunk:
 //   * each 16-lane quarter-wave gathers one selected token's 256-byte K row and
-//     256-byte V row of head g (16 bytes per lane), 4 chunks-rounds x 4 waves x
-//     4 quarters = 64 tokens, all loads issued before any math;
+//     256-byte V row of head g (16 bytes per lane); 4 rounds x 4 waves x 4
+//     quarters = 64 tokens.  Index loads, page-table loads and the K/V loads
+//     are each issued as one unconditional batch (positions past the end are
+//     clamped and masked afterwards), so a workgroup waits for memory about
+//     three times instead of once per token;
 //   * the G query heads of the GQA group share those rows: each lane dots its
 //     8 key values with the matching 8 values of every head (v_dot2_f32_bf16),
 //     a transpose-reduction over the 16 lanes leaves one (head, token) logit
@@ -15,10 +18,12 @@
 //     updates the running max / denominator and rescales its accumulators
 //     (online softmax), so a split of any length needs one pass;
 //   * each lane accumulates weight x V for its 8 dimensions and G heads.
-// At the end the accumulators are reduced over lanes and waves in LDS.  With
-// one split the workgroup writes the bf16 output and lse itself; otherwise it
-// writes fp32 partials (o, m, l) and a merge kernel combines the splits with
-// the exact log-sum-exp rule.
+// The accumulators are then reduced over lanes and waves in LDS.  With one
+// split the workgroup writes the bf16 output and lse itself.  Otherwise it
+// writes fp32 partials (o, m, l) and attn_merge_kernel combines the splits with
+// the exact log-sum-exp rule.  The merge is a second launch rather than a
+// "last workgroup merges" ticket: the agent-scope release fence such a ticket
+// needs writes back the whole L2 of the XCD from every workgroup on this chip.
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -27,6 +32,7 @@ namespace clsa {
 constexpr int kHeadDim = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kMaxSplits = 128;  // top_k <= 8192 in 64-token chunks
 
 struct AttnArgs {
     const uint16_t *q;
@@ -35,19 +41,19 @@ struct AttnArgs {
     const int32_t *page_table;
     const int32_t *idx;
     const int32_t *n_sel;
-    uint16_t *out;      // direct output (splits == 1)
-    float *lse;         // direct lse (splits == 1), may be null
-    float *part_o;      // [rows, Hq, splits, 128]
-    float *part_ml;     // [rows, Hq, splits, 2]
+    uint16_t *out;
+    float *lse;          // may be null
+    float *part_o;       // [rows, Hq, splits, 128]
+    float *part_ml;      // [rows, Hq, splits, 2]
     int n_q, max_len, page_shift, max_pages, top_k, kv_heads, q_heads, splits, chunks_per_split;
-    float scale_log2;   // softmax_scale * log2(e)
+    float scale_log2;    // softmax_scale * log2(e)
 };
 
 __host__ __device__ constexpr int pow2_at_least(int x) {
     return x <= 1 ? 1 : 2 * pow2_at_least((x + 1) / 2);
 }
 
-template <int G>
+template <int G, bool PAGED>
 __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
     constexpr int NO = pow2_at_least(8 * G);   // accumulators per lane before the reduction
@@ -61,14 +67,33 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     const int rg = blockIdx.x / a.splits;
     const int g = rg % a.kv_heads, row = rg / a.kv_heads;
     const int b = row / a.n_q;
-    const int n = min(max(a.n_sel[row], 0), a.top_k);
-    const int tok_begin = split * a.chunks_per_split * 64;
-    const int Hq = a.kv_heads * G;
+    const int Hq = a.q_heads;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int qq = lane >> 4, sub = lane & 15;
-    if (tok_begin >= n && !(split == 0 && a.splits == 1)) return;  // uniform
-    const int tok_end = min(n, tok_begin + a.chunks_per_split * 64);
+    const int span = a.chunks_per_split * 64;
+    const int tok_begin = split * span;
     const int row_elems = a.kv_heads * kHeadDim;
+    const int32_t *sel = a.idx + (size_t)row * a.top_k;
+
+    // Index loads of the first chunk do not wait for n_sel: the index list has
+    // top_k entries (padding included), so any position below top_k is readable.
+    int jpre[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        jpre[i] = sel[min(tok_begin + i * 16 + wave * 4 + qq, a.top_k - 1)];
+    const int n = min(max(a.n_sel[row], 0), a.top_k);
+    const int nsplit = div_up(n, span);  // splits that hold tokens
+
+    if (n == 0) {  // empty index set: output 0, lse -inf
+        if (split == 0) {
+            for (int e = tid; e < G * kHeadDim; e += 256)
+                a.out[((size_t)row * Hq + g * G) * kHeadDim + e] = 0;
+            if (a.lse && tid < G) a.lse[(size_t)row * Hq + g * G + tid] = -INFINITY;
+        }
+        return;
+    }
+    if (split >= nsplit) return;  // uniform; the merge only reads the first nsplit splits
+    const int tok_end = min(n, tok_begin + span);
 
     uint4 qv[G];
 #pragma unroll
@@ -85,24 +110,35 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.0f;
 
-    const int32_t *sel = a.idx + (size_t)row * a.top_k;
     for (int c0 = tok_begin; c0 < tok_end; c0 += 64) {
+        int jr[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) jr[i] = min(max(jpre[i], 0), a.max_len - 1);  // -1 pad -> row 0
+        uint32_t trow[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (PAGED) {
+                const int page = a.page_table[(size_t)b * a.max_pages + (jr[i] >> a.page_shift)];
+                trow[i] = ((uint32_t)page << a.page_shift) + (jr[i] & ((1 << a.page_shift) - 1));
+            } else {
+                trow[i] = (uint32_t)b * a.max_len + jr[i];
+            }
+        }
         uint4 kr[4], vr[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int t = c0 + i * 16 + wave * 4 + qq;
-            if (t < tok_end) {
-                const int j = min(max(sel[t], 0), a.max_len - 1);
-                const size_t off = token_offset(a.page_table, a.page_shift, a.max_pages,
-                                                a.max_len, b, j, row_elems) +
-                                   (size_t)g * kHeadDim + sub * 8;
-                kr[i] = *reinterpret_cast<const uint4 *>(a.k + off);
-                vr[i] = *reinterpret_cast<const uint4 *>(a.v + off);
-            } else {
-                kr[i] = make_uint4(0u, 0u, 0u, 0u);
-                vr[i] = make_uint4(0u, 0u, 0u, 0u);
-            }
+            const size_t off = (size_t)trow[i] * row_elems + (size_t)g * kHeadDim + sub * 8;
+            kr[i] = *reinterpret_cast<const uint4 *>(a.k + off);
+            vr[i] = *reinterpret_cast<const uint4 *>(a.v + off);
         }
+        // prefetch the next chunk's indices (clamped, so always readable)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            jpre[i] = sel[min(c0 + 64 + i * 16 + wave * 4 + qq, a.top_k - 1)];
+        // All K and V gathers of the chunk are in flight before any math (without
+        // this the scheduler sinks the V loads below the logits, which costs a
+        // second memory round trip per chunk).
+        __builtin_amdgcn_sched_barrier(0);
         // logits: value index i*G + h, transpose-reduced over the 16 lanes of the quarter
         float p[NV];
 #pragma unroll
@@ -111,27 +147,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int h = 0; h < G; ++h) p[i * G + h] = dot8_bf16(kr[i], qv[h], 0.0f);
-        {
-            int cnt = NV;
-#pragma unroll
-            for (int m = 8; m >= 1; m >>= 1) {
-                if (cnt > 1) {
-                    const int hlf = cnt / 2;
-                    const bool up = sub & m;
-#pragma unroll
-                    for (int v = 0; v < NV / 2; ++v) {
-                        if (v < hlf) {
-                            const float keep = up ? p[v + hlf] : p[v];
-                            const float send = up ? p[v] : p[v + hlf];
-                            p[v] = keep + __shfl_xor(send, m);
-                        }
-                    }
-                    cnt = hlf;
-                } else {
-                    p[0] += __shfl_xor(p[0], m);
-                }
-            }
-        }
+        transpose_reduce<NV, 8, 1, NV>(p, sub);
         // lane `sub` now holds value indices [sub*NV/16, sub*NV/16 + NV/16) (NV >= 16)
         // or index sub / (16/NV) (NV < 16).
         constexpr int PER = NV >= 16 ? NV / 16 : 1;
@@ -141,8 +157,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             if (orig < 4 * G) {
                 const int i = orig / G, h = orig - i * G;
                 const int tl = i * 16 + wave * 4 + qq;
-                const bool ok = c0 + tl < tok_end;
-                zs[h][tl] = ok ? p[v] * a.scale_log2 : -INFINITY;
+                zs[h][tl] = c0 + tl < tok_end ? p[v] * a.scale_log2 : -INFINITY;
             }
         }
         __syncthreads();
@@ -153,8 +168,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int m = 32; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
             const float m_old = s_ml[h][0];
-            const float m_new = fmaxf(m_old, mx);
-            const float w = exp2f(z - m_new);   // z = -inf -> 0
+            const float m_new = fmaxf(m_old, mx);   // finite: the chunk has a valid token
+            const float w = exp2f(z - m_new);        // z = -inf -> 0
             float sum = w;
 #pragma unroll
             for (int m = 32; m >= 1; m >>= 1) sum += __shfl_xor(sum, m);
@@ -183,7 +198,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             vf[6] = bf16_lo(vr[i].w); vf[7] = bf16_hi(vr[i].w);
 #pragma unroll
             for (int h = 0; h < G; ++h) {
-                const float w = zs[h][tl];
+                const float w = zs[h][tl];  // 0 for positions past the end
 #pragma unroll
                 for (int d = 0; d < 8; ++d) acc[h][d] = fmaf(w, vf[d], acc[h][d]);
             }
@@ -199,23 +214,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int d = 0; d < 8; ++d) o[h * 8 + d] = acc[h][d];
-    {
-        int cnt = NO;
-#pragma unroll
-        for (int m = 32; m >= 16; m >>= 1) {
-            const int hlf = cnt / 2;
-            const bool up = lane & m;
-#pragma unroll
-            for (int v = 0; v < NO / 2; ++v) {
-                if (v < hlf) {
-                    const float keep = up ? o[v + hlf] : o[v];
-                    const float send = up ? o[v] : o[v + hlf];
-                    o[v] = keep + __shfl_xor(send, m);
-                }
-            }
-            cnt = hlf;
-        }
-    }
+    transpose_reduce<NO, 32, 16, NO>(o, lane);
     // lane (qq, sub) holds value indices [qq*NO/4, qq*NO/4 + NO/4); index = h*8 + d
 #pragma unroll
     for (int v = 0; v < NO / 4; ++v) {
@@ -226,52 +225,78 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         }
     }
     __syncthreads();
+    if (a.splits == 1) {
+        for (int e = tid; e < G * kHeadDim; e += 256) {
+            const int h = e / kHeadDim, dim = e - h * kHeadDim;
+            const float sum = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+            const int hq = g * G + h;
+            const float l = s_ml[h][1];
+            a.out[((size_t)row * Hq + hq) * kHeadDim + dim] =
+                (uint16_t)f32_to_bf16_bits(sum / l);
+            if (a.lse && dim == 0) a.lse[(size_t)row * Hq + hq] = (s_ml[h][0] + log2f(l)) * kLn2;
+        }
+        return;
+    }
+    const size_t base = ((size_t)row * Hq + g * G) * a.splits;  // slot of (head g*G, split 0)
     for (int e = tid; e < G * kHeadDim; e += 256) {
         const int h = e / kHeadDim, dim = e - h * kHeadDim;
-        const float sum = red[0][e] + red[1][e] + red[2][e] + red[3][e];
-        const int hq = g * G + h;
-        if (a.splits == 1) {
-            const float l = s_ml[h][1];
-            const float val = l > 0.0f ? sum / l : 0.0f;
-            a.out[((size_t)row * Hq + hq) * kHeadDim + dim] = (uint16_t)f32_to_bf16_bits(val);
-            if (a.lse && dim == 0)
-                a.lse[(size_t)row * Hq + hq] = l > 0.0f ? (s_ml[h][0] + log2f(l)) * kLn2 : -INFINITY;
-        } else {
-            const size_t slot = ((size_t)row * Hq + hq) * a.splits + split;
-            a.part_o[slot * kHeadDim + dim] = sum;
-            if (dim == 0) {
-                a.part_ml[slot * 2] = s_ml[h][0];
-                a.part_ml[slot * 2 + 1] = s_ml[h][1];
-            }
+        const size_t slot = base + (size_t)h * a.splits + split;
+        a.part_o[slot * kHeadDim + dim] = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+        if (dim == 0) {
+            a.part_ml[slot * 2] = s_ml[h][0];
+            a.part_ml[slot * 2 + 1] = s_ml[h][1];
         }
     }
 }
 
-// Combine the splits of one (row, query head): one wave, two dimensions per lane.
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a, int rows) {
+// Combine the splits of one (row, KV head): the G heads' partials (o, m, l) are
+// weighted by 2^(m_s - max m) and normalised by the weighted denominators.
+template <int G>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+    __shared__ float s_w[G][kMaxSplits];
+    __shared__ float s_inv[G], s_lse[G];
+    const int rg = blockIdx.x;
+    const int g = rg % a.kv_heads, row = rg / a.kv_heads;
     const int Hq = a.q_heads;
-    const int unit = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (unit >= rows * Hq) return;
-    const int lane = threadIdx.x & 63;
-    const int row = unit / Hq, hq = unit - row * Hq;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int n = min(max(a.n_sel[row], 0), a.top_k);
-    const int nsplit = min(a.splits, div_up(n, a.chunks_per_split * 64));
-    const size_t base = ((size_t)row * Hq + hq) * a.splits;
-    float mx = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.part_ml[(base + s) * 2]);
-    float l = 0.0f, o0 = 0.0f, o1 = 0.0f;
-    for (int s = 0; s < nsplit; ++s) {
-        const float w = exp2f(a.part_ml[(base + s) * 2] - mx);
-        l += w * a.part_ml[(base + s) * 2 + 1];
-        const float2 po = *reinterpret_cast<const float2 *>(a.part_o + (base + s) * kHeadDim + lane * 2);
-        o0 = fmaf(w, po.x, o0);
-        o1 = fmaf(w, po.y, o1);
+    const int nsplit = div_up(n, a.chunks_per_split * 64);
+    if (nsplit == 0) return;  // the attention kernel wrote the empty-set result
+    const size_t base = ((size_t)row * Hq + g * G) * a.splits;
+    for (int x = tid; x < G * nsplit; x += 256) {
+        const int h = x / nsplit, s = x - h * nsplit;
+        s_w[h][s] = a.part_ml[(base + (size_t)h * a.splits + s) * 2];
     }
-    const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-    const uint32_t packed = f32_to_bf16_bits(o0 * inv) | (f32_to_bf16_bits(o1 * inv) << 16);
-    *reinterpret_cast<uint32_t *>(a.out + ((size_t)row * Hq + hq) * kHeadDim + lane * 2) = packed;
-    if (a.lse && lane == 0)
-        a.lse[(size_t)row * Hq + hq] = l > 0.0f ? (mx + log2f(l)) * kLn2 : -INFINITY;
+    __syncthreads();
+    for (int h = wave; h < G; h += 4) {  // per head: max over splits, weights, denominator
+        float mx = -INFINITY;
+        for (int s = lane; s < nsplit; s += 64) mx = fmaxf(mx, s_w[h][s]);
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
+        float l = 0.0f;
+        for (int s = lane; s < nsplit; s += 64) {
+            const float w = exp2f(s_w[h][s] - mx);
+            l += w * a.part_ml[(base + (size_t)h * a.splits + s) * 2 + 1];
+            s_w[h][s] = w;
+        }
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) l += __shfl_xor(l, m);
+        if (lane == 0) {
+            s_inv[h] = 1.0f / l;
+            s_lse[h] = (mx + log2f(l)) * kLn2;
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < G * kHeadDim; e += 256) {
+        const int h = e / kHeadDim, dim = e - h * kHeadDim;
+        const float *po = a.part_o + (base + (size_t)h * a.splits) * kHeadDim + dim;
+        float sum = 0.0f;
+#pragma unroll 8
+        for (int s = 0; s < nsplit; ++s) sum = fmaf(s_w[h][s], po[(size_t)s * kHeadDim], sum);
+        const int hq = g * G + h;
+        a.out[((size_t)row * Hq + hq) * kHeadDim + dim] = (uint16_t)f32_to_bf16_bits(sum * s_inv[h]);
+        if (a.lse && dim == 0) a.lse[(size_t)row * Hq + hq] = s_lse[h];
+    }
 }
 
 // Splits per (row, KV head): enough workgroups to cover the chip, at least one
@@ -294,8 +319,14 @@ size_t attn_partial_floats(const Geometry &g) {
 }
 
 template <int G>
-static void launch_attn_g(const AttnArgs &a, dim3 grid, hipStream_t stream) {
-    sparse_attn_kernel<G><<<grid, dim3(256), 0, stream>>>(a);
+static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int units,
+                                hipStream_t stream) {
+    if (paged) sparse_attn_kernel<G, true><<<grid, dim3(256), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false><<<grid, dim3(256), 0, stream>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits == 1) return e;
+    attn_merge_kernel<G><<<dim3(units), dim3(256), 0, stream>>>(a);
+    return hipGetLastError();
 }
 
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
@@ -327,19 +358,16 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
     const size_t blocks = (size_t)g.rows * g.kv_heads * a.splits;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)blocks);
+    const bool paged = g.page_shift >= 0;
+    const int units = g.rows * g.kv_heads;
     switch (g.group) {
-        case 1: launch_attn_g<1>(a, grid, stream); break;
-        case 2: launch_attn_g<2>(a, grid, stream); break;
-        case 4: launch_attn_g<4>(a, grid, stream); break;
-        case 5: launch_attn_g<5>(a, grid, stream); break;
-        case 8: launch_attn_g<8>(a, grid, stream); break;
+        case 1: return launch_attn_g<1>(a, paged, grid, units, stream);
+        case 2: return launch_attn_g<2>(a, paged, grid, units, stream);
+        case 4: return launch_attn_g<4>(a, paged, grid, units, stream);
+        case 5: return launch_attn_g<5>(a, paged, grid, units, stream);
+        case 8: return launch_attn_g<8>(a, paged, grid, units, stream);
         default: return hipErrorInvalidValue;
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || a.splits == 1) return e;
-    const int units = g.rows * g.q_heads;
-    attn_merge_kernel<<<dim3(div_up(units, 4)), dim3(256), 0, stream>>>(a, g.rows);
-    return hipGetLastError();
 }
 
 }  // namespace clsa

@@ -167,9 +167,15 @@ def test_workspace_sizes(lib):
     from paper_2606_06467_amd import binding as B
     sh = _shape(batch=4, max_len=131072, top_k=2048)
     assert B.clsa_workspace_bytes(sh, B.CLSA_OP_INDEX) == 0
-    assert B.clsa_workspace_bytes(sh, B.CLSA_OP_TOPK) == 0
+    # few rows: the multi-workgroup top-k keeps bitmaps and candidates in the workspace
+    assert B.clsa_workspace_bytes(sh, B.CLSA_OP_TOPK) >= 2 * 4 * 131072 // 8
+    # many rows: one workgroup per row, everything in LDS
+    many = _shape(batch=1, n_q=4096, max_len=131072, top_k=2048, causal=True)
+    assert B.clsa_workspace_bytes(many, B.CLSA_OP_TOPK) == 0
+    assert B.clsa_workspace_bytes(many, B.CLSA_OP_ATTN) == 0       # one split per row
     dec = B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 16)
     assert dec >= 4 * 131072 * 4 + 4 * 256 * 4
+    assert dec == B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 1)   # layers reuse buffers
     assert B.clsa_workspace_bytes(_shape(top_k=0), B.CLSA_OP_DECODE, 1) == 0
     assert B.clsa_workspace_bytes(sh, 99) == 0
 

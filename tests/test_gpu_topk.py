@@ -22,7 +22,7 @@ def _run(scores, k, lens, q_pos=None):
     qp = None if q_pos is None else torch.from_numpy(np.asarray(q_pos, np.int32)).cuda()
     idx = torch.full((Bt, T, k), -7, dtype=torch.int32, device="cuda")
     ns = torch.full((Bt, T), -7, dtype=torch.int32, device="cuda")
-    B.clsa_topk(sh, sc, sl, qp, idx, ns)
+    B.clsa_topk(sh, sc, sl, qp, idx, ns, B.workspace(sh, B.CLSA_OP_TOPK))
     torch.cuda.synchronize()
     return idx.cpu().numpy(), ns.cpu().numpy()
 
