@@ -174,8 +174,9 @@ def test_workspace_sizes(lib):
     assert B.clsa_workspace_bytes(many, B.CLSA_OP_TOPK) == 0
     assert B.clsa_workspace_bytes(many, B.CLSA_OP_ATTN) == 0       # one split per row
     dec = B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 16)
-    assert dec >= 4 * 131072 * 4 + 4 * 256 * 4
+    assert dec >= 4 * 131072 * 4 + 4 * 2048 * 4
     assert dec == B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 1)   # layers reuse buffers
+    assert B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, -1) == 0
     assert B.clsa_workspace_bytes(_shape(top_k=0), B.CLSA_OP_DECODE, 1) == 0
     assert B.clsa_workspace_bytes(sh, 99) == 0
 

@@ -67,6 +67,16 @@ def test_small_ragged_with_short_rows():
     _check_step(w, x, range(3), "ragged small")
 
 
+def test_single_layer_gathers_from_the_cache():
+    """With one layer the step attends straight from the cache (no compact copy)."""
+    w = inputs.small_workload(batch=3, lens=(9000, 2500, 4000), top_k=1024, n_layers=1, wid=94)
+    x = inputs.make_inputs(w)
+    _check_step(w, x, range(1), "one layer")
+    wp = inputs.small_workload(batch=2, lens=(9000, 2500), top_k=1024, n_layers=1, page_size=64,
+                               wid=95)
+    _check_step(wp, inputs.make_inputs(wp), range(1), "one layer paged")
+
+
 def test_small_paged():
     w = inputs.small_workload(batch=3, lens=(7000, 3000, 64), top_k=1024, page_size=64, n_layers=2,
                               wid=92)
