@@ -76,6 +76,9 @@ def main() -> int:
     ap.add_argument("--workload", default="decode_b4_n128k_planted")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after the timed steps, run plain device-to-device copies of this "
+                         "many MiB (a known-size reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the decode path "
@@ -154,6 +157,15 @@ def main() -> int:
                    for i in range(args.steps)])
     ev.close()
     index_ms, topk_ms, layers_ms = (float(v) for v in ph.mean(axis=0))
+
+    if args.copy_mib > 0:
+        n = args.copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     ab = algorithmic_bytes(w)
     step_us = ms_per_step * 1e3

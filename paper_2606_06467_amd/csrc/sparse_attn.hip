@@ -92,7 +92,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         }
         return;
     }
-    if (split >= nsplit) return;  // uniform; the merge only reads the first nsplit splits
+    if (split >= nsplit) return;  // uniform; the merge masks splits past the last one
     const int tok_end = min(n, tok_begin + span);
 
     uint4 qv[G];
@@ -249,53 +249,71 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     }
 }
 
-// Combine the splits of one (row, KV head): the G heads' partials (o, m, l) are
-// weighted by 2^(m_s - max m) and normalised by the weighted denominators.
-template <int G>
+// Combine the splits of one (row, query head) with the exact log-sum-exp rule:
+// o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s, M = max_s m_s.
+// 256 threads = 8 split groups x 32 four-dimension slices.  Every load the
+// workgroup needs (the row's selection count and all of its splits' (m, l) and
+// o) is issued in one batch before the first wait: splits past the row's last
+// one are read anyway (the buffer holds `splits` slots) and masked afterwards,
+// so the kernel costs one memory round trip.
+template <int SPT>  // splits per thread (8 * SPT >= splits)
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-    __shared__ float s_w[G][kMaxSplits];
-    __shared__ float s_inv[G], s_lse[G];
-    const int rg = blockIdx.x;
-    const int g = rg % a.kv_heads, row = rg / a.kv_heads;
-    const int Hq = a.q_heads;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    __shared__ float s_max[8], s_l[8];
+    __shared__ float4 s_o[8][32];
+    const int rh = blockIdx.x;  // row * Hq + head
+    const int row = rh / a.q_heads;
+    const int tid = threadIdx.x, dq = tid & 31, sg = tid >> 5;
+    const size_t base = (size_t)rh * a.splits;
+    float4 o[SPT];
+    float2 ml[SPT];
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+        const int s = min(sg + 8 * j, a.splits - 1);
+        o[j] = *reinterpret_cast<const float4 *>(a.part_o + (base + s) * kHeadDim + dq * 4);
+        ml[j] = *reinterpret_cast<const float2 *>(a.part_ml + (base + s) * 2);
+    }
     const int n = min(max(a.n_sel[row], 0), a.top_k);
-    const int nsplit = div_up(n, a.chunks_per_split * 64);
+    const int nsplit = div_up(n, a.chunks_per_split * 64);  // splits that hold tokens
     if (nsplit == 0) return;  // the attention kernel wrote the empty-set result
-    const size_t base = ((size_t)row * Hq + g * G) * a.splits;
-    for (int x = tid; x < G * nsplit; x += 256) {
-        const int h = x / nsplit, s = x - h * nsplit;
-        s_w[h][s] = a.part_ml[(base + (size_t)h * a.splits + s) * 2];
-    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j)
+        if (sg + 8 * j < nsplit) mx = fmaxf(mx, ml[j].x);
+    if (dq == 0) s_max[sg] = mx;
     __syncthreads();
-    for (int h = wave; h < G; h += 4) {  // per head: max over splits, weights, denominator
-        float mx = -INFINITY;
-        for (int s = lane; s < nsplit; s += 64) mx = fmaxf(mx, s_w[h][s]);
+    float M = s_max[0];
 #pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
-        float l = 0.0f;
-        for (int s = lane; s < nsplit; s += 64) {
-            const float w = exp2f(s_w[h][s] - mx);
-            l += w * a.part_ml[(base + (size_t)h * a.splits + s) * 2 + 1];
-            s_w[h][s] = w;
-        }
+    for (int x = 1; x < 8; ++x) M = fmaxf(M, s_max[x]);  // finite: split 0 holds tokens
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float l = 0.0f;
 #pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) l += __shfl_xor(l, m);
-        if (lane == 0) {
-            s_inv[h] = 1.0f / l;
-            s_lse[h] = (mx + log2f(l)) * kLn2;
+    for (int j = 0; j < SPT; ++j) {
+        if (sg + 8 * j < nsplit) {
+            const float w = exp2f(ml[j].x - M);
+            l = fmaf(w, ml[j].y, l);
+            acc.x = fmaf(w, o[j].x, acc.x);
+            acc.y = fmaf(w, o[j].y, acc.y);
+            acc.z = fmaf(w, o[j].z, acc.z);
+            acc.w = fmaf(w, o[j].w, acc.w);
         }
     }
+    s_o[sg][dq] = acc;
+    if (dq == 0) s_l[sg] = l;
     __syncthreads();
-    for (int e = tid; e < G * kHeadDim; e += 256) {
-        const int h = e / kHeadDim, dim = e - h * kHeadDim;
-        const float *po = a.part_o + (base + (size_t)h * a.splits) * kHeadDim + dim;
-        float sum = 0.0f;
-#pragma unroll 8
-        for (int s = 0; s < nsplit; ++s) sum = fmaf(s_w[h][s], po[(size_t)s * kHeadDim], sum);
-        const int hq = g * G + h;
-        a.out[((size_t)row * Hq + hq) * kHeadDim + dim] = (uint16_t)f32_to_bf16_bits(sum * s_inv[h]);
-        if (a.lse && dim == 0) a.lse[(size_t)row * Hq + hq] = s_lse[h];
+    if (tid < 32) {
+        float4 r = s_o[0][dq];
+        float L = s_l[0];
+#pragma unroll
+        for (int x = 1; x < 8; ++x) {
+            const float4 t = s_o[x][dq];
+            r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
+            L += s_l[x];
+        }
+        const float inv = 1.0f / L;
+        const uint32_t lo = f32_to_bf16_bits(r.x * inv) | (f32_to_bf16_bits(r.y * inv) << 16);
+        const uint32_t hi = f32_to_bf16_bits(r.z * inv) | (f32_to_bf16_bits(r.w * inv) << 16);
+        *reinterpret_cast<uint2 *>(a.out + (size_t)rh * kHeadDim + dq * 4) = make_uint2(lo, hi);
+        if (a.lse && tid == 0) a.lse[rh] = (M + log2f(L)) * kLn2;
     }
 }
 
@@ -325,7 +343,12 @@ static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int un
     else sparse_attn_kernel<G, false><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits == 1) return e;
-    attn_merge_kernel<G><<<dim3(units), dim3(256), 0, stream>>>(a);
+    const dim3 mgrid(units), mblock(256);
+    if (a.splits <= 8) attn_merge_kernel<1><<<mgrid, mblock, 0, stream>>>(a);
+    else if (a.splits <= 16) attn_merge_kernel<2><<<mgrid, mblock, 0, stream>>>(a);
+    else if (a.splits <= 32) attn_merge_kernel<4><<<mgrid, mblock, 0, stream>>>(a);
+    else if (a.splits <= 64) attn_merge_kernel<8><<<mgrid, mblock, 0, stream>>>(a);
+    else attn_merge_kernel<16><<<mgrid, mblock, 0, stream>>>(a);
     return hipGetLastError();
 }
 
@@ -359,7 +382,7 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)blocks);
     const bool paged = g.page_shift >= 0;
-    const int units = g.rows * g.kv_heads;
+    const int units = g.rows * g.q_heads;  // merge workgroups: one per (row, query head)
     switch (g.group) {
         case 1: return launch_attn_g<1>(a, paged, grid, units, stream);
         case 2: return launch_attn_g<2>(a, paged, grid, units, stream);
