@@ -151,12 +151,16 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
 /* Static, human-readable name of a status code. */
 const char *clsa_status_string(clsa_status status);
 
-/* Profiling hook (not thread-safe; set and use from one thread).  With n == 4
- * and four hipEvent_t handles, the next clsa_decode_step calls record
- * events[0] right before the indexer kernel, events[1] after it, events[2]
- * after the top-k and events[3] after the last layer, on the call's stream.
- * n == 0 (events may be NULL) switches the hook off.  Any other n is
- * CLSA_ERR_INVALID_ARG. */
+/* Profiling hook (not thread-safe; set and use from one thread).  With
+ * n = 4 + 2m (0 <= m <= 64) non-null hipEvent_t handles, the next
+ * clsa_decode_step calls record, on the call's stream: events[0] right before
+ * the indexer kernel, events[1] after it, events[2] after the top-k and
+ * events[3] after the last layer; and for each layer l < m, events[4 + 2l]
+ * right before the layer's sparse-attention kernel and events[5 + 2l] right
+ * after it (before its split merge, if any).  The handles are kept, not
+ * copied: they must stay valid while the hook is on.  n == 0 (events may be
+ * NULL) switches the hook off.  Any other n, or a NULL handle, is
+ * CLSA_ERR_INVALID_ARG and leaves the hook as it was. */
 clsa_status clsa_set_phase_events(void *const *events, int32_t n);
 
 #ifdef __cplusplus

@@ -156,7 +156,9 @@ def clsa_decode_step(shape, q_idx, k_idx, k_cache, v_cache, page_table, seq_lens
 
 
 def clsa_set_phase_events(events: Optional[Sequence[int]]) -> None:
-    """events: four raw hipEvent_t handles (ints), or None to switch the hook off."""
+    """events: 4 + 2m raw hipEvent_t handles (ints): the four phase marks, then a
+    (before, after) pair around the attention kernel of each of the first m
+    layers; None switches the hook off."""
     if not events:
         _check(lib().clsa_set_phase_events(None, 0), "clsa_set_phase_events")
         return
@@ -172,12 +174,21 @@ def workspace(shape: ClsaShape, op: int, n_layers: int = 0, device="cuda") -> Op
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-class HipEvents:
-    """Raw HIP events (libamdhip64) for timing work on a given stream."""
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000  # hipEventDisableSystemFence
 
-    def __init__(self, n: int):
+
+class HipEvents:
+    """Raw HIP events (libamdhip64) for timing work on a given stream.
+
+    ``timing_only`` events skip the system-scope fence that an event record
+    otherwise performs (a cache write-back and invalidate, which both costs time
+    and slows the work after it); read them only after the device has been
+    synchronised."""
+
+    def __init__(self, n: int, timing_only: bool = False):
         self._hip = ctypes.CDLL("libamdhip64.so")
-        self._hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p),
+                                                      ctypes.c_uint]
         self._hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         self._hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
         self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
@@ -186,8 +197,9 @@ class HipEvents:
         self.handles = []
         for _ in range(n):
             h = ctypes.c_void_p()
-            if self._hip.hipEventCreate(ctypes.byref(h)) != 0:
-                raise RuntimeError("hipEventCreate failed")
+            flags = HIP_EVENT_DISABLE_SYSTEM_FENCE if timing_only else 0
+            if self._hip.hipEventCreateWithFlags(ctypes.byref(h), flags) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
             self.handles.append(h.value)
 
     def record(self, i: int, stream=None) -> None:

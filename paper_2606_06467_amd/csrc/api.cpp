@@ -15,8 +15,10 @@ constexpr int kMaxTopK = 8192;
 constexpr int kMaxLen = 262144;
 constexpr size_t kAlign = 256;
 
+constexpr int kHookLayers = 64;  // layers whose attention kernel the hook can bracket
 struct PhaseHook {
-    hipEvent_t ev[4];
+    hipEvent_t ev[4 + 2 * kHookLayers];
+    int layers = 0;                 // layers bracketed by ev[4 + 2l], ev[5 + 2l]
     bool on = false;
 } g_hook;
 
@@ -323,8 +325,11 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
         const uint16_t *ql = static_cast<const uint16_t *>(q_layers) + l * q_stride;
         uint16_t *ol = static_cast<uint16_t *>(out_layers) + l * q_stride;
         float *lsel = lse_layers ? lse_layers + l * lse_stride : nullptr;
+        const bool mark = hook && l < g_hook.layers;
+        if (mark && hipEventRecord(g_hook.ev[4 + 2 * l], st) != hipSuccess) return CLSA_ERR_HIP;
         CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, idx, n_sel,
-                                                   ol, lsel, w.partials, st)));
+                                                   ol, lsel, w.partials, st,
+                                                   mark ? g_hook.ev[5 + 2 * l] : nullptr)));
     }
     if (hook && hipEventRecord(g_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
     return CLSA_OK;
@@ -346,11 +351,11 @@ clsa_status clsa_set_phase_events(void *const *events, int32_t n) {
         g_hook.on = false;
         return CLSA_OK;
     }
-    if (n != 4 || !events) return CLSA_ERR_INVALID_ARG;
-    for (int i = 0; i < 4; ++i) {
+    if (n < 4 || n > 4 + 2 * kHookLayers || (n & 1) || !events) return CLSA_ERR_INVALID_ARG;
+    for (int i = 0; i < n; ++i)
         if (!events[i]) return CLSA_ERR_INVALID_ARG;
-        g_hook.ev[i] = static_cast<hipEvent_t>(events[i]);
-    }
+    for (int i = 0; i < n; ++i) g_hook.ev[i] = static_cast<hipEvent_t>(events[i]);
+    g_hook.layers = (n - 4) / 2;
     g_hook.on = true;
     return CLSA_OK;
 }

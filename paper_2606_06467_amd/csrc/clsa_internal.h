@@ -64,9 +64,13 @@ hipError_t launch_zero_u32(uint32_t *p, size_t n, hipStream_t stream);
 
 // ---- sparse_attn.hip ----
 size_t attn_partial_floats(const Geometry &g);  // 0 when one split per (row, KV head)
+// Attention gathering K/V rows from the cache through idx (and the page table).
+// split_done, if not null, is recorded right after the attention kernel, before
+// the split merge.
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
-                              float *partials, hipStream_t stream);
+                              float *partials, hipStream_t stream,
+                              hipEvent_t split_done = nullptr);
 
 }  // namespace clsa

@@ -338,10 +338,11 @@ size_t attn_partial_floats(const Geometry &g) {
 
 template <int G>
 static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int units,
-                                hipStream_t stream) {
+                                hipStream_t stream, hipEvent_t split_done) {
     if (paged) sparse_attn_kernel<G, true><<<grid, dim3(256), 0, stream>>>(a);
     else sparse_attn_kernel<G, false><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1) return e;
     const dim3 mgrid(units), mblock(256);
     if (a.splits <= 8) attn_merge_kernel<1><<<mgrid, mblock, 0, stream>>>(a);
@@ -355,7 +356,7 @@ static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int un
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
-                              float *partials, hipStream_t stream) {
+                              float *partials, hipStream_t stream, hipEvent_t split_done) {
     AttnArgs a;
     a.q = static_cast<const uint16_t *>(q);
     a.k = static_cast<const uint16_t *>(k_cache);
@@ -384,11 +385,11 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
     const bool paged = g.page_shift >= 0;
     const int units = g.rows * g.q_heads;  // merge workgroups: one per (row, query head)
     switch (g.group) {
-        case 1: return launch_attn_g<1>(a, paged, grid, units, stream);
-        case 2: return launch_attn_g<2>(a, paged, grid, units, stream);
-        case 4: return launch_attn_g<4>(a, paged, grid, units, stream);
-        case 5: return launch_attn_g<5>(a, paged, grid, units, stream);
-        case 8: return launch_attn_g<8>(a, paged, grid, units, stream);
+        case 1: return launch_attn_g<1>(a, paged, grid, units, stream, split_done);
+        case 2: return launch_attn_g<2>(a, paged, grid, units, stream, split_done);
+        case 4: return launch_attn_g<4>(a, paged, grid, units, stream, split_done);
+        case 5: return launch_attn_g<5>(a, paged, grid, units, stream, split_done);
+        case 8: return launch_attn_g<8>(a, paged, grid, units, stream, split_done);
         default: return hipErrorInvalidValue;
     }
 }

@@ -189,6 +189,11 @@ def test_phase_event_hook_arguments(lib):
     assert lib.clsa_set_phase_events(arr, 3) == -1
     arr4 = (ctypes.c_void_p * 4)(A, A, None, A)
     assert lib.clsa_set_phase_events(arr4, 4) == -1
+    many = (ctypes.c_void_p * (4 + 2 * 65))(*([A] * (4 + 2 * 65)))
+    assert lib.clsa_set_phase_events(many, 5) == -1              # odd: pairs per layer
+    assert lib.clsa_set_phase_events(many, 4 + 2 * 65) == -1     # at most 64 layers
+    assert lib.clsa_set_phase_events(many, 4 + 2 * 64) == 0
+    assert lib.clsa_set_phase_events(many, 6) == 0
     assert lib.clsa_set_phase_events(None, 0) == 0
 
 
