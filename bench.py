@@ -30,19 +30,31 @@ if ROOT not in sys.path:
 
 METRIC = "CLSA decode-step µs + HBM GB/s (index+top-k+L sparse attn), 128K ctx"
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak
+PREFILL_MIN_ROWS = 32            # query rows per sequence from which the indexer uses MFMA
 
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(w):
-    """Bytes the step must move at least once (unique): index keys + scores out,
-    the selected K/V rows once, per-layer queries and outputs, the index set."""
+def valid_keys_per_row(w, x):
+    """Valid keys of every query row (causal rows stop at their position)."""
+    lens = np.asarray(w.lens, dtype=np.int64)[:, None].repeat(w.n_q, axis=1)
+    if x.get("q_pos") is not None:
+        lens = np.minimum(lens, np.maximum(x["q_pos"].astype(np.int64) + 1, 0))
+    return lens
+
+
+def algorithmic_bytes(w, x):
+    """Bytes the step must move at least once: index keys read + scores written,
+    the selected K/V rows (for decode each row's once; for many query rows the
+    logical gather of every row), per-layer queries and outputs, the index set."""
+    n = valid_keys_per_row(w, x)
     toks = sum(w.lens)
     index_keys = toks * w.idx_heads * w.idx_dim * 2
-    scores = toks * 4
-    sel = sum(min(w.top_k, n) for n in w.lens) * w.n_q
+    scores = int(n.sum()) * 4
+    sel = int(np.minimum(n, w.top_k).sum())
     kv_rows = sel * w.kv_heads * w.head_dim * 2 * 2
     qo = w.n_layers * w.batch * w.n_q * w.q_heads * w.head_dim * 2 * 2
     idx = w.batch * w.n_q * w.top_k * 4
@@ -50,12 +62,13 @@ def algorithmic_bytes(w):
     # and its index list (the output leaves through the split merge)
     attn = kv_rows + w.batch * w.n_q * (w.q_heads * w.head_dim * 2 + w.top_k * 4)
     return dict(index=index_keys + scores, step=index_keys + scores + kv_rows + qo + idx,
-                kv_rows=kv_rows, attn=attn)
+                kv_rows=kv_rows, attn=attn, index_flops=2 * w.idx_heads * w.idx_dim * int(n.sum()))
 
 
 KERNEL_SOURCES = {
     "sparse_attn_kernel": ["sparse_attn.hip", "device_common.h", "clsa_internal.h"],
     "index_decode_kernel": ["index_decode.hip", "device_common.h", "clsa_internal.h"],
+    "index_prefill_kernel": ["index_prefill.hip", "device_common.h", "clsa_internal.h"],
 }
 
 
@@ -86,6 +99,15 @@ def traffic_bytes(kernel: str, workload: str):
     return None
 
 
+def roofline_mfma(kernel: str, w, flops: int, ms: float):
+    achieved = flops / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 1),
+            "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": traffic_bytes(kernel, w.name), "algorithmic_flops_per_launch": flops,
+            "avg_launch_us": round(ms * 1e3, 2)}
+
+
 def roofline(kernel: str, w, alg_bytes: int, ms: float):
     achieved = alg_bytes / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
@@ -96,21 +118,38 @@ def roofline(kernel: str, w, alg_bytes: int, ms: float):
 
 def cpu_baseline(w, x, budget_s: float):
     """Time the CPU oracle on the same workload, repeating whole steps until
-    ``budget_s`` seconds have passed (at least one)."""
+    ``budget_s`` seconds have passed (at least one).  With many query rows per
+    sequence (chunked prefill) a whole step would take the oracle far longer;
+    it then runs the step for the first 16 query rows of each sequence (same
+    caches, same layers) and the time is scaled to all rows, and labelled so."""
+    import dataclasses
     import oracle as orc
-    sh = orc.shape_of(w)
+    ws, xs, scale = w, x, 1.0
+    if w.n_q > 16:
+        ws = dataclasses.replace(w, n_q=16)
+        xs = dict(x, q_idx=np.ascontiguousarray(x["q_idx"][:, :16]),
+                  q_layers=np.ascontiguousarray(x["q_layers"][:, :, :16]),
+                  q_pos=None if x["q_pos"] is None else np.ascontiguousarray(x["q_pos"][:, :16]))
+        scale = w.n_q / 16
+    sh = orc.shape_of(ws)
     reps, t0 = 0, time.perf_counter()
     while True:
-        orc.decode_step(sh, x["q_idx"], x["k_idx"], x["k_cache"], x["v_cache"], x["seq_lens"],
-                        x["q_layers"], x["q_pos"], x["page_table"])
+        orc.decode_step(sh, xs["q_idx"], xs["k_idx"], xs["k_cache"], xs["v_cache"],
+                        xs["seq_lens"], xs["q_layers"], xs["q_pos"], xs["page_table"])
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
             break
-    us = el / reps * 1e6
+    us = el / reps * 1e6 * scale
+    if scale == 1.0:
+        sample = (f"{reps} full step(s) of {w.name} (B={w.batch}, L={w.n_layers}), "
+                  f"single-threaded C, {el:.1f} s")
+    else:
+        sample = (f"{reps} step(s) over the first 16 of {w.n_q} query rows of {w.name} "
+                  f"(L={w.n_layers}), single-threaded C, {el:.1f} s; scaled x{scale:g} "
+                  f"to all rows (extrapolated)")
     return {"value": round(us, 1), "unit": "us/step", "cores": 1, "kind": "oracle",
-            "sample": f"{reps} full decode step(s) of {w.name} (B={w.batch}, L={w.n_layers}), "
-                      f"single-threaded C, {el:.1f} s"}
+            "sample": sample}
 
 
 def main() -> int:
@@ -221,7 +260,7 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    ab = algorithmic_bytes(w)
+    ab = algorithmic_bytes(w, x)
     step_us = ms_per_step * 1e3
     res = {
         "metric": METRIC,
@@ -237,7 +276,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "batch": w.batch, "context": max(w.lens),
+        "config": {"workload": w.name, "batch": w.batch, "query_rows": w.n_q, "context": max(w.lens),
                    "top_k": w.top_k, "layers": L, "q_heads": w.q_heads, "kv_heads": w.kv_heads,
                    "head_dim": w.head_dim, "index_dim": w.idx_heads * w.idx_dim,
                    "paged": bool(w.page_size), "planted": w.planted},
@@ -251,7 +290,9 @@ def main() -> int:
         # the kernel with the largest share of the step: the sparse-attention
         # kernel, launched once per layer
         "roofline": roofline("sparse_attn_kernel", w, ab["attn"], attn_ms),
-        "roofline_index": roofline("index_decode_kernel", w, ab["index"], index_ms),
+        "roofline_index": (roofline_mfma("index_prefill_kernel", w, ab["index_flops"], index_ms)
+                           if w.n_q >= PREFILL_MIN_ROWS else
+                           roofline("index_decode_kernel", w, ab["index"], index_ms)),
     }
     if args.cpu_budget > 0:
         log("[bench] CPU oracle baseline ...")

@@ -233,8 +233,12 @@ clsa_status clsa_index_scores(const clsa_shape *shape, const void *q_idx, const 
     CLSA_TRY(check_ptr(seq_lens, 4));
     CLSA_TRY(check_ptr(scores, 4));
     CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (clsa::index_uses_mfma(g))
+        return from_hip(clsa::launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos,
+                                                   scores, st));
     return from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, scores,
-                                              nullptr, static_cast<hipStream_t>(stream)));
+                                              nullptr, st));
 }
 
 clsa_status clsa_topk(const clsa_shape *shape, const float *scores, const int32_t *seq_lens,
@@ -311,12 +315,21 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
     carve_decode(g, ws, w);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool hook = g_hook.on;
-    CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
+    // Many query rows per sequence (chunked prefill): scores on the matrix cores,
+    // without the coarse histogram, which the top-k then makes itself.  The
+    // histogram and counters need clearing unless that top-k is the per-row one.
+    const bool mfma = clsa::index_uses_mfma(g);
+    if (!mfma || clsa::topk_uses_wide(g))
+        CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
     if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
-    CLSA_TRY(from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos,
-                                                w.scores, w.topk.hist, st)));
+    if (mfma)
+        CLSA_TRY(from_hip(clsa::launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos,
+                                                     w.scores, st)));
+    else
+        CLSA_TRY(from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos,
+                                                    w.scores, w.topk.hist, st)));
     if (hook && hipEventRecord(g_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
-    CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, true, idx, n_sel,
+    CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, idx, n_sel,
                                         st)));
     if (hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
     const size_t q_stride = (size_t)g.rows * g.q_heads * 128;  // bf16 elements per layer

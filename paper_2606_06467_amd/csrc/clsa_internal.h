@@ -42,6 +42,15 @@ hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void 
                                const int32_t *q_pos, float *scores, uint32_t *coarse_hist,
                                hipStream_t stream);
 
+// ---- index_prefill.hip ----
+// Query rows per sequence from which the indexer runs on the matrix cores.
+constexpr int kPrefillMinRows = 32;
+bool index_uses_mfma(const Geometry &g);
+// Scores only (no coarse histogram).
+hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void *k_idx,
+                                const int32_t *page_table, const int32_t *seq_lens,
+                                const int32_t *q_pos, float *scores, hipStream_t stream);
+
 // ---- topk.hip ----
 struct TopkWideLayout {
     int words_max, cand_cap;
