@@ -29,31 +29,94 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float acc) {
     return acc;
 }
 
+// Lane exchanges without the LDS crossbar.  Inside a row of 16 lanes, DPP (a
+// VALU operand modifier): lane i reads lane 15 - i (row mirror), 7 - i within
+// its half-row (half mirror), i ^ 2 or i ^ 1 (quad permutes).  Across rows,
+// the gfx950 permlane swaps: v_permlane32_swap(x, y) leaves lanes 0-31 with
+// (x[i], x[i + 32]) and lanes 32-63 with (y[i - 32], y[i]); v_permlane16_swap
+// does the same between rows 0 and 1 and between rows 2 and 3.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+// The value of `x` held by this lane's exchange partner at distance M <= 8
+// inside a row.  A transpose step needs a partner with the other value of bit M
+// that shares every higher exchanged bit, so the mirrors serve M = 8 and 4.
+template <int M>
+__device__ __forceinline__ float row_partner(float x) {
+    static_assert(M == 8 || M == 4 || M == 2 || M == 1, "inside a row");
+    if constexpr (M == 8) return dpp_f32<0x140>(x);
+    else if constexpr (M == 4) return dpp_f32<0x141>(x);
+    else if constexpr (M == 2) return dpp_f32<0x4E>(x);
+    else return dpp_f32<0xB1>(x);
+}
+
+// lo + partner's lo for lanes with bit M clear, hi + partner's hi for lanes with
+// it set (M = 16 or 32): the exchange step across rows.
+template <int M>
+__device__ __forceinline__ float cross_row_step(float lo, float hi) {
+    static_assert(M == 16 || M == 32, "across rows");
+    const auto r = M == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(lo),
+                                                              __float_as_uint(hi), false, false)
+                           : __builtin_amdgcn_permlane16_swap(__float_as_uint(lo),
+                                                              __float_as_uint(hi), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Transpose-reduction across lanes.  Each lane holds CNT partial values; at the
-// exchange with lane ^ M it keeps the half selected by (lane & M) and adds the
-// partner's copy of that half, for M, M/2, ..., MSTOP.  Once a single value is
-// left the remaining exchanges are plain sums.  With CNT = 2^s values and s
-// halving steps, lane L ends with value index (L's step bits, high to low) of
-// the original CNT, summed over every lane the steps visited.  All sizes are
-// compile-time so that every register index stays static.
+// exchange with its partner at distance M it keeps the half selected by
+// (lane & M) and adds the partner's copy of that half, for M, M/2, ..., MSTOP.
+// Once a single value is left the remaining exchanges are plain sums.  With
+// CNT = 2^s values and s halving steps, lane L ends with value index (L's step
+// bits, high to low) of the original CNT, summed over every lane the steps
+// visited.  All sizes are compile-time so that every register index stays static.
 template <int CNT, int M, int MSTOP, int NV>
 __device__ __forceinline__ void transpose_reduce(float (&p)[NV], int lane) {
     if constexpr (M >= MSTOP) {
         if constexpr (CNT > 1) {
             constexpr int H = CNT / 2;
-            const bool up = (lane & M) != 0;
+            if constexpr (M >= 16) {
 #pragma unroll
-            for (int v = 0; v < H; ++v) {
-                const float keep = up ? p[v + H] : p[v];
-                const float send = up ? p[v] : p[v + H];
-                p[v] = keep + __shfl_xor(send, M);
+                for (int v = 0; v < H; ++v) p[v] = cross_row_step<M>(p[v], p[v + H]);
+            } else {
+                const bool up = (lane & M) != 0;
+#pragma unroll
+                for (int v = 0; v < H; ++v) {
+                    const float keep = up ? p[v + H] : p[v];
+                    const float send = up ? p[v] : p[v + H];
+                    p[v] = keep + row_partner<M>(send);
+                }
             }
             transpose_reduce<H, M / 2, MSTOP, NV>(p, lane);
         } else {
-            p[0] += __shfl_xor(p[0], M);
+            if constexpr (M >= 16) p[0] = cross_row_step<M>(p[0], p[0]);
+            else p[0] += row_partner<M>(p[0]);
             transpose_reduce<1, M / 2, MSTOP, NV>(p, lane);
         }
     }
+}
+
+// Maximum / sum over all 64 lanes; every lane gets the result.
+__device__ __forceinline__ float wave_max(float x) {
+    x = fmaxf(x, dpp_f32<0xB1>(x));
+    x = fmaxf(x, dpp_f32<0x4E>(x));
+    x = fmaxf(x, dpp_f32<0x141>(x));
+    x = fmaxf(x, dpp_f32<0x140>(x));
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+    x += dpp_f32<0xB1>(x);
+    x += dpp_f32<0x4E>(x);
+    x += dpp_f32<0x141>(x);
+    x += dpp_f32<0x140>(x);
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }

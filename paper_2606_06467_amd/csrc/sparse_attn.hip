@@ -164,15 +164,11 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         // per-head chunk statistics and online-softmax update
         for (int h = wave; h < G; h += 4) {
             const float z = zs[h][lane];
-            float mx = z;
-#pragma unroll
-            for (int m = 32; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
+            const float mx = wave_max(z);
             const float m_old = s_ml[h][0];
             const float m_new = fmaxf(m_old, mx);   // finite: the chunk has a valid token
             const float w = exp2f(z - m_new);        // z = -inf -> 0
-            float sum = w;
-#pragma unroll
-            for (int m = 32; m >= 1; m >>= 1) sum += __shfl_xor(sum, m);
+            const float sum = wave_sum(w);
             zs[h][lane] = w;
             if (lane == 0) {
                 const float sc = exp2f(m_old - m_new);  // m_old = -inf -> 0
