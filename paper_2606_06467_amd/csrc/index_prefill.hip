@@ -7,9 +7,7 @@
 //   * A = 16 index keys x 32 index dims, B = 32 dims x 16 queries, so C is
 //     keys x queries.  Lane l supplies A row / B column (l & 15) for dims
 //     (l >> 4) * 8 .. +8 of a 32-dim step, and receives C rows 4 * (l >> 4) + r
-//     (r = 0..3) of column (l & 15): four consecutive keys of one query, so a
-//     16-byte store per key tile, and the four lanes of a query cover 64
-//     contiguous bytes.
+//     (r = 0..3) of column (l & 15): four consecutive keys of one query.
 // Key-stationary work split: a workgroup owns 256 consecutive keys of one
 // sequence (each of its 4 waves holds 64 of them, all 256 dims, as A operands
 // in registers for the whole kernel) and streams that sequence's queries 16 at
@@ -19,7 +17,10 @@
 // by every workgroup and stay in the L2.  Query tiles whose rows all end
 // before the block's first key (causal) are skipped.  The score block is
 // written once, non-temporally (the top-k reads it back), which bounds the
-// kernel by HBM writes (4 bytes per 512 FLOP) rather than by the matrix cores.
+// kernel by HBM writes (4 bytes per 512 FLOP) rather than by the matrix cores;
+// each query tile's 16 x 256 scores are therefore staged in LDS and written as
+// whole 1 KiB row segments (direct 16-byte stores of 64-byte row pieces
+// reached only about 3 TB/s).
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -67,18 +68,27 @@ __device__ __forceinline__ int key_limit(const int32_t *qpos, int len, int n_q, 
     return t < n_q ? n : 0;
 }
 
-// Scores of query tile qt against the wave's 64 keys, then their stores.
-// n: key limit of this lane's query (qt*16 + col).
+// LDS staging of one query tile's scores: 16 rows x the workgroup's 256 keys
+// (padded rows against bank conflicts), two buffers used alternately.
+constexpr int kTileStride = kPfKeys + 4;
+
+// Scores of query tile qt against the workgroup's 256 keys.  Each wave writes
+// its 16 x 64 part into the LDS tile; after a barrier each wave stores four
+// whole rows (one 1 KiB row segment per store instruction).  n: key limit of
+// this lane's query (qt*16 + (lane & 15)).  The early exit is uniform over the
+// workgroup (every wave holds the same 16 queries); it still passes a barrier
+// so that a buffer is never rewritten while another wave reads it.
 __device__ __forceinline__ void score_tile(const PrefillArgs &a, const bf16x8 (&kv)[4][8],
-                                           const bf16x8 (&qv)[8], int n, int b, int qt, int jw,
-                                           int col, int grp) {
+                                           const bf16x8 (&qv)[8], int n, int b, int qt, int jg,
+                                           int wave, int lane, float (*tile)[kTileStride]) {
+    const int col = lane & 15, grp = lane >> 4;
     int nmax = n;
 #pragma unroll
     for (int m = 8; m >= 1; m >>= 1) nmax = max(nmax, __shfl_xor(nmax, m));
-    nmax = max(nmax, __shfl_xor(nmax, 16));
-    nmax = max(nmax, __shfl_xor(nmax, 32));
-    if (nmax <= jw) return;  // no query of the tile reaches this wave's keys
-
+    if (nmax <= jg) {  // no query of the tile reaches the workgroup's keys
+        __syncthreads();
+        return;
+    }
     f32x4 c[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) c[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -87,19 +97,25 @@ __device__ __forceinline__ void score_tile(const PrefillArgs &a, const bf16x8 (&
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
             c[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv[kt][kb], qv[kb], c[kt], 0, 0, 0);
-
-    // lane holds keys jw + 16*kt + 4*grp + r (r = 0..3) of query t (none if n == 0)
-    const int t = qt * 16 + col;
-    float *dst = a.scores + ((size_t)b * a.n_q + t) * a.max_len + jw + 4 * grp;
+    // lane holds keys wave*64 + 16*kt + 4*grp + r (r = 0..3) of query col
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-        const int j0 = jw + 16 * kt + 4 * grp;
-        if (a.vec_store && j0 + 4 <= n) {
-            __builtin_nontemporal_store(c[kt], reinterpret_cast<f32x4 *>(dst + 16 * kt));
+    for (int kt = 0; kt < 4; ++kt)
+        *reinterpret_cast<f32x4 *>(&tile[col][wave * kPfWaveKeys + 16 * kt + 4 * grp]) = c[kt];
+    __syncthreads();
+    const int j0 = jg + 4 * lane;  // this lane's 4 keys of every row
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rr = wave * 4 + i;
+        const int nr = __builtin_amdgcn_readlane(n, rr);  // lane rr holds query rr's limit
+        if (j0 >= nr) continue;
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(&tile[rr][4 * lane]);
+        float *dst = a.scores + ((size_t)b * a.n_q + qt * 16 + rr) * a.max_len + j0;
+        if (a.vec_store && j0 + 4 <= nr) {
+            __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
         } else {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                if (j0 + r < n) dst[16 * kt + r] = c[kt][r];
+                if (j0 + r < nr) dst[r] = v[r];
         }
     }
 }
@@ -111,8 +127,10 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int col = lane & 15, grp = lane >> 4;
     const int len = clamp_len(a.seq_lens[b], a.max_len);
-    const int jw = kblk * kPfKeys + wave * kPfWaveKeys;  // first key of this wave
-    if (jw >= len) return;                                // uniform per wave; no barriers below
+    const int jg = kblk * kPfKeys;                       // first key of this workgroup
+    const int jw = jg + wave * kPfWaveKeys;              // first key of this wave
+    if (jg >= len) return;                               // uniform over the workgroup
+    __shared__ float tile[2][16][kTileStride];
 
     // the wave's 64 keys as A operands: key tile kt, row col = key jw + 16*kt + col
     bf16x8 kv[4][8];
@@ -144,13 +162,13 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
             n_b = key_limit<CAUSAL>(qpos, len, a.n_q, (qt + 1) * 16 + col);
             load_queries(a, b, qt + 1, col, grp, qb);
         }
-        score_tile(a, kv, qa, n_a, b, qt, jw, col, grp);
+        score_tile(a, kv, qa, n_a, b, qt, jg, wave, lane, tile[0]);
         if (qt + 1 >= ntiles) break;
         if (qt + 2 < ntiles) {
             n_a = key_limit<CAUSAL>(qpos, len, a.n_q, (qt + 2) * 16 + col);
             load_queries(a, b, qt + 2, col, grp, qa);
         }
-        score_tile(a, kv, qb, n_b, b, qt + 1, jw, col, grp);
+        score_tile(a, kv, qb, n_b, b, qt + 1, jg, wave, lane, tile[1]);
     }
 }
 
