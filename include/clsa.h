@@ -86,7 +86,8 @@ typedef enum {
     CLSA_OP_INDEX = 0,  /* clsa_index_scores (needs no workspace) */
     CLSA_OP_TOPK = 1,   /* clsa_topk */
     CLSA_OP_ATTN = 2,   /* clsa_sparse_attn */
-    CLSA_OP_DECODE = 3  /* clsa_decode_step */
+    CLSA_OP_DECODE = 3, /* clsa_decode_step and clsa_decode_step_grouped */
+    CLSA_OP_DENSE = 4   /* clsa_dense_attn */
 } clsa_op;
 
 typedef struct clsa_shape {
@@ -107,7 +108,7 @@ typedef struct clsa_shape {
 } clsa_shape;
 
 /* Bytes of workspace `op` needs for `shape` (n_layers only matters for
- * CLSA_OP_DECODE).  Returns 0 for CLSA_OP_INDEX, and also 0 when the shape is
+ * CLSA_OP_DECODE, where it never changes the size).  Returns 0 for CLSA_OP_INDEX, and also 0 when the shape is
  * invalid or unsupported (the entry point then reports the reason). */
 size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layers);
 
@@ -147,6 +148,38 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
                              const int32_t *q_pos, int32_t n_layers, const void *q_layers,
                              void *out_layers, float *lse_layers, int32_t *idx, int32_t *n_sel,
                              void *ws, size_t ws_bytes, void *stream);
+
+/* The same step with the routing refreshed every `group` layers, for measuring
+ * what the shared routing saves (Section 3.4 and Appendix D compare per-layer
+ * and every-few-layers routing with it): layers s*group .. s*group+group-1
+ * attend over index set s, which is computed from the index query
+ * q_idx + s * q_idx_group_stride and the index keys k_idx + s *
+ * k_idx_group_stride (strides in bf16 elements, multiples of 8, >= 0; 0 reuses
+ * the same index keys for every set).  group >= n_layers is clsa_decode_step;
+ * group = 1 selects a fresh set before every layer.  idx / n_sel receive every
+ * set: [n_sets, batch, n_q, top_k] / [n_sets, batch, n_q] with
+ * n_sets = max(1, ceil(n_layers / group)).  Workspace: CLSA_OP_DECODE.  The
+ * profiling hook's first three marks bracket the first set's index pass and
+ * top-k; the fourth follows the last layer. */
+clsa_status clsa_decode_step_grouped(const clsa_shape *shape, const void *q_idx,
+                                     int64_t q_idx_group_stride, const void *k_idx,
+                                     int64_t k_idx_group_stride, const void *k_cache,
+                                     const void *v_cache, const int32_t *page_table,
+                                     const int32_t *seq_lens, const int32_t *q_pos,
+                                     int32_t n_layers, int32_t group, const void *q_layers,
+                                     void *out_layers, float *lse_layers, int32_t *idx,
+                                     int32_t *n_sel, void *ws, size_t ws_bytes, void *stream);
+
+/* Dense GQA attention (Eq. 1 with GQA: the attention that Eq. 4 restricts to
+ * S_t), for every row (b,t) and query head h over every valid key of sequence
+ * b (j < seq_lens[b], and j <= q_pos[b,t] when causal), as the reference
+ * point for the cost of the sparse path.  Same layouts, scale, output and lse
+ * conventions as clsa_sparse_attn; top_k is not used (it must still be a valid
+ * value); max_len <= 262144.  Workspace: CLSA_OP_DENSE. */
+clsa_status clsa_dense_attn(const clsa_shape *shape, const void *q, const void *k_cache,
+                            const void *v_cache, const int32_t *page_table,
+                            const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
+                            void *ws, size_t ws_bytes, void *stream);
 
 /* Static, human-readable name of a status code. */
 const char *clsa_status_string(clsa_status status);

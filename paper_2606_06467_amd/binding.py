@@ -28,6 +28,7 @@ CLSA_OP_INDEX = 0
 CLSA_OP_TOPK = 1
 CLSA_OP_ATTN = 2
 CLSA_OP_DECODE = 3
+CLSA_OP_DENSE = 4
 
 
 class ClsaError(RuntimeError):
@@ -70,13 +71,16 @@ def lib() -> ctypes.CDLL:
                            "(there is no fallback implementation)")
     L = ctypes.CDLL(LIB_PATH)
     P, SP = ctypes.c_void_p, ctypes.POINTER(ClsaShape)
-    i32, sz = ctypes.c_int32, ctypes.c_size_t
+    i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     sig = {
         "clsa_workspace_bytes": (sz, [SP, i32, i32]),
         "clsa_index_scores": (i32, [SP, P, P, P, P, P, P, P]),
         "clsa_topk": (i32, [SP, P, P, P, P, P, P, sz, P]),
         "clsa_sparse_attn": (i32, [SP, P, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_decode_step": (i32, [SP, P, P, P, P, P, P, P, i32, P, P, P, P, P, P, sz, P]),
+        "clsa_decode_step_grouped": (i32, [SP, P, i64, P, i64, P, P, P, P, P, i32, i32, P, P, P,
+                                           P, P, P, sz, P]),
+        "clsa_dense_attn": (i32, [SP, P, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_status_string": (ctypes.c_char_p, [i32]),
         "clsa_set_phase_events": (i32, [ctypes.POINTER(P), i32]),
     }
@@ -153,6 +157,31 @@ def clsa_decode_step(shape, q_idx, k_idx, k_cache, v_cache, page_table, seq_lens
                                   _ptr(out_layers, "out_layers"), _ptr(lse_layers, "lse_layers"),
                                   _ptr(idx, "idx"), _ptr(n_sel, "n_sel"), _ptr(ws, "ws"), wsb,
                                   _stream(stream)), "clsa_decode_step")
+
+
+def clsa_decode_step_grouped(shape, q_idx, q_idx_group_stride, k_idx, k_idx_group_stride,
+                             k_cache, v_cache, page_table, seq_lens, q_pos, group, q_layers,
+                             out_layers, lse_layers, idx, n_sel, ws, stream=None):
+    """Strides in bf16 elements between the index queries / keys of consecutive sets."""
+    n_layers = 0 if q_layers is None else int(q_layers.shape[0])
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().clsa_decode_step_grouped(
+        ctypes.byref(shape), _ptr(q_idx, "q_idx"), int(q_idx_group_stride), _ptr(k_idx, "k_idx"),
+        int(k_idx_group_stride), _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
+        _ptr(page_table, "page_table"), _ptr(seq_lens, "seq_lens"), _ptr(q_pos, "q_pos"),
+        n_layers, int(group), _ptr(q_layers, "q_layers"), _ptr(out_layers, "out_layers"),
+        _ptr(lse_layers, "lse_layers"), _ptr(idx, "idx"), _ptr(n_sel, "n_sel"), _ptr(ws, "ws"),
+        wsb, _stream(stream)), "clsa_decode_step_grouped")
+
+
+def clsa_dense_attn(shape, q, k_cache, v_cache, page_table, seq_lens, q_pos, out, lse=None,
+                    ws=None, stream=None):
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().clsa_dense_attn(ctypes.byref(shape), _ptr(q, "q"), _ptr(k_cache, "k_cache"),
+                                 _ptr(v_cache, "v_cache"), _ptr(page_table, "page_table"),
+                                 _ptr(seq_lens, "seq_lens"), _ptr(q_pos, "q_pos"),
+                                 _ptr(out, "out"), _ptr(lse, "lse"), _ptr(ws, "ws"), wsb,
+                                 _stream(stream)), "clsa_dense_attn")
 
 
 def clsa_set_phase_events(events: Optional[Sequence[int]]) -> None:

@@ -34,7 +34,7 @@ int log2i(int x) {
     return s;
 }
 
-enum Needs : unsigned { kIndex = 1u, kTopk = 2u, kAttn = 4u };
+enum Needs : unsigned { kIndex = 1u, kTopk = 2u, kAttn = 4u, kDense = 8u };
 
 // Checks the shape for the operations in `needs` and fills the kernel geometry.
 clsa_status check_shape(const clsa_shape *s, unsigned needs, Geometry *g) {
@@ -59,7 +59,7 @@ clsa_status check_shape(const clsa_shape *s, unsigned needs, Geometry *g) {
         if (grp != 1 && grp != 2 && grp != 4 && grp != 5 && grp != 8) return CLSA_ERR_UNSUPPORTED;
     }
     if (s->top_k > kMaxTopK) return CLSA_ERR_UNSUPPORTED;
-    if ((needs & (kIndex | kTopk)) && s->max_len > kMaxLen) return CLSA_ERR_UNSUPPORTED;
+    if ((needs & (kIndex | kTopk | kDense)) && s->max_len > kMaxLen) return CLSA_ERR_UNSUPPORTED;
     g->batch = s->batch;
     g->n_q = s->n_q;
     g->rows = s->batch * s->n_q;
@@ -144,8 +144,8 @@ struct AttnWs {
     float *partials = nullptr;
 };
 
-void carve_attn(const Geometry &g, Carver &c, AttnWs &w) {
-    w.partials = c.take<float>(clsa::attn_partial_floats(g));  // none with one split
+void carve_attn(const Geometry &g, Carver &c, AttnWs &w, bool dense = false) {
+    w.partials = c.take<float>(clsa::attn_partial_floats(g, dense));  // none with one split
 }
 
 struct DecodeWs {
@@ -187,10 +187,10 @@ size_t topk_ws_bytes(const Geometry &g) {
     return c.off;
 }
 
-size_t attn_ws_bytes(const Geometry &g) {
+size_t attn_ws_bytes(const Geometry &g, bool dense = false) {
     Carver c{nullptr};
     AttnWs w;
-    carve_attn(g, c, w);
+    carve_attn(g, c, w, dense);
     return c.off;
 }
 
@@ -211,6 +211,9 @@ size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layer
         case CLSA_OP_ATTN:
             if (check_shape(shape, kAttn, &g) != CLSA_OK) return 0;
             return attn_ws_bytes(g);
+        case CLSA_OP_DENSE:
+            if (check_shape(shape, kAttn | kDense, &g) != CLSA_OK) return 0;
+            return attn_ws_bytes(g, true);
         case CLSA_OP_DECODE: {
             // layers run one after another and reuse the same buffers
             if (check_shape(shape, kIndex | kTopk | kAttn, &g) != CLSA_OK || n_layers < 0)
@@ -285,15 +288,24 @@ clsa_status clsa_sparse_attn(const clsa_shape *shape, const void *q, const void 
                                              lse, w.partials, static_cast<hipStream_t>(stream)));
 }
 
-clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const void *k_idx,
-                             const void *k_cache, const void *v_cache,
-                             const int32_t *page_table, const int32_t *seq_lens,
-                             const int32_t *q_pos, int32_t n_layers, const void *q_layers,
-                             void *out_layers, float *lse_layers, int32_t *idx, int32_t *n_sel,
-                             void *ws, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// One index pass + one top-k per group of `group` layers, then the group's
+// layer passes; group >= n_layers is the shared-routing step.
+clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t q_idx_stride,
+                             const void *k_idx, int64_t k_idx_stride, const void *k_cache,
+                             const void *v_cache, const int32_t *page_table,
+                             const int32_t *seq_lens, const int32_t *q_pos, int32_t n_layers,
+                             int32_t group, const void *q_layers, void *out_layers,
+                             float *lse_layers, int32_t *idx, int32_t *n_sel, void *ws,
+                             size_t ws_bytes, void *stream) {
     Geometry g;
     CLSA_TRY(check_shape(shape, kIndex | kTopk | kAttn, &g));
-    if (n_layers < 0) return CLSA_ERR_INVALID_ARG;
+    if (n_layers < 0 || group < 1 || q_idx_stride < 0 || k_idx_stride < 0)
+        return CLSA_ERR_INVALID_ARG;
+    if (q_idx_stride % 8 || k_idx_stride % 8) return CLSA_ERR_INVALID_ARG;  // 16-byte aligned sets
     CLSA_TRY(check_ptr(q_idx, 16));
     CLSA_TRY(check_ptr(k_idx, 16));
     CLSA_TRY(check_ptr(seq_lens, 4));
@@ -319,33 +331,96 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
     // without the coarse histogram, which the top-k then makes itself.  The
     // histogram and counters need clearing unless that top-k is the per-row one.
     const bool mfma = clsa::index_uses_mfma(g);
-    if (!mfma || clsa::topk_uses_wide(g))
-        CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
-    if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
-    if (mfma)
-        CLSA_TRY(from_hip(clsa::launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos,
-                                                     w.scores, st)));
-    else
-        CLSA_TRY(from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos,
-                                                    w.scores, w.topk.hist, st)));
-    if (hook && hipEventRecord(g_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
-    CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, idx, n_sel,
-                                        st)));
-    if (hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
     const size_t q_stride = (size_t)g.rows * g.q_heads * 128;  // bf16 elements per layer
     const size_t lse_stride = (size_t)g.rows * g.q_heads;
-    for (int l = 0; l < n_layers; ++l) {
-        const uint16_t *ql = static_cast<const uint16_t *>(q_layers) + l * q_stride;
-        uint16_t *ol = static_cast<uint16_t *>(out_layers) + l * q_stride;
-        float *lsel = lse_layers ? lse_layers + l * lse_stride : nullptr;
-        const bool mark = hook && l < g_hook.layers;
-        if (mark && hipEventRecord(g_hook.ev[4 + 2 * l], st) != hipSuccess) return CLSA_ERR_HIP;
-        CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, idx, n_sel,
-                                                   ol, lsel, w.partials, st,
-                                                   mark ? g_hook.ev[5 + 2 * l] : nullptr)));
+    const size_t set_stride = (size_t)g.rows * g.top_k;         // index entries per set
+    const int n_sets = n_layers > 0 ? (n_layers + group - 1) / group : 1;
+    for (int s = 0; s < n_sets; ++s) {
+        const uint16_t *qi = static_cast<const uint16_t *>(q_idx) + (size_t)s * q_idx_stride;
+        const uint16_t *ki = static_cast<const uint16_t *>(k_idx) + (size_t)s * k_idx_stride;
+        int32_t *is = idx + (size_t)s * set_stride;
+        int32_t *ns = n_sel + (size_t)s * g.rows;
+        const bool first = s == 0;
+        if (!mfma || clsa::topk_uses_wide(g))
+            CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
+        if (first && hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+        if (mfma)
+            CLSA_TRY(from_hip(clsa::launch_index_prefill(g, qi, ki, page_table, seq_lens, q_pos,
+                                                         w.scores, st)));
+        else
+            CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
+                                                        w.scores, w.topk.hist, st)));
+        if (first && hook && hipEventRecord(g_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
+        CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, is, ns,
+                                            st)));
+        if (first && hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
+        const int l_end = n_layers < (s + 1) * group ? n_layers : (s + 1) * group;
+        for (int l = s * group; l < l_end; ++l) {
+            const uint16_t *ql = static_cast<const uint16_t *>(q_layers) + l * q_stride;
+            uint16_t *ol = static_cast<uint16_t *>(out_layers) + l * q_stride;
+            float *lsel = lse_layers ? lse_layers + l * lse_stride : nullptr;
+            const bool mark = hook && l < g_hook.layers;
+            if (mark && hipEventRecord(g_hook.ev[4 + 2 * l], st) != hipSuccess)
+                return CLSA_ERR_HIP;
+            CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, is,
+                                                       ns, ol, lsel, w.partials, st,
+                                                       mark ? g_hook.ev[5 + 2 * l] : nullptr)));
+        }
     }
     if (hook && hipEventRecord(g_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
     return CLSA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const void *k_idx,
+                             const void *k_cache, const void *v_cache,
+                             const int32_t *page_table, const int32_t *seq_lens,
+                             const int32_t *q_pos, int32_t n_layers, const void *q_layers,
+                             void *out_layers, float *lse_layers, int32_t *idx, int32_t *n_sel,
+                             void *ws, size_t ws_bytes, void *stream) {
+    const int32_t group = n_layers > 0 ? n_layers : 1;
+    return decode_step_impl(shape, q_idx, 0, k_idx, 0, k_cache, v_cache, page_table, seq_lens,
+                            q_pos, n_layers, group, q_layers, out_layers, lse_layers, idx, n_sel,
+                            ws, ws_bytes, stream);
+}
+
+clsa_status clsa_decode_step_grouped(const clsa_shape *shape, const void *q_idx,
+                                     int64_t q_idx_group_stride, const void *k_idx,
+                                     int64_t k_idx_group_stride, const void *k_cache,
+                                     const void *v_cache, const int32_t *page_table,
+                                     const int32_t *seq_lens, const int32_t *q_pos,
+                                     int32_t n_layers, int32_t group, const void *q_layers,
+                                     void *out_layers, float *lse_layers, int32_t *idx,
+                                     int32_t *n_sel, void *ws, size_t ws_bytes, void *stream) {
+    return decode_step_impl(shape, q_idx, q_idx_group_stride, k_idx, k_idx_group_stride, k_cache,
+                            v_cache, page_table, seq_lens, q_pos, n_layers, group, q_layers,
+                            out_layers, lse_layers, idx, n_sel, ws, ws_bytes, stream);
+}
+
+clsa_status clsa_dense_attn(const clsa_shape *shape, const void *q, const void *k_cache,
+                            const void *v_cache, const int32_t *page_table,
+                            const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
+                            void *ws, size_t ws_bytes, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kAttn | kDense, &g));
+    CLSA_TRY(check_ptr(q, 16));
+    CLSA_TRY(check_ptr(k_cache, 16));
+    CLSA_TRY(check_ptr(v_cache, 16));
+    CLSA_TRY(check_ptr(seq_lens, 4));
+    CLSA_TRY(check_ptr(out, 16));
+    if (lse) CLSA_TRY(check_ptr(lse, 4));
+    CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
+    const size_t need = attn_ws_bytes(g, true);
+    if (need && (!ws || ws_bytes < need || !aligned(ws, kAlign))) return CLSA_ERR_WORKSPACE;
+    Carver c{static_cast<char *>(ws)};
+    AttnWs w;
+    carve_attn(g, c, w, true);
+    return from_hip(clsa::launch_dense_attn(g, q, k_cache, v_cache, page_table, seq_lens, q_pos,
+                                            out, lse, w.partials,
+                                            static_cast<hipStream_t>(stream)));
 }
 
 const char *clsa_status_string(clsa_status status) {

@@ -72,7 +72,8 @@ hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *se
 hipError_t launch_zero_u32(uint32_t *p, size_t n, hipStream_t stream);
 
 // ---- sparse_attn.hip ----
-size_t attn_partial_floats(const Geometry &g);  // 0 when one split per (row, KV head)
+// Partial buffer floats (0 when one split per (row, KV head)); dense: over max_len keys.
+size_t attn_partial_floats(const Geometry &g, bool dense = false);
 // Attention gathering K/V rows from the cache through idx (and the page table).
 // split_done, if not null, is recorded right after the attention kernel, before
 // the split merge.
@@ -81,5 +82,11 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
                               float *partials, hipStream_t stream,
                               hipEvent_t split_done = nullptr);
+// Dense attention of every row over all of its valid keys (seq_lens, and q_pos
+// when causal), same layouts as the sparse call.
+hipError_t launch_dense_attn(const Geometry &g, const void *q, const void *k_cache,
+                             const void *v_cache, const int32_t *page_table,
+                             const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
+                             float *partials, hipStream_t stream);
 
 }  // namespace clsa

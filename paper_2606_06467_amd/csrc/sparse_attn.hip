@@ -24,6 +24,10 @@
 // the exact log-sum-exp rule.  The merge is a second launch rather than a
 // "last workgroup merges" ticket: the agent-scope release fence such a ticket
 // needs writes back the whole L2 of the XCD from every workgroup on this chip.
+// The same kernels serve dense attention over every valid key (Eq. 1, the
+// attention that Eq. 4 restricts), used as the reference point for the cost of
+// sparse attention: token positions then come straight from the chunk, with no
+// index list.
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -32,20 +36,23 @@ namespace clsa {
 constexpr int kHeadDim = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kMaxSplits = 128;  // top_k <= 8192 in 64-token chunks
+constexpr int kMaxSplits = 128;  // splits per (row, KV head): the merge's largest shape
 
 struct AttnArgs {
     const uint16_t *q;
     const uint16_t *k;
     const uint16_t *v;
     const int32_t *page_table;
-    const int32_t *idx;
-    const int32_t *n_sel;
+    const int32_t *idx;      // sparse: [rows, top_k] selected positions
+    const int32_t *n_sel;    // sparse: [rows] their count
+    const int32_t *seq_lens; // dense: [batch]
+    const int32_t *q_pos;    // dense, causal: [rows]
     uint16_t *out;
     float *lse;          // may be null
     float *part_o;       // [rows, Hq, splits, 128]
     float *part_ml;      // [rows, Hq, splits, 2]
     int n_q, max_len, page_shift, max_pages, top_k, kv_heads, q_heads, splits, chunks_per_split;
+    int causal;
     float scale_log2;    // softmax_scale * log2(e)
 };
 
@@ -53,7 +60,16 @@ __host__ __device__ constexpr int pow2_at_least(int x) {
     return x <= 1 ? 1 : 2 * pow2_at_least((x + 1) / 2);
 }
 
-template <int G, bool PAGED>
+// Keys of row `row`: the first n_sel entries of its index list, or (DENSE) every
+// valid position 0 .. n-1 in order, n = its sequence length (causal: up to its
+// own position).
+template <bool DENSE>
+__device__ __forceinline__ int row_keys(const AttnArgs &a, int row) {
+    if (DENSE) return valid_keys(a.seq_lens, a.q_pos, a.causal, row / a.n_q, row, a.max_len);
+    return min(max(a.n_sel[row], 0), a.top_k);
+}
+
+template <int G, bool PAGED, bool DENSE>
 __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
     constexpr int NO = pow2_at_least(8 * G);   // accumulators per lane before the reduction
@@ -73,15 +89,16 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     const int span = a.chunks_per_split * 64;
     const int tok_begin = split * span;
     const int row_elems = a.kv_heads * kHeadDim;
-    const int32_t *sel = a.idx + (size_t)row * a.top_k;
+    const int32_t *sel = DENSE ? nullptr : a.idx + (size_t)row * a.top_k;
 
     // Index loads of the first chunk do not wait for n_sel: the index list has
     // top_k entries (padding included), so any position below top_k is readable.
     int jpre[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        jpre[i] = sel[min(tok_begin + i * 16 + wave * 4 + qq, a.top_k - 1)];
-    const int n = min(max(a.n_sel[row], 0), a.top_k);
+        jpre[i] = DENSE ? tok_begin + i * 16 + wave * 4 + qq
+                        : sel[min(tok_begin + i * 16 + wave * 4 + qq, a.top_k - 1)];
+    const int n = row_keys<DENSE>(a, row);
     const int nsplit = div_up(n, span);  // splits that hold tokens
 
     if (n == 0) {  // empty index set: output 0, lse -inf
@@ -113,7 +130,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     for (int c0 = tok_begin; c0 < tok_end; c0 += 64) {
         int jr[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) jr[i] = min(max(jpre[i], 0), a.max_len - 1);  // -1 pad -> row 0
+        for (int i = 0; i < 4; ++i)  // -1 padding -> row 0; dense positions past n -> row n-1
+            jr[i] = DENSE ? min(jpre[i], n - 1) : min(max(jpre[i], 0), a.max_len - 1);
         uint32_t trow[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -134,7 +152,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         // prefetch the next chunk's indices (clamped, so always readable)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            jpre[i] = sel[min(c0 + 64 + i * 16 + wave * 4 + qq, a.top_k - 1)];
+            jpre[i] = DENSE ? c0 + 64 + i * 16 + wave * 4 + qq
+                            : sel[min(c0 + 64 + i * 16 + wave * 4 + qq, a.top_k - 1)];
         // All K and V gathers of the chunk are in flight before any math (without
         // this the scheduler sinks the V loads below the logits, which costs a
         // second memory round trip per chunk).
@@ -252,7 +271,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 // o) is issued in one batch before the first wait: splits past the row's last
 // one are read anyway (the buffer holds `splits` slots) and masked afterwards,
 // so the kernel costs one memory round trip.
-template <int SPT>  // splits per thread (8 * SPT >= splits)
+template <int SPT, bool DENSE>  // SPT: splits per thread (8 * SPT >= splits)
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     __shared__ float s_max[8], s_l[8];
     __shared__ float4 s_o[8][32];
@@ -268,7 +287,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
         o[j] = *reinterpret_cast<const float4 *>(a.part_o + (base + s) * kHeadDim + dq * 4);
         ml[j] = *reinterpret_cast<const float2 *>(a.part_ml + (base + s) * 2);
     }
-    const int n = min(max(a.n_sel[row], 0), a.top_k);
+    const int n = row_keys<DENSE>(a, row);
     const int nsplit = div_up(n, a.chunks_per_split * 64);  // splits that hold tokens
     if (nsplit == 0) return;  // the attention kernel wrote the empty-set result
     float mx = -INFINITY;
@@ -317,53 +336,69 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 // least two 64-token chunks per split while that still leaves 256 workgroups,
 // so that a workgroup's second chunk of gathers overlaps its first chunk's
 // arithmetic (measured best on the 128K, 32K and ragged-batch workloads; the
-// 4K single-sequence step prefers one chunk per split).
-static void plan_splits(const Geometry &g, int &splits, int &chunks_per_split) {
-    const int chunks = div_up(g.top_k, 64);
+// 4K single-sequence step prefers one chunk per split).  keys: the most keys
+// a row can have (top_k, or max_len for dense attention).
+static void plan_splits(const Geometry &g, int keys, int &splits, int &chunks_per_split) {
+    const int chunks = div_up(keys, 64);
     const long units = (long)g.rows * g.kv_heads;
     long want = units > 0 ? (1024 + units - 1) / units : 1;
     const long cap = units * (chunks / 2) >= 256 ? chunks / 2 : chunks;
     if (want > cap) want = cap;
+    if (want > kMaxSplits) want = kMaxSplits;
     if (want < 1) want = 1;
     chunks_per_split = div_up(chunks, (int)want);
     splits = div_up(chunks, chunks_per_split);
 }
 
-size_t attn_partial_floats(const Geometry &g) {
+size_t attn_partial_floats(const Geometry &g, bool dense) {
     int splits, cps;
-    plan_splits(g, splits, cps);
+    plan_splits(g, dense ? g.max_len : g.top_k, splits, cps);
     if (splits == 1) return 0;
     return (size_t)g.rows * g.q_heads * splits * (kHeadDim + 2);
 }
 
-template <int G>
+template <int G, bool DENSE>
 static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int units,
                                 hipStream_t stream, hipEvent_t split_done) {
-    if (paged) sparse_attn_kernel<G, true><<<grid, dim3(256), 0, stream>>>(a);
-    else sparse_attn_kernel<G, false><<<grid, dim3(256), 0, stream>>>(a);
+    if (paged) sparse_attn_kernel<G, true, DENSE><<<grid, dim3(256), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false, DENSE><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1) return e;
     const dim3 mgrid(units), mblock(256);
-    if (a.splits <= 8) attn_merge_kernel<1><<<mgrid, mblock, 0, stream>>>(a);
-    else if (a.splits <= 16) attn_merge_kernel<2><<<mgrid, mblock, 0, stream>>>(a);
-    else if (a.splits <= 32) attn_merge_kernel<4><<<mgrid, mblock, 0, stream>>>(a);
-    else if (a.splits <= 64) attn_merge_kernel<8><<<mgrid, mblock, 0, stream>>>(a);
-    else attn_merge_kernel<16><<<mgrid, mblock, 0, stream>>>(a);
+    if (a.splits <= 8) attn_merge_kernel<1, DENSE><<<mgrid, mblock, 0, stream>>>(a);
+    else if (a.splits <= 16) attn_merge_kernel<2, DENSE><<<mgrid, mblock, 0, stream>>>(a);
+    else if (a.splits <= 32) attn_merge_kernel<4, DENSE><<<mgrid, mblock, 0, stream>>>(a);
+    else if (a.splits <= 64) attn_merge_kernel<8, DENSE><<<mgrid, mblock, 0, stream>>>(a);
+    else attn_merge_kernel<16, DENSE><<<mgrid, mblock, 0, stream>>>(a);
     return hipGetLastError();
 }
 
-hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
-                              const void *v_cache, const int32_t *page_table,
-                              const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
-                              float *partials, hipStream_t stream, hipEvent_t split_done) {
+template <bool DENSE>
+static hipError_t launch_attn(const Geometry &g, const AttnArgs &a, bool paged, dim3 grid,
+                              int units, hipStream_t stream, hipEvent_t split_done) {
+    switch (g.group) {
+        case 1: return launch_attn_g<1, DENSE>(a, paged, grid, units, stream, split_done);
+        case 2: return launch_attn_g<2, DENSE>(a, paged, grid, units, stream, split_done);
+        case 4: return launch_attn_g<4, DENSE>(a, paged, grid, units, stream, split_done);
+        case 5: return launch_attn_g<5, DENSE>(a, paged, grid, units, stream, split_done);
+        case 8: return launch_attn_g<8, DENSE>(a, paged, grid, units, stream, split_done);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+static AttnArgs attn_args(const Geometry &g, const void *q, const void *k_cache,
+                          const void *v_cache, const int32_t *page_table, void *out, float *lse,
+                          float *partials, int keys) {
     AttnArgs a;
     a.q = static_cast<const uint16_t *>(q);
     a.k = static_cast<const uint16_t *>(k_cache);
     a.v = static_cast<const uint16_t *>(v_cache);
     a.page_table = page_table;
-    a.idx = idx;
-    a.n_sel = n_sel;
+    a.idx = nullptr;
+    a.n_sel = nullptr;
+    a.seq_lens = nullptr;
+    a.q_pos = nullptr;
     a.out = static_cast<uint16_t *>(out);
     a.lse = lse;
     a.n_q = g.n_q;
@@ -373,25 +408,43 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
     a.top_k = g.top_k;
     a.kv_heads = g.kv_heads;
     a.q_heads = g.q_heads;
-    plan_splits(g, a.splits, a.chunks_per_split);
+    a.causal = g.causal;
+    plan_splits(g, keys, a.splits, a.chunks_per_split);
     a.scale_log2 = g.softmax_scale * kLog2e;
     const size_t part_o = (size_t)g.rows * g.q_heads * a.splits * kHeadDim;
     a.part_o = a.splits > 1 ? partials : nullptr;
     a.part_ml = a.splits > 1 ? partials + part_o : nullptr;
+    return a;
+}
+
+hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
+                              const void *v_cache, const int32_t *page_table,
+                              const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
+                              float *partials, hipStream_t stream, hipEvent_t split_done) {
+    AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, g.top_k);
+    a.idx = idx;
+    a.n_sel = n_sel;
     if (g.rows == 0) return hipSuccess;
     const size_t blocks = (size_t)g.rows * g.kv_heads * a.splits;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
-    const dim3 grid((unsigned)blocks);
-    const bool paged = g.page_shift >= 0;
     const int units = g.rows * g.q_heads;  // merge workgroups: one per (row, query head)
-    switch (g.group) {
-        case 1: return launch_attn_g<1>(a, paged, grid, units, stream, split_done);
-        case 2: return launch_attn_g<2>(a, paged, grid, units, stream, split_done);
-        case 4: return launch_attn_g<4>(a, paged, grid, units, stream, split_done);
-        case 5: return launch_attn_g<5>(a, paged, grid, units, stream, split_done);
-        case 8: return launch_attn_g<8>(a, paged, grid, units, stream, split_done);
-        default: return hipErrorInvalidValue;
-    }
+    return launch_attn<false>(g, a, g.page_shift >= 0, dim3((unsigned)blocks), units, stream,
+                              split_done);
+}
+
+hipError_t launch_dense_attn(const Geometry &g, const void *q, const void *k_cache,
+                             const void *v_cache, const int32_t *page_table,
+                             const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
+                             float *partials, hipStream_t stream) {
+    AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, g.max_len);
+    a.seq_lens = seq_lens;
+    a.q_pos = q_pos;
+    if (g.rows == 0) return hipSuccess;
+    const size_t blocks = (size_t)g.rows * g.kv_heads * a.splits;
+    if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
+    const int units = g.rows * g.q_heads;
+    return launch_attn<true>(g, a, g.page_shift >= 0, dim3((unsigned)blocks), units, stream,
+                             nullptr);
 }
 
 }  // namespace clsa

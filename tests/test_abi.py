@@ -30,7 +30,8 @@ def declared_functions():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("clsa_index_scores", "clsa_topk", "clsa_sparse_attn", "clsa_decode_step",
-              "clsa_workspace_bytes", "clsa_status_string", "clsa_set_phase_events"):
+              "clsa_decode_step_grouped", "clsa_dense_attn", "clsa_workspace_bytes",
+              "clsa_status_string", "clsa_set_phase_events"):
         assert n in names
 
 
@@ -203,3 +204,36 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="no fallback"):
         B.lib()
+
+
+def _grouped_call(lib, sh, ws=A, wsb=1 << 30, group=1, sq=0, sk=0, L=2):
+    return lib.clsa_decode_step_grouped(ctypes.byref(sh), A, sq, A, sk, A, A, None, A, None, L,
+                                        group, A, A, None, A, A, ws, wsb, None)
+
+
+def test_grouped_step_checks(lib):
+    sh = _shape()
+    assert _grouped_call(lib, sh, group=0) == -1
+    assert _grouped_call(lib, sh, group=-3) == -1
+    assert _grouped_call(lib, sh, sq=4) == -1          # set strides keep 16-byte alignment
+    assert _grouped_call(lib, sh, sk=-8) == -1
+    assert _grouped_call(lib, sh, L=-1) == -1
+    assert _grouped_call(lib, sh, ws=None) == -3
+    assert _grouped_call(lib, _shape(head_dim=64)) == -2
+
+
+def test_dense_attn_checks(lib):
+    from paper_2606_06467_amd import binding as B
+    def call(sh, ws=None, wsb=0, q=A, sl=A, qp=None):
+        return lib.clsa_dense_attn(ctypes.byref(sh), q, A, A, None, sl, qp, A, None, ws, wsb, None)
+    sh = _shape(batch=4, max_len=131072, top_k=2048)
+    need = B.clsa_workspace_bytes(sh, B.CLSA_OP_DENSE)
+    assert need > B.clsa_workspace_bytes(sh, B.CLSA_OP_ATTN)   # splits over every key
+    assert call(sh, ws=None, wsb=0) == -3
+    assert call(sh, ws=A, wsb=need - 1) == -3
+    assert call(sh, ws=A, wsb=need, q=MIS) == -1
+    assert call(sh, ws=A, wsb=need, sl=None) == -1
+    assert call(_shape(causal=True), ws=A, wsb=1 << 30) == -1      # causal needs q_pos
+    assert call(_shape(max_len=262144 * 2), ws=A, wsb=1 << 30) == -2
+    assert call(_shape(head_dim=96), ws=A, wsb=1 << 30) == -2
+    assert B.clsa_workspace_bytes(_shape(max_len=262144 * 2), B.CLSA_OP_DENSE) == 0

@@ -120,3 +120,65 @@ def test_full_decode_b32_ragged_paged():
     w = inputs.workload("decode_b32_ragged_paged")
     x = inputs.make_inputs(w)
     _check_step(w, x, [0, w.n_layers - 1], w.name)
+
+
+def _grouped(w, q_idx_sets, k_idx_sets, x, group, stride_q, stride_k):
+    import torch
+    from paper_2606_06467_amd import binding as B
+    d = U.to_dev(x)
+    qi, ki = B.bf16_from_bits(q_idx_sets), B.bf16_from_bits(k_idx_sets)
+    L = x["q_layers"].shape[0]
+    n_sets = max(1, -(-L // group))
+    out = torch.full((L, w.batch, w.n_q, w.q_heads, w.head_dim), float("nan"),
+                     dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((L, w.batch, w.n_q, w.q_heads), float("nan"), device="cuda")
+    idx = torch.full((n_sets, w.batch, w.n_q, w.top_k), -7, dtype=torch.int32, device="cuda")
+    ns = torch.full((n_sets, w.batch, w.n_q), -7, dtype=torch.int32, device="cuda")
+    sh = U.shape_of(w)
+    ws = B.workspace(sh, B.CLSA_OP_DECODE, L)
+    B.clsa_decode_step_grouped(sh, qi, stride_q, ki, stride_k, d["k_cache"], d["v_cache"],
+                               d["page_table"], d["seq_lens"], d["q_pos"], group, d["q_layers"],
+                               out, lse, idx, ns, ws)
+    torch.cuda.synchronize()
+    return (B.bits_from_bf16(out), lse.cpu().numpy().astype(np.float64), idx.cpu().numpy(),
+            ns.cpu().numpy())
+
+
+def test_grouped_fresh_routing_per_layer():
+    """group = 1 with a different indexer per layer: layer l attends over the set
+    its own index keys select (per-layer routing)."""
+    w = inputs.small_workload(batch=2, lens=(5000, 3100), top_k=512, n_layers=3, wid=96)
+    x = inputs.make_inputs(w)
+    sets = [inputs.make_inputs(w, seed_base=1000 * w.wid + 10000 * (s + 1), index_only=True)
+            for s in range(3)]
+    q_sets = np.stack([s_["q_idx"] for s_ in sets])
+    k_sets = np.stack([s_["k_idx"] for s_ in sets])
+    out, lse, gidx, gns = _grouped(w, q_sets, k_sets, x, 1, q_sets[0].size, k_sets[0].size)
+    sh = orc.shape_of(w)
+    for l in range(3):
+        scores = orc.index_scores(sh, q_sets[l], k_sets[l], x["seq_lens"], x["q_pos"],
+                                  x["page_table"])
+        oidx, ons = orc.topk(sh, scores.astype(np.float32), x["seq_lens"], x["q_pos"])
+        U.check_index_sets(w, sh, scores, gidx[l], gns[l], x["seq_lens"], x["q_pos"],
+                           ref=(oidx, ons), bound=U.higham_bound(w, dict(x, q_idx=q_sets[l],
+                                                                          k_idx=k_sets[l])))
+        same = np.array([[np.array_equal(gidx[l][b, t], oidx[b, t]) for t in range(w.n_q)]
+                         for b in range(w.batch)])
+        ro, rl = orc.sparse_attn(sh, x["q_layers"][l], x["k_cache"], x["v_cache"], oidx, ons,
+                                 x["page_table"])
+        U.compare_attn(out[l], lse[l], ro, rl, mask_rows=same, what=f"per-layer routing l={l}")
+
+
+def test_grouped_reused_keys_match_the_shared_step():
+    """group = 2 over 3 layers with the same index keys for both sets: every set
+    and every layer output equals the shared-routing step's, bit for bit."""
+    w = inputs.small_workload(batch=3, lens=(4000, 2500, 700), top_k=1024, n_layers=3,
+                              page_size=64, wid=97)
+    x = inputs.make_inputs(w)
+    out0, lse0, idx0, ns0 = _gpu_step(w, x, 3)
+    out, lse, gidx, gns = _grouped(w, x["q_idx"], x["k_idx"], x, 2, 0, 0)
+    for s in range(2):
+        np.testing.assert_array_equal(gidx[s], idx0)
+        np.testing.assert_array_equal(gns[s], ns0)
+    np.testing.assert_array_equal(out, out0)
+    np.testing.assert_array_equal(lse, lse0)
