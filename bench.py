@@ -152,6 +152,76 @@ def cpu_baseline(w, x, budget_s: float):
             "sample": sample}
 
 
+def run_schedules(args, w) -> int:
+    """Per-layer decode cost of routing schedules on one workload.
+
+    * shared: one index pass + one top-k, every layer reuses the set (the
+      method's schedule, clsa_decode_step);
+    * every 4 / every layer: the set is recomputed every 4 layers / before
+      every layer (clsa_decode_step_grouped), each set from its own copy of the
+      index keys (so that every index pass reads HBM like a distinct indexer);
+    * dense: every layer attends over all valid keys (clsa_dense_attn).
+    Each is timed over K steps after W warm-up steps."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    from paper_2606_06467_amd import inputs
+    log(f"[schedules] generating {w.name} ...")
+    x = inputs.make_inputs(w)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bf = lambda a: B.bf16_from_bits(a, dev)
+    q_idx, k_idx = bf(x["q_idx"]), bf(x["k_idx"])
+    kc, vc, ql = bf(x["k_cache"]), bf(x["v_cache"]), bf(x["q_layers"])
+    seq_lens = torch.from_numpy(x["seq_lens"]).to(dev)
+    q_pos = None if x["q_pos"] is None else torch.from_numpy(x["q_pos"]).to(dev)
+    pt = None if x["page_table"] is None else torch.from_numpy(x["page_table"]).to(dev)
+    sh = B.make_shape(batch=w.batch, n_q=w.n_q, max_len=w.max_len, top_k=w.top_k,
+                      q_heads=w.q_heads, kv_heads=w.kv_heads, page_size=w.page_size,
+                      max_pages=w.max_pages, causal=w.causal)
+    L = w.n_layers
+    out = torch.empty((L, w.batch, w.n_q, w.q_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((L, w.batch, w.n_q, w.q_heads), dtype=torch.float32, device=dev)
+    ws = B.workspace(sh, B.CLSA_OP_DECODE, L, dev)
+    wsd = B.workspace(sh, B.CLSA_OP_DENSE, 0, dev)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) * 1e6 / args.steps
+
+    res = {}
+    for name, group in (("shared", L), ("every 4 layers", 4), ("every layer", 1)):
+        n_sets = max(1, -(-L // group))
+        qi = q_idx.unsqueeze(0).repeat(n_sets, *([1] * q_idx.dim())).contiguous()
+        ki = k_idx.unsqueeze(0).repeat(n_sets, *([1] * k_idx.dim())).contiguous()
+        idx = torch.empty((n_sets, w.batch, w.n_q, w.top_k), dtype=torch.int32, device=dev)
+        ns = torch.empty((n_sets, w.batch, w.n_q), dtype=torch.int32, device=dev)
+        fn = lambda: B.clsa_decode_step_grouped(sh, qi, q_idx.numel(), ki, k_idx.numel(), kc, vc,
+                                                pt, seq_lens, q_pos, group, ql, out, lse, idx, ns,
+                                                ws)
+        log(f"[schedules] {name} ...")
+        us = timed(fn)
+        res[name] = {"index_sets": n_sets, "step_us": round(us, 2),
+                     "per_layer_us": round(us / L, 2)}
+        del qi, ki
+    log("[schedules] dense ...")
+
+    def dense_step():
+        for l in range(L):
+            B.clsa_dense_attn(sh, ql[l], kc, vc, pt, seq_lens, q_pos, out[l], lse[l], wsd)
+    us = timed(dense_step)
+    res["dense"] = {"step_us": round(us, 2), "per_layer_us": round(us / L, 2)}
+    print(json.dumps({"metric": "per-layer decode cost by routing schedule", "unit": "us",
+                      "workload": w.name, "layers": L, "steps": args.steps,
+                      "warmup": args.warmup, "schedules": res}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -163,6 +233,10 @@ def main() -> int:
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the timed steps, run plain device-to-device copies of this "
                          "many MiB (a known-size reference for hardware byte counters)")
+    ap.add_argument("--schedules", action="store_true",
+                    help="instead of the step benchmark, compare routing schedules on the "
+                         "workload: one shared index set, a fresh set every 4 layers, a fresh "
+                         "set every layer, and dense attention (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the decode path "
@@ -175,6 +249,8 @@ def main() -> int:
     from paper_2606_06467_amd import inputs
 
     w = inputs.workload(args.workload)
+    if args.schedules:
+        return run_schedules(args, w)
     if w.n_q != 1:
         log("note: chunked-prefill workload timed through the decode-step entry point")
     log(f"[bench] generating {w.name} ...")
