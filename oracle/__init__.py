@@ -78,7 +78,9 @@ def _load():
     lib.oracle_topk.argtypes = [SP, P, P, P, P, P]
     lib.oracle_sparse_attn.argtypes = [SP, P, P, P, P, P, P, P, P]
     lib.oracle_decode_step.argtypes = [SP, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, P, P, P]
-    for f in ("oracle_index_scores", "oracle_topk", "oracle_sparse_attn", "oracle_decode_step"):
+    lib.oracle_project.argtypes = [SP, ctypes.c_int, P, P, ctypes.c_int, P, P, P, P]
+    for f in ("oracle_index_scores", "oracle_topk", "oracle_sparse_attn", "oracle_decode_step",
+              "oracle_project"):
         getattr(lib, f).restype = None
     _lib = lib
     return lib
@@ -133,6 +135,24 @@ def sparse_attn(sh: Shape, q, k_cache, v_cache, idx, n_sel, page_table=None):
     lib.oracle_sparse_attn(ctypes.byref(sh), _p(q), _p(k_cache), _p(v_cache), _p(page_table),
                            _p(idx), _p(n_sel), _p(out), _p(lse))
     return out, lse
+
+
+def project(sh: Shape, h, w, pos, page_table=None):
+    """Eq. 2 for new tokens: (out [rows, n_out] fp64 = h w^T, dest [rows] int64 cache
+    row of each token, -1 outside [0, max_len)); h [rows, d_model], w [n_out, d_model]
+    as bf16 bits."""
+    lib = _load()
+    h, w = _c(h, np.uint16), _c(w, np.uint16)
+    pos, page_table = _c(pos, np.int32), _c(page_table, np.int32)
+    rows = sh.batch * sh.n_q
+    d_model = h.shape[-1]
+    n_out = w.shape[0]
+    assert h.size == rows * d_model and w.shape[1] == d_model and pos.size == rows
+    out = np.empty((rows, n_out), dtype=np.float64)
+    dest = np.empty(rows, dtype=np.int64)
+    lib.oracle_project(ctypes.byref(sh), int(d_model), _p(h), _p(w), int(n_out), _p(pos),
+                       _p(page_table), _p(out), _p(dest))
+    return out, dest
 
 
 def decode_step(sh: Shape, q_idx, k_idx, k_cache, v_cache, seq_lens, q_layers, q_pos=None,

@@ -19,6 +19,10 @@
  *   oracle_topk          Section 2.1, Eq. (3): S_t = TopK(I_t, k).
  *   oracle_sparse_attn   Section 2.1, Eq. (4): O_t = Attn(Q_t, K_{S_t}, V_{S_t}),
  *                        softmax attention of Eq. (1) restricted to S_t, with GQA.
+ *   oracle_project       Section 2.1, Eq. (2): Q_idx = H W_idx^Q, K_idx = H W_idx^K,
+ *                        and the shared K = H W^K, V = H W^V of the same hidden
+ *                        states, for new tokens, with the cache row each of
+ *                        them occupies.
  *   oracle_decode_step   Section 2.1 last paragraph and Section 2.3 ("compute
  *                        top-k once"): one index pass, one top-k, then every
  *                        layer reuses the same S_t.
@@ -224,4 +228,28 @@ void oracle_decode_step(const oracle_shape *s, const uint16_t *q_idx, const uint
         oracle_sparse_attn(s, q_layers + l * per_layer_q, k_cache, v_cache, page_table, idx, n_sel,
                            out_layers + l * per_layer_q,
                            lse_layers ? lse_layers + l * per_layer_lse : NULL);
+}
+
+/* Eq. (2) for the new tokens of a step: out[r, c] = sum_i h[r, i] * w[c, i],
+ * with the output features' weight vectors stacked in w (rows 0..255 the index
+ * query W_idx^Q, then the index key W_idx^K, then K, then V), and dest[r] the
+ * cache row that token pos[r] of sequence r / n_q occupies (-1 when pos[r] is
+ * outside [0, max_len)). */
+void oracle_project(const oracle_shape *s, int d_model, const uint16_t *h, const uint16_t *w,
+                    int n_out, const int32_t *pos, const int32_t *page_table, double *out,
+                    int64_t *dest)
+{
+    const int rows = s->batch * s->n_q;
+    for (int r = 0; r < rows; r++) {
+        for (int c = 0; c < n_out; c++) {
+            double acc = 0.0;
+            for (int i = 0; i < d_model; i++)
+                acc += oracle_bf16_to_double(h[(size_t)r * d_model + i]) *
+                       oracle_bf16_to_double(w[(size_t)c * d_model + i]);
+            out[(size_t)r * n_out + c] = acc;
+        }
+        const int b = r / s->n_q;
+        const int p = pos[r];
+        dest[r] = (p < 0 || p >= s->max_len) ? -1 : (int64_t)token_row(s, page_table, b, p, 1);
+    }
 }

@@ -14,6 +14,7 @@ import oracle
 from tests import test_oracle_attn as A
 from tests import test_oracle_decode_step as DS
 from tests import test_oracle_index as I
+from tests import test_oracle_project as PJ
 from tests import test_oracle_topk as T
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "clsa_oracle.c")
@@ -28,9 +29,17 @@ PINS = [
     A.test_matches_masked_sdpa, A.test_lse_matches_scipy, A.test_single_token_returns_its_value_row,
     A.test_gqa_head_mapping, A.test_empty_set,
     lambda o: DS.test_step_matches_library_composition(o, 100),
+    PJ.test_matches_numpy_float64, PJ.test_exact_on_small_integers, PJ.test_unit_vector_probe,
+    PJ.test_destination_rows,
 ]
 
 MUTANTS = {
+    "projection_weight_transposed": ("oracle_bf16_to_double(w[(size_t)c * d_model + i]);",
+                                     "oracle_bf16_to_double(w[(size_t)i * n_out + c]);"),
+    "projection_drops_last_term": ("for (int i = 0; i < d_model; i++)\n                acc +=",
+                                   "for (int i = 0; i < d_model - 1; i++)\n                acc +="),
+    "destination_ignores_page_table": ("(int64_t)token_row(s, page_table, b, p, 1);",
+                                       "(int64_t)((size_t)b * (size_t)s->max_len + (size_t)p);"),
     "drop_first_index_component": ("for (int i = 0; i < d_idx; i++)", "for (int i = 1; i < d_idx; i++)"),
     "index_key_off_by_one_token": ("token_row(s, page_table, b, j, (size_t)d_idx)",
                                    "token_row(s, page_table, b, (j + 1) % s->max_len, (size_t)d_idx)"),
