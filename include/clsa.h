@@ -181,6 +181,24 @@ clsa_status clsa_dense_attn(const clsa_shape *shape, const void *q, const void *
                             const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
                             void *ws, size_t ws_bytes, void *stream);
 
+/* Section 2.1, Eq. 2 for the new tokens of a step, with their cache write:
+ * for every row r = (b,t) of the new hidden states h[b,t,0..d_model-1],
+ *   q_idx[b,t,:]                  = h W_idx^Q             (256 values),
+ *   index-key cache row of pos[r] = h W_idx^K             (256 values),
+ *   key cache row of pos[r]       = h W^K, value row = h W^V (kv_heads*head_dim each),
+ * where pos[b,t] is the token's absolute position in sequence b (paged caches
+ * through page_table; positions outside [0, max_len) are not written to the
+ * caches).  w is one bf16 matrix [512 + 2*kv_heads*head_dim, d_model]: row c
+ * is the weight vector of output feature c, in the order W_idx^Q, W_idx^K,
+ * W^K, W^V (each head's 128 features consecutive).  bf16 inputs, fp32 products
+ * and accumulation, bf16 results rounded to nearest even.  d_model: a multiple
+ * of 512 up to 8192.  Two rows must not write the same cache row.  Needs no
+ * workspace. */
+clsa_status clsa_project_append(const clsa_shape *shape, int32_t d_model, const void *h,
+                                const void *w, const int32_t *pos, const int32_t *page_table,
+                                void *q_idx, void *k_idx, void *k_cache, void *v_cache,
+                                void *stream);
+
 /* Static, human-readable name of a status code. */
 const char *clsa_status_string(clsa_status status);
 

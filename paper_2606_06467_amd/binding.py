@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
         "clsa_decode_step_grouped": (i32, [SP, P, i64, P, i64, P, P, P, P, P, i32, i32, P, P, P,
                                            P, P, P, sz, P]),
         "clsa_dense_attn": (i32, [SP, P, P, P, P, P, P, P, P, P, sz, P]),
+        "clsa_project_append": (i32, [SP, i32, P, P, P, P, P, P, P, P, P]),
         "clsa_status_string": (ctypes.c_char_p, [i32]),
         "clsa_set_phase_events": (i32, [ctypes.POINTER(P), i32]),
     }
@@ -182,6 +183,15 @@ def clsa_dense_attn(shape, q, k_cache, v_cache, page_table, seq_lens, q_pos, out
                                  _ptr(seq_lens, "seq_lens"), _ptr(q_pos, "q_pos"),
                                  _ptr(out, "out"), _ptr(lse, "lse"), _ptr(ws, "ws"), wsb,
                                  _stream(stream)), "clsa_dense_attn")
+
+
+def clsa_project_append(shape, d_model, h, w, pos, page_table, q_idx, k_idx, k_cache, v_cache,
+                        stream=None):
+    _check(lib().clsa_project_append(ctypes.byref(shape), int(d_model), _ptr(h, "h"), _ptr(w, "w"),
+                                     _ptr(pos, "pos"), _ptr(page_table, "page_table"),
+                                     _ptr(q_idx, "q_idx"), _ptr(k_idx, "k_idx"),
+                                     _ptr(k_cache, "k_cache"), _ptr(v_cache, "v_cache"),
+                                     _stream(stream)), "clsa_project_append")
 
 
 def clsa_set_phase_events(events: Optional[Sequence[int]]) -> None:

@@ -400,6 +400,26 @@ clsa_status clsa_decode_step_grouped(const clsa_shape *shape, const void *q_idx,
                             out_layers, lse_layers, idx, n_sel, ws, ws_bytes, stream);
 }
 
+clsa_status clsa_project_append(const clsa_shape *shape, int32_t d_model, const void *h,
+                                const void *w, const int32_t *pos, const int32_t *page_table,
+                                void *q_idx, void *k_idx, void *k_cache, void *v_cache,
+                                void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kIndex | kAttn, &g));
+    if (d_model < 1) return CLSA_ERR_INVALID_ARG;
+    if (!clsa::project_supported(d_model)) return CLSA_ERR_UNSUPPORTED;
+    CLSA_TRY(check_ptr(h, 16));
+    CLSA_TRY(check_ptr(w, 16));
+    CLSA_TRY(check_ptr(pos, 4));
+    CLSA_TRY(check_ptr(q_idx, 16));
+    CLSA_TRY(check_ptr(k_idx, 16));
+    CLSA_TRY(check_ptr(k_cache, 16));
+    CLSA_TRY(check_ptr(v_cache, 16));
+    CLSA_TRY(check_common(shape, page_table, nullptr, false, true));
+    return from_hip(clsa::launch_project(g, d_model, h, w, pos, page_table, q_idx, k_idx, k_cache,
+                                         v_cache, static_cast<hipStream_t>(stream)));
+}
+
 clsa_status clsa_dense_attn(const clsa_shape *shape, const void *q, const void *k_cache,
                             const void *v_cache, const int32_t *page_table,
                             const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,

@@ -89,4 +89,12 @@ hipError_t launch_dense_attn(const Geometry &g, const void *q, const void *k_cac
                              const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
                              float *partials, hipStream_t stream);
 
+// ---- project.hip ----
+// d_model values the projection kernels support (multiples of 512 up to 8192).
+bool project_supported(int d_model);
+// Eq. 2 for new tokens + cache write; w: [512 + 2 * kv_heads * 128, d_model].
+hipError_t launch_project(const Geometry &g, int d_model, const void *h, const void *w,
+                          const int32_t *pos, const int32_t *page_table, void *q_idx,
+                          void *k_idx, void *k_cache, void *v_cache, hipStream_t stream);
+
 }  // namespace clsa

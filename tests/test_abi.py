@@ -30,7 +30,8 @@ def declared_functions():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("clsa_index_scores", "clsa_topk", "clsa_sparse_attn", "clsa_decode_step",
-              "clsa_decode_step_grouped", "clsa_dense_attn", "clsa_workspace_bytes",
+              "clsa_decode_step_grouped", "clsa_dense_attn", "clsa_project_append",
+              "clsa_workspace_bytes",
               "clsa_status_string", "clsa_set_phase_events"):
         assert n in names
 
@@ -237,3 +238,18 @@ def test_dense_attn_checks(lib):
     assert call(_shape(max_len=262144 * 2), ws=A, wsb=1 << 30) == -2
     assert call(_shape(head_dim=96), ws=A, wsb=1 << 30) == -2
     assert B.clsa_workspace_bytes(_shape(max_len=262144 * 2), B.CLSA_OP_DENSE) == 0
+
+
+def test_project_append_checks(lib):
+    def call(sh, d=2560, h=A, w=A, pos=A, pt=None):
+        return lib.clsa_project_append(ctypes.byref(sh), d, h, w, pos, pt, A, A, A, A, None)
+    sh = _shape()
+    assert call(sh, d=0) == -1
+    assert call(sh, d=2500) == -2          # not a multiple of 512
+    assert call(sh, d=8704) == -2          # above 8192
+    assert call(sh, h=MIS) == -1
+    assert call(sh, w=None) == -1
+    assert call(sh, pos=None) == -1
+    assert call(_shape(page_size=64, max_pages=16), pt=None) == -1
+    assert call(_shape(idx_dim=32)) == -2
+    assert call(_shape(head_dim=64)) == -2
