@@ -13,10 +13,10 @@
 // 4 * (l >> 4) + r (r = 0..3) of feature (l & 15).  A wave owns 16 rows x 64
 // features (four feature tiles).
 //   * few rows (decode): a workgroup of 8 waves splits d_model eight ways for
-//     one 16 x 64 tile, each wave issuing all of its loads before its first
-//     product, and the eight partial tiles are added in LDS: the weights
-//     (13 MB at d_model 2560, the bytes that bound this case) are then read by
-//     many CUs at once;
+//     one 16-row x 16-feature tile, each wave issuing all of its loads before
+//     its first product, and the eight partial tiles are added in LDS: the
+//     weights (13 MB at d_model 2560, the bytes that bound this case) are then
+//     read by 160 workgroups at once;
 //   * many rows (prefill): four waves per workgroup on four row tiles of the
 //     same 64 features (their weight loads meet in L1), each over all of
 //     d_model with the next step's loads issued before the current products.
@@ -72,45 +72,36 @@ __device__ __forceinline__ void store_feature(const ProjArgs &a, int r, int f, f
     else a.v_cache[row * a.kvw + (f - 512 - a.kvw)] = bits;
 }
 
-// Few rows: one 16-row x 64-feature tile per workgroup, d_model split over 8
+// Few rows: one 16-row x 16-feature tile per workgroup, d_model split over 8
 // waves of KS 32-dim steps each (d_model = 256 * KS).
 template <int KS, bool PAGED>
 __global__ __launch_bounds__(512) void project_splitk_kernel(ProjArgs a) {
-    __shared__ float part[kSplitWaves][16][kProjFeat + 4];
+    __shared__ float part[kSplitWaves][16][16 + 1];
     const int ft = blockIdx.x, rt = blockIdx.y;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int col = lane & 15, grp = lane >> 4;
     const int k0 = wave * KS * 32 + grp * 8;
     const uint16_t *hp = a.h + (size_t)min(rt * 16 + col, a.rows - 1) * a.d + k0;
-    bf16x8 av[KS], bv[KS][4];
+    const uint16_t *wp = a.w + (size_t)(ft * 16 + col) * a.d + k0;
+    bf16x8 av[KS], bv[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
         av[s] = ld8(hp + s * 32);
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
-            bv[s][ct] = ld8(a.w + (size_t)(ft * kProjFeat + ct * 16 + col) * a.d + k0 + s * 32);
+        bv[s] = ld8(wp + s * 32);
     }
     __builtin_amdgcn_sched_barrier(0);  // every load in flight before the first product
-    f32x4 c[4];
+    f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) c[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < KS; ++s) c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[s], bv[s], c, 0, 0, 0);
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
-            c[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[s], bv[s][ct], c[ct], 0, 0, 0);
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) part[wave][4 * grp + r][ct * 16 + col] = c[ct][r];
+    for (int r = 0; r < 4; ++r) part[wave][4 * grp + r][col] = c[r];
     __syncthreads();
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {  // 16 x 64 outputs, two per thread
-        const int rr = (threadIdx.x >> 6) + 8 * e, f = threadIdx.x & 63;
+    if (threadIdx.x < 256) {  // 16 x 16 outputs
+        const int rr = threadIdx.x >> 4, f = threadIdx.x & 15;
         float sum = 0.0f;
 #pragma unroll
         for (int w = 0; w < kSplitWaves; ++w) sum += part[w][rr][f];
-        store_feature<PAGED>(a, rt * 16 + rr, ft * kProjFeat + f, sum);
+        store_feature<PAGED>(a, rt * 16 + rr, ft * 16 + f, sum);
     }
 }
 
@@ -187,7 +178,7 @@ hipError_t launch_project(const Geometry &g, int d_model, const void *h, const v
     const int n_feat = 512 + 2 * a.kvw;  // a multiple of 64
     const bool paged = g.page_shift >= 0;
     if (g.rows <= 64 && d_model <= kSplitMaxD) {
-        const dim3 grid(n_feat / kProjFeat, div_up(g.rows, 16));
+        const dim3 grid(n_feat / 16, div_up(g.rows, 16));
         switch (d_model / 512) {
             case 1: launch_splitk<2>(a, paged, grid, stream); break;
             case 2: launch_splitk<4>(a, paged, grid, stream); break;
