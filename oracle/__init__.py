@@ -79,8 +79,10 @@ def _load():
     lib.oracle_sparse_attn.argtypes = [SP, P, P, P, P, P, P, P, P]
     lib.oracle_decode_step.argtypes = [SP, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, P, P, P]
     lib.oracle_project.argtypes = [SP, ctypes.c_int, P, P, ctypes.c_int, P, P, P, P]
+    lib.oracle_kd_target.argtypes = [SP, ctypes.c_int, P, P, P, P, P, P]
+    lib.oracle_kd_loss.argtypes = [SP, P, P, P, P, P, P, P, P, P]
     for f in ("oracle_index_scores", "oracle_topk", "oracle_sparse_attn", "oracle_decode_step",
-              "oracle_project"):
+              "oracle_project", "oracle_kd_target", "oracle_kd_loss"):
         getattr(lib, f).restype = None
     _lib = lib
     return lib
@@ -153,6 +155,34 @@ def project(sh: Shape, h, w, pos, page_table=None):
     lib.oracle_project(ctypes.byref(sh), int(d_model), _p(h), _p(w), int(n_out), _p(pos),
                        _p(page_table), _p(out), _p(dest))
     return out, dest
+
+
+def kd_target(sh: Shape, q_layers, k_cache, seq_lens, q_pos=None, page_table=None,
+              fill=np.nan) -> np.ndarray:
+    """Eq. 5 target abar [B, T, max_len] fp64 (invalid positions hold ``fill``)."""
+    lib = _load()
+    q_layers, k_cache = _c(q_layers, np.uint16), _c(k_cache, np.uint16)
+    seq_lens, q_pos, page_table = _c(seq_lens, np.int32), _c(q_pos, np.int32), _c(page_table, np.int32)
+    n_layers = q_layers.shape[0]
+    out = np.full((sh.batch, sh.n_q, sh.max_len), fill, dtype=np.float64)
+    lib.oracle_kd_target(ctypes.byref(sh), int(n_layers), _p(q_layers), _p(k_cache), _p(page_table),
+                         _p(seq_lens), _p(q_pos), _p(out))
+    return out
+
+
+def kd_loss(sh: Shape, abar, q_idx, k_idx, seq_lens, q_pos=None, page_table=None):
+    """Eq. 6: (loss, dq_idx [B,T,256] fp64, dk_idx fp64 shaped like k_idx; rows never
+    written hold nan)."""
+    lib = _load()
+    abar = np.ascontiguousarray(abar, dtype=np.float64)
+    q_idx, k_idx = _c(q_idx, np.uint16), _c(k_idx, np.uint16)
+    seq_lens, q_pos, page_table = _c(seq_lens, np.int32), _c(q_pos, np.int32), _c(page_table, np.int32)
+    loss = np.zeros(1, dtype=np.float64)
+    dq = np.empty(q_idx.shape, dtype=np.float64)
+    dk = np.full(k_idx.shape, np.nan, dtype=np.float64)
+    lib.oracle_kd_loss(ctypes.byref(sh), _p(abar), _p(q_idx), _p(k_idx), _p(page_table),
+                       _p(seq_lens), _p(q_pos), _p(loss), _p(dq), _p(dk))
+    return float(loss[0]), dq, dk
 
 
 def decode_step(sh: Shape, q_idx, k_idx, k_cache, v_cache, seq_lens, q_layers, q_pos=None,

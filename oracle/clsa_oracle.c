@@ -23,6 +23,13 @@
  *                        and the shared K = H W^K, V = H W^V of the same hidden
  *                        states, for new tokens, with the cache row each of
  *                        them occupies.
+ *   oracle_kd_target     Section 2.2, Eq. (5): the average over layers and query
+ *                        heads of the attention distributions (each layer's own
+ *                        scaled softmax over the row's valid keys).
+ *   oracle_kd_loss       Section 2.2, Eq. (6): the mean over rows of
+ *                        KL(A_bar_t || softmax(I_t)), I from Eq. (3), and its
+ *                        gradient with respect to the index queries and keys
+ *                        (A_bar held constant, the stop-gradient of Eq. (6)).
  *   oracle_decode_step   Section 2.1 last paragraph and Section 2.3 ("compute
  *                        top-k once"): one index pass, one top-k, then every
  *                        layer reuses the same S_t.
@@ -252,4 +259,121 @@ void oracle_project(const oracle_shape *s, int d_model, const uint16_t *h, const
         const int p = pos[r];
         dest[r] = (p < 0 || p >= s->max_len) ? -1 : (int64_t)token_row(s, page_table, b, p, 1);
     }
+}
+
+/* Eq. (5): abar[b,t,j] = (1 / (L * Hq)) * sum over layers l and query heads h of
+ * softmax_j(scale * <q_l[b,t,h], K[b,j,g(h)]>), j over the valid keys of row
+ * (b,t); positions outside them are left untouched.  q_layers [L, B, T, Hq, D]. */
+void oracle_kd_target(const oracle_shape *s, int n_layers, const uint16_t *q_layers,
+                      const uint16_t *k_cache, const int32_t *page_table,
+                      const int32_t *seq_lens, const int32_t *q_pos, double *abar)
+{
+    const int D = s->head_dim, Hq = s->q_heads, Hkv = s->kv_heads;
+    const int group = Hq / Hkv;
+    const size_t kv_row = (size_t)Hkv * D;
+    const size_t rows = (size_t)s->batch * s->n_q;
+    double *z = (double *)malloc(sizeof(double) * (size_t)(s->max_len > 0 ? s->max_len : 1));
+    for (int b = 0; b < s->batch; b++) {
+        for (int t = 0; t < s->n_q; t++) {
+            const size_t r = (size_t)b * s->n_q + t;
+            const int n = oracle_valid_len(s, seq_lens, q_pos, b, t);
+            double *a = abar + r * (size_t)s->max_len;
+            for (int j = 0; j < n; j++)
+                a[j] = 0.0;
+            if (n == 0)
+                continue;
+            for (int l = 0; l < n_layers; l++) {
+                for (int h = 0; h < Hq; h++) {
+                    const int g = h / group;
+                    const uint16_t *qh = q_layers + (((size_t)l * rows + r) * Hq + h) * D;
+                    double zmax = -INFINITY;
+                    for (int j = 0; j < n; j++) {
+                        const uint16_t *kr = k_cache + token_row(s, page_table, b, j, kv_row) + (size_t)g * D;
+                        double acc = 0.0;
+                        for (int e = 0; e < D; e++)
+                            acc += oracle_bf16_to_double(qh[e]) * oracle_bf16_to_double(kr[e]);
+                        z[j] = s->softmax_scale * acc;
+                        if (z[j] > zmax)
+                            zmax = z[j];
+                    }
+                    double denom = 0.0;
+                    for (int j = 0; j < n; j++)
+                        denom += exp(z[j] - zmax);
+                    for (int j = 0; j < n; j++)
+                        a[j] += exp(z[j] - zmax) / denom;
+                }
+            }
+            for (int j = 0; j < n; j++)
+                a[j] /= (double)n_layers * (double)Hq;
+        }
+    }
+    free(z);
+}
+
+/* Eq. (6) and its gradient.  For every row with at least one valid key,
+ * P = abar (the target, held constant) and Q = softmax(I_t) over the valid keys,
+ * I_t[j] = <q_idx[b,t], k_idx[b,j]> (Eq. 3, unscaled); the loss is the mean over
+ * those rows of KL(P || Q) = sum_j P_j (log P_j - log Q_j), with 0 log 0 = 0.
+ * dL/dI_t[j] = (Q_j - P_j) / n_rows, and by the chain rule
+ *   dq_idx[b,t] = sum_j dL/dI_t[j] k_idx[b,j],   dk_idx[b,j] = sum_t dL/dI_t[j] q_idx[b,t].
+ * dk_idx has the index-key cache's layout; its rows for positions j < seq_lens[b]
+ * are written (zero when no row sees j), the others are left untouched. */
+void oracle_kd_loss(const oracle_shape *s, const double *abar, const uint16_t *q_idx,
+                    const uint16_t *k_idx, const int32_t *page_table, const int32_t *seq_lens,
+                    const int32_t *q_pos, double *loss, double *dq_idx, double *dk_idx)
+{
+    const int d = s->idx_heads * s->idx_dim;
+    double *sc = (double *)malloc(sizeof(double) * (size_t)(s->max_len > 0 ? s->max_len : 1));
+    int n_rows = 0;
+    for (int b = 0; b < s->batch; b++)
+        for (int t = 0; t < s->n_q; t++)
+            if (oracle_valid_len(s, seq_lens, q_pos, b, t) > 0)
+                n_rows++;
+    for (int b = 0; b < s->batch; b++)
+        for (int j = 0; j < seq_lens[b] && j < s->max_len; j++) {
+            double *dk = dk_idx + token_row(s, page_table, b, j, (size_t)d);
+            for (int e = 0; e < d; e++)
+                dk[e] = 0.0;
+        }
+    double total = 0.0;
+    for (int b = 0; b < s->batch; b++) {
+        for (int t = 0; t < s->n_q; t++) {
+            const size_t r = (size_t)b * s->n_q + t;
+            const int n = oracle_valid_len(s, seq_lens, q_pos, b, t);
+            double *dq = dq_idx + r * (size_t)d;
+            for (int e = 0; e < d; e++)
+                dq[e] = 0.0;
+            if (n == 0)
+                continue;
+            const uint16_t *qr = q_idx + r * (size_t)d;
+            double smax = -INFINITY;
+            for (int j = 0; j < n; j++) {
+                const uint16_t *kr = k_idx + token_row(s, page_table, b, j, (size_t)d);
+                double acc = 0.0;
+                for (int e = 0; e < d; e++)
+                    acc += oracle_bf16_to_double(qr[e]) * oracle_bf16_to_double(kr[e]);
+                sc[j] = acc;
+                if (acc > smax)
+                    smax = acc;
+            }
+            double denom = 0.0;
+            for (int j = 0; j < n; j++)
+                denom += exp(sc[j] - smax);
+            const double lse = smax + log(denom);
+            const double *p = abar + r * (size_t)s->max_len;
+            for (int j = 0; j < n; j++) {
+                if (p[j] > 0.0)
+                    total += p[j] * (log(p[j]) - (sc[j] - lse));
+                const double g = (exp(sc[j] - lse) - p[j]) / (double)n_rows;
+                const uint16_t *kr = k_idx + token_row(s, page_table, b, j, (size_t)d);
+                double *dk = dk_idx + token_row(s, page_table, b, j, (size_t)d);
+                for (int e = 0; e < d; e++) {
+                    dq[e] += g * oracle_bf16_to_double(kr[e]);
+                    dk[e] += g * oracle_bf16_to_double(qr[e]);
+                }
+            }
+        }
+    }
+    *loss = n_rows > 0 ? total / (double)n_rows : 0.0;
+    free(sc);
 }

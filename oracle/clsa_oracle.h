@@ -47,6 +47,12 @@ void oracle_sparse_attn(const oracle_shape *s, const uint16_t *q, const uint16_t
 void oracle_project(const oracle_shape *s, int d_model, const uint16_t *h, const uint16_t *w,
                     int n_out, const int32_t *pos, const int32_t *page_table, double *out,
                     int64_t *dest);
+void oracle_kd_target(const oracle_shape *s, int n_layers, const uint16_t *q_layers,
+                      const uint16_t *k_cache, const int32_t *page_table,
+                      const int32_t *seq_lens, const int32_t *q_pos, double *abar);
+void oracle_kd_loss(const oracle_shape *s, const double *abar, const uint16_t *q_idx,
+                    const uint16_t *k_idx, const int32_t *page_table, const int32_t *seq_lens,
+                    const int32_t *q_pos, double *loss, double *dq_idx, double *dk_idx);
 void oracle_decode_step(const oracle_shape *s, const uint16_t *q_idx, const uint16_t *k_idx,
                         const uint16_t *k_cache, const uint16_t *v_cache,
                         const int32_t *page_table, const int32_t *seq_lens, const int32_t *q_pos,

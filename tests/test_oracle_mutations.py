@@ -14,6 +14,7 @@ import oracle
 from tests import test_oracle_attn as A
 from tests import test_oracle_decode_step as DS
 from tests import test_oracle_index as I
+from tests import test_oracle_kd as KD
 from tests import test_oracle_project as PJ
 from tests import test_oracle_topk as T
 
@@ -31,9 +32,21 @@ PINS = [
     lambda o: DS.test_step_matches_library_composition(o, 100),
     PJ.test_matches_numpy_float64, PJ.test_exact_on_small_integers, PJ.test_unit_vector_probe,
     PJ.test_destination_rows,
+    KD.test_target_is_a_mean_of_scipy_softmaxes, KD.test_target_rows_sum_to_one,
+    KD.test_kl_of_the_indexer_distribution_with_itself_is_zero,
+    KD.test_loss_matches_scipy_relative_entropy, KD.test_gradient_matches_central_differences,
+    KD.test_rows_without_keys_do_not_count,
 ]
 
 MUTANTS = {
+    "target_not_averaged": ("a[j] /= (double)n_layers * (double)Hq;", "a[j] /= (double)n_layers;"),
+    "target_unscaled_logits": ("z[j] = s->softmax_scale * acc;", "z[j] = acc;"),
+    "kd_gradient_sign": ("const double g = (exp(sc[j] - lse) - p[j]) / (double)n_rows;",
+                         "const double g = (p[j] - exp(sc[j] - lse)) / (double)n_rows;"),
+    "kd_loss_not_normalised": ("*loss = n_rows > 0 ? total / (double)n_rows : 0.0;",
+                               "*loss = total;"),
+    "kd_dk_uses_keys": ("dk[e] += g * oracle_bf16_to_double(qr[e]);",
+                        "dk[e] += g * oracle_bf16_to_double(kr[e]);"),
     "projection_weight_transposed": ("oracle_bf16_to_double(w[(size_t)c * d_model + i]);",
                                      "oracle_bf16_to_double(w[(size_t)i * n_out + c]);"),
     "projection_drops_last_term": ("for (int i = 0; i < d_model; i++)\n                acc +=",
