@@ -66,7 +66,8 @@ MUTANTS = {
                          "int lim = q_pos[(size_t)b * s->n_q + t];"),
     "gqa_modulo_mapping": ("const int g = h / group;", "const int g = h % Hkv;"),
     "no_softmax_scale": ("z[i] = s->softmax_scale * acc;", "z[i] = acc;"),
-    "keys_read_from_values": ("const uint16_t *kr = k_cache +", "const uint16_t *kr = v_cache +"),
+    "keys_read_from_values": ("const uint16_t *kr = k_cache + token_row(s, page_table, b, S[i]",
+                              "const uint16_t *kr = v_cache + token_row(s, page_table, b, S[i]"),
     "unnormalised_weights": ("const double w = exp(z[i] - zmax) / denom;",
                              "const double w = exp(z[i] - zmax);"),
     "lse_without_max": ("lse[r * Hq + h] = zmax + log(denom);", "lse[r * Hq + h] = log(denom);"),
