@@ -87,7 +87,9 @@ typedef enum {
     CLSA_OP_TOPK = 1,   /* clsa_topk */
     CLSA_OP_ATTN = 2,   /* clsa_sparse_attn */
     CLSA_OP_DECODE = 3, /* clsa_decode_step and clsa_decode_step_grouped */
-    CLSA_OP_DENSE = 4   /* clsa_dense_attn */
+    CLSA_OP_DENSE = 4,  /* clsa_dense_attn */
+    CLSA_OP_KD_TARGET = 5, /* clsa_kd_target (size grows with n_layers) */
+    CLSA_OP_KD_LOSS = 6    /* clsa_kd_loss */
 } clsa_op;
 
 typedef struct clsa_shape {
@@ -107,9 +109,10 @@ typedef struct clsa_shape {
     float softmax_scale; /* logit scale of Eq. 4's softmax (1/sqrt(head_dim))     */
 } clsa_shape;
 
-/* Bytes of workspace `op` needs for `shape` (n_layers only matters for
- * CLSA_OP_DECODE, where it never changes the size).  Returns 0 for CLSA_OP_INDEX, and also 0 when the shape is
- * invalid or unsupported (the entry point then reports the reason). */
+/* Bytes of workspace `op` needs for `shape` (n_layers matters for
+ * CLSA_OP_KD_TARGET only; for CLSA_OP_DECODE it never changes the size).
+ * Returns 0 for CLSA_OP_INDEX, and also 0 when the shape is invalid or
+ * unsupported (the entry point then reports the reason). */
 size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layers);
 
 /* Eq. 3, first half: scores[b,t,j] = sum_i q_idx[b,t,i] * k_idx[b,j,i] over the
@@ -198,6 +201,40 @@ clsa_status clsa_project_append(const clsa_shape *shape, int32_t d_model, const 
                                 const void *w, const int32_t *pos, const int32_t *page_table,
                                 void *q_idx, void *k_idx, void *k_cache, void *v_cache,
                                 void *stream);
+
+/* Section 2.2, Eq. 5: the distillation target of the indexer,
+ *   abar[b,t,j] = 1/(n_layers*q_heads) * sum_l sum_h softmax_j(softmax_scale *
+ *                 q_layers[l,b,t,h] . K[b,j,g(h)]),
+ * each softmax over the valid keys j of row (b,t) (j < seq_lens[b], and
+ * j <= q_pos[b,t] when causal) of the one shared key cache, g(h) =
+ * h / (q_heads / kv_heads).  abar: fp32 [batch, n_q, max_len]; only the valid
+ * positions of each row are written (a row without valid keys is left as it
+ * is).  bf16 inputs, fp32 logits and softmax.  n_layers >= 1; v_cache is not
+ * read.  Workspace: CLSA_OP_KD_TARGET with the same n_layers. */
+clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void *q_layers,
+                           const void *k_cache, const int32_t *page_table,
+                           const int32_t *seq_lens, const int32_t *q_pos, float *abar, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/* Section 2.2, Eq. 6 and its gradient.  With P = abar[b,t,:] (the target,
+ * held constant: the stop-gradient of Eq. 6) and Q = softmax(I_t) over the
+ * valid keys of row (b,t), I the unscaled index scores of Eq. 3 computed here
+ * from q_idx and k_idx, the loss is the mean of KL(P || Q) =
+ * sum_j P_j (log P_j - log Q_j) (0 log 0 = 0) over the n_rows rows that have a
+ * valid key, and dL/dI_t[j] = (Q_j - P_j) / n_rows, so that
+ *   dq_idx[b,t,:]            = sum_j dL/dI_t[j] k_idx[b,j,:],
+ *   dk_idx row of token j    = sum_t dL/dI_t[j] q_idx[b,t,:].
+ * loss: one fp32 value (0 when n_rows == 0).  dq_idx: fp32 [batch, n_q, 256],
+ * every row written (zero for rows without keys).  dk_idx: fp32 with the
+ * layout of the index-key cache (256 values per token, through page_table when
+ * paged), written for every token j < seq_lens[b] (zero when no row sees it);
+ * other rows are left as they are.  abar is read at valid positions only and
+ * should be a distribution over them.  fp32 scores, softmax and products;
+ * the loss is summed in double.  Workspace: CLSA_OP_KD_LOSS. */
+clsa_status clsa_kd_loss(const clsa_shape *shape, const float *abar, const void *q_idx,
+                         const void *k_idx, const int32_t *page_table, const int32_t *seq_lens,
+                         const int32_t *q_pos, float *loss, float *dq_idx, float *dk_idx,
+                         void *ws, size_t ws_bytes, void *stream);
 
 /* Static, human-readable name of a status code. */
 const char *clsa_status_string(clsa_status status);

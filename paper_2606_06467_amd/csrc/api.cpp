@@ -214,6 +214,15 @@ size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layer
         case CLSA_OP_DENSE:
             if (check_shape(shape, kAttn | kDense, &g) != CLSA_OK) return 0;
             return attn_ws_bytes(g, true);
+        case CLSA_OP_KD_TARGET:
+            if (check_shape(shape, kAttn, &g) != CLSA_OK || n_layers < 1 ||
+                !clsa::kd_target_supported(g, n_layers))
+                return 0;
+            return align_up(sizeof(float) * clsa::kd_target_ws_floats(g, n_layers));
+        case CLSA_OP_KD_LOSS:
+            if (check_shape(shape, kIndex | kDense, &g) != CLSA_OK || !clsa::kd_loss_supported(g))
+                return 0;
+            return align_up(sizeof(float) * clsa::kd_loss_ws_floats(g));
         case CLSA_OP_DECODE: {
             // layers run one after another and reuse the same buffers
             if (check_shape(shape, kIndex | kTopk | kAttn, &g) != CLSA_OK || n_layers < 0)
@@ -441,6 +450,48 @@ clsa_status clsa_dense_attn(const clsa_shape *shape, const void *q, const void *
     return from_hip(clsa::launch_dense_attn(g, q, k_cache, v_cache, page_table, seq_lens, q_pos,
                                             out, lse, w.partials,
                                             static_cast<hipStream_t>(stream)));
+}
+
+clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void *q_layers,
+                           const void *k_cache, const int32_t *page_table,
+                           const int32_t *seq_lens, const int32_t *q_pos, float *abar, void *ws,
+                           size_t ws_bytes, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kAttn, &g));
+    if (n_layers < 1) return CLSA_ERR_INVALID_ARG;
+    if (!clsa::kd_target_supported(g, n_layers)) return CLSA_ERR_UNSUPPORTED;
+    CLSA_TRY(check_ptr(q_layers, 16));
+    CLSA_TRY(check_ptr(k_cache, 16));
+    CLSA_TRY(check_ptr(seq_lens, 4));
+    CLSA_TRY(check_ptr(abar, 4));
+    CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
+    const size_t need = align_up(sizeof(float) * clsa::kd_target_ws_floats(g, n_layers));
+    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
+    return from_hip(clsa::launch_kd_target(g, n_layers, q_layers, k_cache, page_table, seq_lens,
+                                           q_pos, abar, static_cast<float *>(ws),
+                                           static_cast<hipStream_t>(stream)));
+}
+
+clsa_status clsa_kd_loss(const clsa_shape *shape, const float *abar, const void *q_idx,
+                         const void *k_idx, const int32_t *page_table, const int32_t *seq_lens,
+                         const int32_t *q_pos, float *loss, float *dq_idx, float *dk_idx,
+                         void *ws, size_t ws_bytes, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kIndex | kDense, &g));
+    if (!clsa::kd_loss_supported(g)) return CLSA_ERR_UNSUPPORTED;
+    CLSA_TRY(check_ptr(abar, 4));
+    CLSA_TRY(check_ptr(q_idx, 16));
+    CLSA_TRY(check_ptr(k_idx, 16));
+    CLSA_TRY(check_ptr(seq_lens, 4));
+    CLSA_TRY(check_ptr(loss, 4));
+    CLSA_TRY(check_ptr(dq_idx, 16));
+    CLSA_TRY(check_ptr(dk_idx, 16));
+    CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
+    const size_t need = align_up(sizeof(float) * clsa::kd_loss_ws_floats(g));
+    if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
+    return from_hip(clsa::launch_kd_loss(g, abar, q_idx, k_idx, page_table, seq_lens, q_pos, loss,
+                                         dq_idx, dk_idx, static_cast<float *>(ws),
+                                         static_cast<hipStream_t>(stream)));
 }
 
 const char *clsa_status_string(clsa_status status) {

@@ -97,6 +97,21 @@ __device__ __forceinline__ void transpose_reduce(float (&p)[NV], int lane) {
     }
 }
 
+// Maximum / sum over the 16 lanes of this lane's row; every lane of the row
+// gets the result (quad swaps, then the half and full row mirrors).
+__device__ __forceinline__ float row16_max(float x) {
+    x = fmaxf(x, dpp_f32<0xB1>(x));
+    x = fmaxf(x, dpp_f32<0x4E>(x));
+    x = fmaxf(x, dpp_f32<0x141>(x));
+    return fmaxf(x, dpp_f32<0x140>(x));
+}
+__device__ __forceinline__ float row16_sum(float x) {
+    x += dpp_f32<0xB1>(x);
+    x += dpp_f32<0x4E>(x);
+    x += dpp_f32<0x141>(x);
+    return x + dpp_f32<0x140>(x);
+}
+
 // Maximum / sum over all 64 lanes; every lane gets the result.
 __device__ __forceinline__ float wave_max(float x) {
     x = fmaxf(x, dpp_f32<0xB1>(x));

@@ -1,0 +1,566 @@
+// Training side of the shared indexer (Section 2.2): the distillation target
+// of Eq. 5 and the KL loss of Eq. 6 with its gradient.
+//
+// Eq. 5: abar[b,t,j] = (1 / (L * Hq)) * sum over layers l and query heads h of
+// softmax_j(scale * q_l[b,t,h] . K[b,j,g(h)]) over the valid keys of row (b,t),
+// one shared key cache for every layer.  Logits on the matrix cores
+// (v_mfma_f32_16x16x32_bf16: A = 16 query rows x 32 dims, B = 32 dims x 16
+// keys; lane l supplies row / key (l & 15) for dims (l >> 4) * 8 .. +8 and
+// receives rows 4 * (l >> 4) + r of key (l & 15), so the 16 keys of one row
+// sit in one DPP row of 16 lanes):
+//   * kd_lse_kernel: per (64-row tile, layer, head), an online softmax over the
+//     row's keys gives each row's log-sum-exp (log2 units, in the workspace);
+//   * kd_target_kernel: per (64-row, 64-key) tile, every (layer, head) adds
+//     exp(logit - lse) into the tile held in registers; the key operands of a
+//     KV head are loaded once for all layers and heads of its group, and abar
+//     is written once, with no atomics.
+// Eq. 6: P = abar (a constant), Q = softmax(I_t) over the valid keys, I the
+// unscaled index scores of Eq. 3 (computed by the indexer kernels); the loss
+// is the mean over rows with at least one key of KL(P || Q), and
+// dL/dI = (Q - P) / n_rows:
+//   * kd_rows_kernel: per row, the log-sum-exp of I, the row's KL term and
+//     Q - P, written over the scores;
+//   * kd_loss_kernel: n_rows and the mean of the row terms (summed in double
+//     in a fixed order);
+//   * kd_dq_kernel / kd_dk_kernel: dq = dL/dI K_idx and dk = dL/dI^T Q_idx,
+//     fp32 products tiled through LDS (64 x 64 outputs per workgroup, 4 x 4
+//     per thread, 32-deep steps).
+#include "clsa_internal.h"
+#include "device_common.h"
+
+namespace clsa {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kKdLog2e = 1.4426950408889634f;
+constexpr float kKdLn2 = 0.6931471805599453f;
+constexpr int kKdDim = 128;  // attention head dimension
+constexpr int kKdTile = 64;  // rows and keys per target tile
+constexpr int kIdxDim = 256; // index vector width
+
+struct KdArgs {
+    const uint16_t *q_layers;  // [L, rows, Hq, 128]
+    const uint16_t *k_cache;   // [B, max_len, Hkv, 128] | paged
+    const int32_t *page_table, *seq_lens, *q_pos;
+    float *lse2;               // [L, rows, Hq], log2 units
+    float *abar;               // [rows, max_len]
+    int n_layers, n_q, rows, max_len, page_shift, max_pages, causal;
+    int q_heads, kv_heads, group, row_tiles, key_tiles;
+    float scale_log2, inv_lh;  // softmax_scale * log2(e), 1 / (L * Hq)
+};
+
+__device__ __forceinline__ bf16x8 kd_ld8(const uint16_t *p) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+}
+
+// Key limits of the lane's four rows t0 + 4 * grp + r (0 for rows past n_q).
+__device__ __forceinline__ void kd_row_limits(const KdArgs &a, int b, int t0, int grp,
+                                              int (&n)[4]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int t = t0 + 4 * grp + r;
+        n[r] = t < a.n_q ? valid_keys(a.seq_lens, a.q_pos, a.causal, b, b * a.n_q + t, a.max_len)
+                         : 0;
+    }
+}
+
+// A operands: query row t0 + col of layer l, head h (rows past n_q clamped).
+__device__ __forceinline__ void kd_load_query(const KdArgs &a, int b, int t0, int l, int h,
+                                              int col, int grp, bf16x8 (&qa)[4]) {
+    const int t = min(t0 + col, a.n_q - 1);
+    const uint16_t *p = a.q_layers +
+                        (((size_t)l * a.rows + (size_t)b * a.n_q + t) * a.q_heads + h) * kKdDim +
+                        grp * 8;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) qa[kb] = kd_ld8(p + kb * 32);
+}
+
+// B operands of keys j0 + 16 * ct + col of KV head g (keys past len clamped to
+// the last one; their logits are masked by the caller).
+__device__ __forceinline__ void kd_load_keys(const KdArgs &a, int b, int j0, int len, int g,
+                                             int col, int grp, bf16x8 (&kv)[4][4]) {
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+        const int j = min(j0 + 16 * ct + col, len - 1);
+        const uint16_t *p = a.k_cache +
+                            token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b, j,
+                                         a.kv_heads * kKdDim) +
+                            g * kKdDim + grp * 8;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) kv[ct][kb] = kd_ld8(p + kb * 32);
+    }
+}
+
+// Unscaled logits of the lane's 4 rows x 4 keys: c[ct][r] = row 4 * grp + r,
+// key 16 * ct + col.
+__device__ __forceinline__ void kd_logits(const bf16x8 (&qa)[4], const bf16x8 (&kv)[4][4],
+                                          f32x4 (&c)[4]) {
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+        c[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            c[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb], kv[ct][kb], c[ct], 0, 0, 0);
+    }
+}
+
+// Largest / smallest of a per-lane-group value over the four groups of a wave.
+__device__ __forceinline__ int kd_groups_max(int v) {
+    v = max(v, __shfl_xor(v, 16));
+    return max(v, __shfl_xor(v, 32));
+}
+__device__ __forceinline__ int kd_groups_min(int v) {
+    v = min(v, __shfl_xor(v, 16));
+    return min(v, __shfl_xor(v, 32));
+}
+
+// grid: (((b * row_tiles + tile) * L + l) * group + hh) * kv_heads + g, so that
+// the workgroups of one KV head land on the same XCD when kv_heads divides 8.
+__global__ __launch_bounds__(256) void kd_lse_kernel(KdArgs a) {
+    int x = blockIdx.x;
+    const int g = x % a.kv_heads;
+    x /= a.kv_heads;
+    const int hh = x % a.group;
+    x /= a.group;
+    const int l = x % a.n_layers;
+    x /= a.n_layers;
+    const int tile = x % a.row_tiles, b = x / a.row_tiles;
+    const int h = g * a.group + hh;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int col = lane & 15, grp = lane >> 4;
+    const int t0 = tile * kKdTile + wave * 16;
+    if (t0 >= a.n_q) return;  // uniform per wave; no barriers
+    const int len = clamp_len(a.seq_lens[b], a.max_len);
+    int n[4];
+    kd_row_limits(a, b, t0, grp, n);
+    const int nmax = kd_groups_max(max(max(n[0], n[1]), max(n[2], n[3])));
+    bf16x8 qa[4];
+    kd_load_query(a, b, t0, l, h, col, grp, qa);
+    float m[4], s[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        m[r] = -INFINITY;
+        s[r] = 0.0f;
+    }
+    for (int j0 = 0; j0 < nmax; j0 += kKdTile) {
+        bf16x8 kv[4][4];
+        kd_load_keys(a, b, j0, len, g, col, grp, kv);
+        f32x4 c[4];
+        kd_logits(qa, kv, c);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float tm = -INFINITY;
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                c[ct][r] = j0 + 16 * ct + col < n[r] ? c[ct][r] * a.scale_log2 : -INFINITY;
+                tm = fmaxf(tm, c[ct][r]);
+            }
+            const float mn = fmaxf(m[r], row16_max(tm));
+            const float base = mn == -INFINITY ? 0.0f : mn;  // row without keys so far
+            float ps = 0.0f;
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) ps += exp2f(c[ct][r] - base);
+            s[r] = s[r] * exp2f(m[r] - base) + row16_sum(ps);
+            m[r] = mn;
+        }
+    }
+    if (col == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = t0 + 4 * grp + r;
+            if (t < a.n_q)
+                a.lse2[((size_t)l * a.rows + (size_t)b * a.n_q + t) * a.q_heads + h] =
+                    n[r] > 0 ? m[r] + log2f(s[r]) : -INFINITY;
+        }
+    }
+}
+
+// grid: (b * row_tiles + tile) * key_tiles + key tile.
+template <bool FULL>
+__device__ __forceinline__ void kd_target_tile(const KdArgs &a, int b, int t0, int j0, int len,
+                                               int col, int grp, const int (&n)[4],
+                                               f32x4 (&acc)[4]) {
+    for (int g = 0; g < a.kv_heads; ++g) {
+        bf16x8 kv[4][4];
+        kd_load_keys(a, b, j0, len, g, col, grp, kv);
+        for (int l = 0; l < a.n_layers; ++l) {
+            for (int hh = 0; hh < a.group; ++hh) {
+                const int h = g * a.group + hh;
+                bf16x8 qa[4];
+                kd_load_query(a, b, t0, l, h, col, grp, qa);
+                float lse[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = min(t0 + 4 * grp + r, a.n_q - 1);
+                    lse[r] = a.lse2[((size_t)l * a.rows + (size_t)b * a.n_q + t) * a.q_heads + h];
+                }
+                f32x4 c[4];
+                kd_logits(qa, kv, c);
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float e = exp2f(fmaf(c[ct][r], a.scale_log2, -lse[r]));
+                        if (FULL) acc[ct][r] += e;
+                        else acc[ct][r] += j0 + 16 * ct + col < n[r] ? e : 0.0f;
+                    }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
+    int x = blockIdx.x;
+    const int kt = x % a.key_tiles;
+    x /= a.key_tiles;
+    const int tile = x % a.row_tiles, b = x / a.row_tiles;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int col = lane & 15, grp = lane >> 4;
+    const int t0 = tile * kKdTile + wave * 16;
+    const int j0 = kt * kKdTile;
+    if (t0 >= a.n_q) return;  // uniform per wave; no barriers
+    int n[4];
+    kd_row_limits(a, b, t0, grp, n);
+    const int nmax = kd_groups_max(max(max(n[0], n[1]), max(n[2], n[3])));
+    const int nmin = kd_groups_min(min(min(n[0], n[1]), min(n[2], n[3])));
+    if (j0 >= nmax) return;  // no valid key of these rows in the tile
+    const int len = clamp_len(a.seq_lens[b], a.max_len);
+    f32x4 acc[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (j0 + kKdTile <= nmin) kd_target_tile<true>(a, b, t0, j0, len, col, grp, n, acc);
+    else kd_target_tile<false>(a, b, t0, j0, len, col, grp, n, acc);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int t = t0 + 4 * grp + r;
+        float *row = a.abar + ((size_t)b * a.n_q + t) * a.max_len;
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+            const int j = j0 + 16 * ct + col;
+            if (j < n[r]) row[j] = acc[ct][r] * a.inv_lh;
+        }
+    }
+}
+
+struct KdLossArgs {
+    const float *abar;         // [rows, max_len]
+    float *dI;                 // [rows, max_len]: index scores in, Q - P out
+    float *row_kl;             // [rows]
+    float *stats;              // [0] = 1 / n_rows (0 when none), [1] = n_rows
+    float *loss;
+    const uint16_t *q_idx;     // [rows, 256]
+    const uint16_t *k_idx;     // index-key cache
+    float *dq, *dk;
+    const int32_t *page_table, *seq_lens, *q_pos;
+    int n_q, rows, max_len, page_shift, max_pages, causal, row_tiles, key_tiles;
+};
+
+// One workgroup of 256 threads per row.
+__global__ __launch_bounds__(256) void kd_rows_kernel(KdLossArgs a) {
+    __shared__ float red_m[4], red_s[4];
+    const int row = blockIdx.x, b = row / a.n_q;
+    const int tid = threadIdx.x, wave = tid >> 6;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+    if (n == 0) {  // uniform: no keys, no loss term
+        if (tid == 0) a.row_kl[row] = 0.0f;
+        return;
+    }
+    float *s = a.dI + (size_t)row * a.max_len;
+    const float *p = a.abar + (size_t)row * a.max_len;
+    float m = -INFINITY, sum = 0.0f;  // log2 units
+    for (int j = tid; j < n; j += 256) {
+        const float x = s[j] * kKdLog2e;
+        if (x > m) {
+            sum = sum * exp2f(m - x) + 1.0f;
+            m = x;
+        } else {
+            sum += exp2f(x - m);
+        }
+    }
+    const float wm = wave_max(m);
+    const float ws = wave_sum(sum > 0.0f ? sum * exp2f(m - wm) : 0.0f);
+    if ((tid & 63) == 0) {
+        red_m[wave] = wm;
+        red_s[wave] = ws;
+    }
+    __syncthreads();
+    const float bm = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
+    float bs = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) bs += red_s[w] > 0.0f ? red_s[w] * exp2f(red_m[w] - bm) : 0.0f;
+    const float lse2 = bm + log2f(bs);
+    float kl = 0.0f;  // log2 units
+    for (int j = tid; j < n; j += 256) {
+        const float z = fmaf(s[j], kKdLog2e, -lse2);
+        const float pj = p[j];
+        if (pj > 0.0f) kl += pj * (log2f(pj) - z);
+        s[j] = exp2f(z) - pj;
+    }
+    kl = wave_sum(kl);
+    __syncthreads();  // red_s reads above are done
+    if ((tid & 63) == 0) red_s[wave] = kl;
+    __syncthreads();
+    if (tid == 0) a.row_kl[row] = (red_s[0] + red_s[1] + red_s[2] + red_s[3]) * kKdLn2;
+}
+
+// One workgroup: n_rows, 1 / n_rows and the mean row term.
+__global__ __launch_bounds__(256) void kd_loss_kernel(KdLossArgs a) {
+    __shared__ double red_t[256];
+    __shared__ int red_c[256];
+    const int tid = threadIdx.x;
+    double tot = 0.0;
+    int cnt = 0;
+    for (int r = tid; r < a.rows; r += 256) {
+        tot += (double)a.row_kl[r];
+        cnt += valid_keys(a.seq_lens, a.q_pos, a.causal, r / a.n_q, r, a.max_len) > 0;
+    }
+    red_t[tid] = tot;
+    red_c[tid] = cnt;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (tid < w) {
+            red_t[tid] += red_t[tid + w];
+            red_c[tid] += red_c[tid + w];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        const int nr = red_c[0];
+        a.loss[0] = nr > 0 ? (float)(red_t[0] / nr) : 0.0f;
+        a.stats[0] = nr > 0 ? 1.0f / (float)nr : 0.0f;
+        a.stats[1] = (float)nr;
+    }
+}
+
+constexpr int kGemmDepth = 32;      // contraction steps per LDS stage
+constexpr int kGemmPitch = 64 + 4;  // LDS row pitch (floats)
+
+// 8 bf16 -> 8 floats stored at dst (16-byte aligned).
+__device__ __forceinline__ void kd_store8(float *dst, u32x4 v) {
+    float4 lo = make_float4(bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y));
+    float4 hi = make_float4(bf16_lo(v.z), bf16_hi(v.z), bf16_lo(v.w), bf16_hi(v.w));
+    *reinterpret_cast<float4 *>(dst) = lo;
+    *reinterpret_cast<float4 *>(dst + 4) = hi;
+}
+
+__device__ __forceinline__ void kd_fma_tile(const float (*As)[kGemmPitch],
+                                            const float (*Bs)[kGemmPitch], int ty, int tx,
+                                            float (&acc)[4][4]) {
+#pragma unroll 8
+    for (int k = 0; k < kGemmDepth; ++k) {
+        const float4 av = *reinterpret_cast<const float4 *>(&As[k][ty * 4]);
+        const float4 bv = *reinterpret_cast<const float4 *>(&Bs[k][tx * 4]);
+        const float ar[4] = {av.x, av.y, av.z, av.w};
+        const float br[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], br[j], acc[i][j]);
+    }
+}
+
+// dq[b,t,c] = (1 / n_rows) sum_{j < n(b,t)} dI[b,t,j] k_idx[b,j,c].
+// grid: ((b * row_tiles + tile) * 4 + column tile), 64 rows x 64 columns each.
+__global__ __launch_bounds__(256) void kd_dq_kernel(KdLossArgs a) {
+    __shared__ __align__(16) float As[kGemmDepth][kGemmPitch];  // [key][row]
+    __shared__ __align__(16) float Bs[kGemmDepth][kGemmPitch];  // [key][column]
+    __shared__ int s_n[64];
+    int x = blockIdx.x;
+    const int c0 = (x & 3) * 64;
+    x >>= 2;
+    const int tile = x % a.row_tiles, b = x / a.row_tiles;
+    const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+    const int t0 = tile * 64;
+    if (tid < 64) {
+        const int t = t0 + tid;
+        s_n[tid] = t < a.n_q ? valid_keys(a.seq_lens, a.q_pos, a.causal, b, b * a.n_q + t, a.max_len)
+                             : 0;
+    }
+    __syncthreads();
+    int nmax = 0;
+    for (int i = 0; i < 64; ++i) nmax = max(nmax, s_n[i]);
+    float acc[4][4] = {};
+    const int ak = tid & 31, ai = tid >> 5;        // A loads: key ak, rows ai + 8 * step
+    const int bk = tid >> 3, bc = (tid & 7) * 8;   // B loads: key bk, columns bc .. bc + 7
+    for (int j0 = 0; j0 < nmax; j0 += kGemmDepth) {
+        const int j = j0 + ak;
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+            const int i = ai + 8 * st;
+            As[ak][i] = j < s_n[i] ? a.dI[((size_t)b * a.n_q + t0 + i) * a.max_len + j] : 0.0f;
+        }
+        const int jb = j0 + bk;
+        u32x4 kv = u32x4{0u, 0u, 0u, 0u};
+        if (jb < nmax)
+            kv = *reinterpret_cast<const u32x4 *>(
+                a.k_idx + token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b, jb,
+                                       kIdxDim) +
+                c0 + bc);
+        kd_store8(&Bs[bk][bc], kv);
+        __syncthreads();
+        kd_fma_tile(As, Bs, ty, tx, acc);
+        __syncthreads();
+    }
+    const float inv_n = a.stats[0];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int t = t0 + ty * 4 + i;
+        if (t < a.n_q)
+            *reinterpret_cast<float4 *>(a.dq + ((size_t)b * a.n_q + t) * kIdxDim + c0 + tx * 4) =
+                make_float4(acc[i][0] * inv_n, acc[i][1] * inv_n, acc[i][2] * inv_n,
+                            acc[i][3] * inv_n);
+    }
+}
+
+// dk[b,j,c] = (1 / n_rows) sum_{t : j < n(b,t)} dI[b,t,j] q_idx[b,t,c], for j < seq_lens[b].
+// grid: ((b * key_tiles + tile) * 4 + column tile), 64 keys x 64 columns each.
+__global__ __launch_bounds__(256) void kd_dk_kernel(KdLossArgs a) {
+    __shared__ __align__(16) float As[kGemmDepth][kGemmPitch];  // [row][key]
+    __shared__ __align__(16) float Bs[kGemmDepth][kGemmPitch];  // [row][column]
+    __shared__ int s_n[kGemmDepth];
+    int x = blockIdx.x;
+    const int c0 = (x & 3) * 64;
+    x >>= 2;
+    const int tile = x % a.key_tiles, b = x / a.key_tiles;
+    const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+    const int j0 = tile * 64;
+    const int len = clamp_len(a.seq_lens[b], a.max_len);
+    if (j0 >= len) return;  // uniform: no token of this tile is written
+    float acc[4][4] = {};
+    const int ai = tid & 63, ak = tid >> 6;        // A loads: key ai, rows ak + 4 * step
+    const int bk = tid >> 3, bc = (tid & 7) * 8;   // B loads: row bk, columns bc .. bc + 7
+    for (int r0 = 0; r0 < a.n_q; r0 += kGemmDepth) {
+        if (tid < kGemmDepth) {
+            const int t = r0 + tid;
+            s_n[tid] = t < a.n_q
+                           ? valid_keys(a.seq_lens, a.q_pos, a.causal, b, b * a.n_q + t, a.max_len)
+                           : 0;
+        }
+        // Skip the step when no row of it sees a key of the tile.
+        if (!__syncthreads_or(tid < kGemmDepth && s_n[tid] > j0)) continue;
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+            const int k = ak + 4 * st;
+            As[k][ai] = j0 + ai < s_n[k]
+                            ? a.dI[((size_t)b * a.n_q + r0 + k) * a.max_len + j0 + ai]
+                            : 0.0f;
+        }
+        const int t = r0 + bk;
+        u32x4 qv = u32x4{0u, 0u, 0u, 0u};
+        if (t < a.n_q)
+            qv = *reinterpret_cast<const u32x4 *>(a.q_idx + ((size_t)b * a.n_q + t) * kIdxDim + c0 +
+                                                  bc);
+        kd_store8(&Bs[bk][bc], qv);
+        __syncthreads();
+        kd_fma_tile(As, Bs, ty, tx, acc);
+        __syncthreads();
+    }
+    const float inv_n = a.stats[0];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int j = j0 + ty * 4 + i;
+        if (j < len)
+            *reinterpret_cast<float4 *>(
+                a.dk + token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b, j,
+                                    kIdxDim) +
+                c0 + tx * 4) = make_float4(acc[i][0] * inv_n, acc[i][1] * inv_n,
+                                           acc[i][2] * inv_n, acc[i][3] * inv_n);
+    }
+}
+
+static bool grid_fits(long long n) { return n >= 1 && n <= 0x7fffffffLL; }
+
+bool kd_target_supported(const Geometry &g, int n_layers) {
+    const long long tiles = (long long)g.batch * div_up(g.n_q, kKdTile);
+    return n_layers >= 1 && grid_fits(tiles * n_layers * g.q_heads) &&
+           grid_fits(tiles * div_up(g.max_len, kKdTile));
+}
+
+size_t kd_target_ws_floats(const Geometry &g, int n_layers) {
+    return (size_t)n_layers * g.rows * g.q_heads;
+}
+
+hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layers,
+                            const void *k_cache, const int32_t *page_table,
+                            const int32_t *seq_lens, const int32_t *q_pos, float *abar,
+                            float *lse2, hipStream_t stream) {
+    if (!kd_target_supported(g, n_layers)) return hipErrorInvalidValue;
+    KdArgs a;
+    a.q_layers = static_cast<const uint16_t *>(q_layers);
+    a.k_cache = static_cast<const uint16_t *>(k_cache);
+    a.page_table = page_table;
+    a.seq_lens = seq_lens;
+    a.q_pos = q_pos;
+    a.lse2 = lse2;
+    a.abar = abar;
+    a.n_layers = n_layers;
+    a.n_q = g.n_q;
+    a.rows = g.rows;
+    a.max_len = g.max_len;
+    a.page_shift = g.page_shift;
+    a.max_pages = g.max_pages;
+    a.causal = g.causal;
+    a.q_heads = g.q_heads;
+    a.kv_heads = g.kv_heads;
+    a.group = g.group;
+    a.row_tiles = div_up(g.n_q, kKdTile);
+    a.key_tiles = div_up(g.max_len, kKdTile);
+    a.scale_log2 = g.softmax_scale * kKdLog2e;
+    a.inv_lh = 1.0f / ((float)n_layers * (float)g.q_heads);
+    const long long tiles = (long long)g.batch * a.row_tiles;
+    kd_lse_kernel<<<dim3((unsigned)(tiles * n_layers * g.q_heads)), dim3(256), 0, stream>>>(a);
+    kd_target_kernel<<<dim3((unsigned)(tiles * a.key_tiles)), dim3(256), 0, stream>>>(a);
+    return hipGetLastError();
+}
+
+bool kd_loss_supported(const Geometry &g) {
+    return grid_fits((long long)g.batch * div_up(g.n_q, 64) * 4) &&
+           grid_fits((long long)g.batch * div_up(g.max_len, 64) * 4);
+}
+
+size_t kd_loss_ws_floats(const Geometry &g) {
+    return (size_t)g.rows * g.max_len + g.rows + 2;
+}
+
+hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_idx,
+                          const void *k_idx, const int32_t *page_table, const int32_t *seq_lens,
+                          const int32_t *q_pos, float *loss, float *dq, float *dk, float *ws,
+                          hipStream_t stream) {
+    if (!kd_loss_supported(g)) return hipErrorInvalidValue;
+    KdLossArgs a;
+    a.abar = abar;
+    a.dI = ws;
+    a.row_kl = ws + (size_t)g.rows * g.max_len;
+    a.stats = a.row_kl + g.rows;
+    a.loss = loss;
+    a.q_idx = static_cast<const uint16_t *>(q_idx);
+    a.k_idx = static_cast<const uint16_t *>(k_idx);
+    a.dq = dq;
+    a.dk = dk;
+    a.page_table = page_table;
+    a.seq_lens = seq_lens;
+    a.q_pos = q_pos;
+    a.n_q = g.n_q;
+    a.rows = g.rows;
+    a.max_len = g.max_len;
+    a.page_shift = g.page_shift;
+    a.max_pages = g.max_pages;
+    a.causal = g.causal;
+    a.row_tiles = div_up(g.n_q, 64);
+    a.key_tiles = div_up(g.max_len, 64);
+    // The scores of Eq. 3 for every valid (row, key), then the row terms in place.
+    hipError_t e = index_uses_mfma(g)
+                       ? launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
+                                              stream)
+                       : launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
+                                             nullptr, stream);
+    if (e != hipSuccess) return e;
+    kd_rows_kernel<<<dim3(g.rows), dim3(256), 0, stream>>>(a);
+    kd_loss_kernel<<<dim3(1), dim3(256), 0, stream>>>(a);
+    kd_dq_kernel<<<dim3((unsigned)(g.batch * a.row_tiles * 4)), dim3(256), 0, stream>>>(a);
+    kd_dk_kernel<<<dim3((unsigned)(g.batch * a.key_tiles * 4)), dim3(256), 0, stream>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace clsa

@@ -31,7 +31,7 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("clsa_index_scores", "clsa_topk", "clsa_sparse_attn", "clsa_decode_step",
               "clsa_decode_step_grouped", "clsa_dense_attn", "clsa_project_append",
-              "clsa_workspace_bytes",
+              "clsa_kd_target", "clsa_kd_loss", "clsa_workspace_bytes",
               "clsa_status_string", "clsa_set_phase_events"):
         assert n in names
 
@@ -253,3 +253,48 @@ def test_project_append_checks(lib):
     assert call(_shape(page_size=64, max_pages=16), pt=None) == -1
     assert call(_shape(idx_dim=32)) == -2
     assert call(_shape(head_dim=64)) == -2
+
+
+def test_kd_target_checks(lib):
+    from paper_2606_06467_amd import binding as B
+    def call(sh, L=4, ws=A, wsb=1 << 30, ql=A, kc=A, sl=A, qp=None, ab=A):
+        return lib.clsa_kd_target(ctypes.byref(sh), L, ql, kc, None, sl, qp, ab, ws, wsb, None)
+    sh = _shape(n_q=128, max_len=4096)
+    need = B.clsa_workspace_bytes(sh, B.CLSA_OP_KD_TARGET, 4)
+    assert need >= 4 * 128 * 32 * 4                       # one lse per (layer, row, head)
+    assert need > B.clsa_workspace_bytes(sh, B.CLSA_OP_KD_TARGET, 2)
+    assert B.clsa_workspace_bytes(sh, B.CLSA_OP_KD_TARGET, 0) == 0
+    assert call(sh, L=0) == -1
+    assert call(sh, ws=None, wsb=0) == -3
+    assert call(sh, wsb=need - 1) == -3
+    assert call(sh, ws=MIS, wsb=need) == -3                # workspace must be 256-byte aligned
+    assert call(sh, ql=MIS) == -1
+    assert call(sh, kc=None) == -1
+    assert call(sh, sl=None) == -1
+    assert call(sh, ab=None) == -1
+    assert call(_shape(n_q=128, max_len=4096, causal=True)) == -1        # causal needs q_pos
+    assert call(_shape(page_size=64, max_pages=16)) == -1                 # paged needs a table
+    assert call(_shape(head_dim=64)) == -2
+    assert call(_shape(q_heads=32, kv_heads=3)) == -1
+
+
+def test_kd_loss_checks(lib):
+    from paper_2606_06467_amd import binding as B
+    def call(sh, ws=A, wsb=1 << 40, ab=A, qi=A, ki=A, sl=A, qp=None, loss=A, dq=A, dk=A):
+        return lib.clsa_kd_loss(ctypes.byref(sh), ab, qi, ki, None, sl, qp, loss, dq, dk, ws, wsb,
+                                None)
+    sh = _shape(n_q=128, max_len=4096)
+    need = B.clsa_workspace_bytes(sh, B.CLSA_OP_KD_LOSS)
+    assert need >= 128 * 4096 * 4                          # scores, then dL/dI, per row and key
+    assert call(sh, ws=None, wsb=0) == -3
+    assert call(sh, wsb=need - 1) == -3
+    assert call(sh, ab=None) == -1
+    assert call(sh, qi=MIS) == -1
+    assert call(sh, ki=None) == -1
+    assert call(sh, loss=None) == -1
+    assert call(sh, dq=MIS) == -1                          # fp32 gradients in 16-byte vectors
+    assert call(sh, dk=None) == -1
+    assert call(_shape(n_q=128, max_len=4096, causal=True)) == -1
+    assert call(_shape(idx_dim=32)) == -2
+    assert call(_shape(max_len=262144 * 2)) == -2
+    assert B.clsa_workspace_bytes(_shape(idx_dim=32), B.CLSA_OP_KD_LOSS) == 0

@@ -1,0 +1,223 @@
+"""GPU parity of the distillation path (Section 2.2) against the fp64 oracle:
+clsa_kd_target (Eq. 5) and clsa_kd_loss (Eq. 6 with its index-query / index-key
+gradient).
+
+Tolerances follow from the fp32 arithmetic of the kernels (U = 2^-24):
+  * target: each logit carries at most scale * gamma_128 * |q| |k| of
+    accumulation error (bf16 products are exact in fp32); a probability of one
+    (layer, head) then carries twice that relative error plus the rounding of
+    the log-sum-exp (a sum over n keys), of exp2 and of the sum over L * Hq terms;
+  * loss: the index scores carry gamma_256 * sum |q_i k_i| (as in the indexer
+    tests); Q = softmax(I) then carries that error twice plus the rounding of
+    its log-sum-exp; dL/dI = Q - P adds one rounding; the gradients add the
+    fp32 accumulation of their n products (gamma_n), and the loss the rounding
+    of each row's terms.
+The abar fed to clsa_kd_loss is the oracle's Eq. 5 target rounded to fp32, and
+the oracle receives the same fp32 values, so only the loss arithmetic differs."""
+import numpy as np
+import pytest
+
+import oracle as orc
+from paper_2606_06467_amd import inputs
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+U32 = 2.0 ** -24
+LOG2E = 1.4426950408889634
+
+
+def _gamma(n):
+    return n * U32 / (1 - n * U32)
+
+
+def _f64(bits):
+    return inputs.f32_from_bf16_bits(bits).astype(np.float64)
+
+
+def _cache_rows(w, x, arr, b, n):
+    """Token rows 0..n-1 of sequence b of a cache array (contiguous or paged)."""
+    if n == 0:
+        return arr[:0].reshape((0,) + arr.shape[2:])
+    if w.page_size:
+        pages = x["page_table"][b, : (n + w.page_size - 1) // w.page_size]
+        return arr[pages].reshape((-1,) + arr.shape[2:])[:n]
+    return arr[b, :n]
+
+
+def _cache_index(w, x, b, j):
+    if w.page_size:
+        return (int(x["page_table"][b, j // w.page_size]), j % w.page_size)
+    return (b, j)
+
+
+def _target_tol(w, x, n_layers, abar_ref, nvalid):
+    """Per-element bound on |abar_gpu - abar_oracle| (see the module docstring)."""
+    scale = w.softmax_scale
+    ql = _f64(x["q_layers"]).reshape(n_layers, w.batch, w.n_q, w.q_heads, w.head_dim)
+    qn = np.sqrt((ql ** 2).sum(-1)).max(axis=(0, 3))           # [B, T]
+    kc = _f64(x["k_cache"])
+    kn = np.sqrt((kc ** 2).sum(-1)).max() if kc.size else 0.0
+    tol = np.zeros_like(abar_ref)
+    for b in range(w.batch):
+        for t in range(w.n_q):
+            n = int(nvalid[b, t])
+            if n == 0:
+                continue
+            dz = scale * _gamma(w.head_dim) * qn[b, t] * kn
+            zb = scale * qn[b, t] * kn + np.log(n)
+            rel = (2 * dz + U32 * (n / 16 + 64 + n_layers * w.q_heads)
+                   + 16 * U32 * (zb * LOG2E + 1))
+            tol[b, t, :n] = abar_ref[b, t, :n] * rel
+    return tol + 1e-30
+
+
+def _target_case(w, what):
+    import torch
+    from paper_2606_06467_amd import binding as B
+    x = inputs.make_inputs(w)
+    d = U.to_dev(x)
+    L = w.n_layers
+    sh = U.shape_of(w)
+    abar = torch.full((w.batch, w.n_q, w.max_len), float("nan"), device="cuda")
+    ws = B.workspace(sh, B.CLSA_OP_KD_TARGET, L)
+    U.log(f"  kd_target {what}: B={w.batch} T={w.n_q} max_len={w.max_len} L={L} "
+          f"Hq={w.q_heads} Hkv={w.kv_heads} paged={w.page_size}")
+    B.clsa_kd_target(sh, L, d["q_layers"], d["k_cache"], d["page_table"], d["seq_lens"],
+                     d["q_pos"], abar, ws)
+    torch.cuda.synchronize()
+    got = abar.cpu().numpy().astype(np.float64)
+    osh = orc.shape_of(w)
+    ref = orc.kd_target(osh, x["q_layers"], x["k_cache"], x["seq_lens"], x["q_pos"],
+                        x["page_table"])
+    nvalid = orc.valid_lens(osh, x["seq_lens"], x["q_pos"])
+    valid = np.arange(w.max_len)[None, None, :] < nvalid[:, :, None]
+    assert np.all(np.isnan(got[~valid])), "positions outside the valid keys were written"
+    assert np.isfinite(got[valid]).all()
+    tol = _target_tol(w, x, L, np.nan_to_num(ref), nvalid)
+    err = np.abs(got - ref)
+    worst = float((err[valid] / tol[valid]).max(initial=0.0))
+    U.log(f"    max|d|={float(err[valid].max(initial=0)):.3e}  worst err/bound={worst:.3f}")
+    assert np.all(err[valid] <= tol[valid]), what
+    rows = nvalid > 0
+    sums = got.copy()
+    sums[~valid] = 0.0
+    np.testing.assert_allclose(sums.sum(-1)[rows], 1.0, rtol=0, atol=1e-5)
+    return x, ref, nvalid
+
+
+@pytest.mark.parametrize("case", ["noncausal", "causal_tiles", "paged_gqa5", "single_key_row"])
+def test_target(case):
+    if case == "noncausal":
+        w = inputs.small_workload(batch=2, lens=(300, 777), n_q=3, n_layers=2, wid=81)
+    elif case == "causal_tiles":   # 3 row tiles with a ragged tail, 11 key tiles, diagonal masks
+        w = inputs.small_workload(batch=2, lens=(700, 450), n_q=150, causal=True,
+                                  q_pos0=(550, 300), n_layers=2, wid=82)
+    elif case == "paged_gqa5":     # group of 5 query heads, an empty sequence, pages shuffled
+        w = inputs.small_workload(batch=3, lens=(500, 0, 260), n_q=2, page_size=64, q_heads=20,
+                                  kv_heads=4, n_layers=3, wid=83)
+    else:                          # row 0 sees one key: its target is exactly 1
+        w = inputs.small_workload(batch=1, lens=(200,), n_q=70, causal=True, q_pos0=(0,),
+                                  n_layers=1, wid=84)
+    _target_case(w, case)
+
+
+def _loss_bounds(w, x, abar, nvalid):
+    """Bounds on the loss, dq and dk differences (see the module docstring)."""
+    osh = orc.shape_of(w)
+    s64 = orc.index_scores(osh, x["q_idx"], x["k_idx"], x["seq_lens"], x["q_pos"],
+                           x["page_table"], fill=0.0)
+    hb = U.higham_bound(w, x)
+    qi = _f64(x["q_idx"]).reshape(w.batch, w.n_q, -1)
+    ki = _f64(x["k_idx"])
+    n_rows = int((nvalid > 0).sum())
+    e_dq = np.zeros_like(qi)
+    e_dk = np.zeros(ki.shape[:-2] + (ki.shape[-2] * ki.shape[-1],))
+    e_loss = 0.0
+    for b in range(w.batch):
+        kb = np.abs(_cache_rows(w, x, ki, b, w.lens[b]).reshape(w.lens[b], qi.shape[-1]))
+        acc_dk = np.zeros_like(kb)
+        for t in range(w.n_q):
+            n = int(nvalid[b, t])
+            if n == 0:
+                continue
+            s = s64[b, t, :n]
+            lse = s.max() + np.log(np.exp(s - s.max()).sum())
+            Q = np.exp(s - lse)
+            P = abar[b, t, :n]
+            ds = hb[b, t, :n]
+            rho = ds + ds.max() + U32 * (n / 16 + 32) + 8 * U32 * (np.abs(s - lse) * LOG2E + 1)
+            eI = Q * rho + 2 * U32 * (Q + P)
+            dI = np.abs(Q - P)
+            e_dq[b, t] = (eI @ kb[:n] + _gamma(n + 1) * (dI @ kb[:n])) / n_rows
+            acc_dk[:n] += np.outer(eI + _gamma(w.n_q + 1) * dI, np.abs(qi[b, t]))
+            pos = P > 0
+            terms = np.abs(P[pos] * (np.log(P[pos]) - (s[pos] - lse)))
+            e_loss += float((P * rho).sum() + (n + 8) * U32 * terms.sum()
+                            + 8 * U32 * (P[pos] * (np.abs(np.log2(P[pos])) + 1)).sum())
+        for j in range(w.lens[b]):
+            e_dk[_cache_index(w, x, b, j)] = acc_dk[j] / n_rows
+    return (e_loss / max(n_rows, 1)), e_dq, e_dk
+
+
+def _loss_case(w, what, abar64=None):
+    import torch
+    from paper_2606_06467_amd import binding as B
+    x = inputs.make_inputs(w)
+    osh = orc.shape_of(w)
+    nvalid = orc.valid_lens(osh, x["seq_lens"], x["q_pos"])
+    if abar64 is None:
+        abar64 = orc.kd_target(osh, x["q_layers"], x["k_cache"], x["seq_lens"], x["q_pos"],
+                               x["page_table"], fill=0.0)
+    abar32 = abar64.astype(np.float32)
+    d = U.to_dev(x)
+    sh = U.shape_of(w)
+    abar = torch.from_numpy(abar32).cuda()
+    loss = torch.full((1,), float("nan"), device="cuda")
+    dq = torch.full(x["q_idx"].shape, float("nan"), device="cuda")
+    dk = torch.full(x["k_idx"].shape, float("nan"), device="cuda")
+    ws = B.workspace(sh, B.CLSA_OP_KD_LOSS)
+    U.log(f"  kd_loss {what}: B={w.batch} T={w.n_q} max_len={w.max_len} paged={w.page_size} "
+          f"causal={w.causal}")
+    B.clsa_kd_loss(sh, abar, d["q_idx"], d["k_idx"], d["page_table"], d["seq_lens"], d["q_pos"],
+                   loss, dq, dk, ws)
+    torch.cuda.synchronize()
+    a_in = abar32.astype(np.float64)
+    r_loss, r_dq, r_dk = orc.kd_loss(osh, a_in, x["q_idx"], x["k_idx"], x["seq_lens"],
+                                     x["q_pos"], x["page_table"])
+    e_loss, e_dq, e_dk = _loss_bounds(w, x, a_in, nvalid)
+    g_loss = float(loss.item())
+    g_dq = dq.cpu().numpy().astype(np.float64)
+    g_dk = dk.cpu().numpy().astype(np.float64)
+    U.log(f"    loss gpu={g_loss:.8g} oracle={r_loss:.8g} |d|={abs(g_loss - r_loss):.2e} "
+          f"bound={e_loss + 4 * U32 * abs(r_loss):.2e}")
+    assert abs(g_loss - r_loss) <= e_loss + 4 * U32 * abs(r_loss) + 1e-12
+    r_dq = r_dq.reshape(g_dq.shape)
+    e_dq = e_dq.reshape(g_dq.shape) + 4 * U32 * np.abs(r_dq) + 1e-30
+    assert np.isfinite(g_dq).all(), "every dq row is written"
+    assert np.all(np.abs(g_dq - r_dq) <= e_dq), (what, float((np.abs(g_dq - r_dq) / e_dq).max()))
+    written = ~np.isnan(r_dk)
+    assert np.array_equal(written, ~np.isnan(g_dk)), "dk rows written differ"
+    e_dk = e_dk.reshape(g_dk.shape) + 4 * U32 * np.abs(np.nan_to_num(r_dk)) + 1e-30
+    dd = np.abs(g_dk - r_dk)[written]
+    assert np.all(dd <= e_dk[written]), (what, float((dd / e_dk[written]).max(initial=0)))
+    U.log(f"    dq max|d|={float(np.abs(g_dq - r_dq).max(initial=0)):.2e} "
+          f"(bound ratio {float((np.abs(g_dq - r_dq) / e_dq).max(initial=0)):.3f}); "
+          f"dk max|d|={float(dd.max(initial=0)):.2e} "
+          f"(bound ratio {float((dd / e_dk[written]).max(initial=0)):.3f})")
+
+
+@pytest.mark.parametrize("case", ["decode_rows_empty_seq", "causal_prefill", "paged",
+                                  "all_empty"])
+def test_loss(case):
+    if case == "decode_rows_empty_seq":   # few rows: the wavefront indexer; n_rows = 2
+        w = inputs.small_workload(batch=3, lens=(300, 0, 777), n_layers=2, wid=85)
+    elif case == "causal_prefill":        # many rows: the matrix-core indexer
+        w = inputs.small_workload(batch=2, lens=(700, 450), n_q=150, causal=True,
+                                  q_pos0=(550, 300), n_layers=2, wid=86)
+    elif case == "paged":
+        w = inputs.small_workload(batch=2, lens=(610, 130), n_q=40, causal=True,
+                                  q_pos0=(570, 90), page_size=64, n_layers=1, wid=87)
+    else:                                 # no row has a key: loss 0, dq 0, dk untouched
+        w = inputs.small_workload(batch=2, lens=(0, 0), n_q=3, n_layers=1, wid=88)
+    _loss_case(w, case)
