@@ -209,8 +209,9 @@ clsa_status clsa_project_append(const clsa_shape *shape, int32_t d_model, const 
  * j <= q_pos[b,t] when causal) of the one shared key cache, g(h) =
  * h / (q_heads / kv_heads).  abar: fp32 [batch, n_q, max_len]; only the valid
  * positions of each row are written (a row without valid keys is left as it
- * is).  bf16 inputs, fp32 logits and softmax.  n_layers >= 1; v_cache is not
- * read.  Workspace: CLSA_OP_KD_TARGET with the same n_layers. */
+ * is).  bf16 inputs, fp32 logits and softmax.  n_layers >= 1 and
+ * softmax_scale > 0; v_cache is not read.  Workspace: CLSA_OP_KD_TARGET with
+ * the same n_layers. */
 clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void *q_layers,
                            const void *k_cache, const int32_t *page_table,
                            const int32_t *seq_lens, const int32_t *q_pos, float *abar, void *ws,

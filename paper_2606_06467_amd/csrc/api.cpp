@@ -458,7 +458,7 @@ clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void
                            size_t ws_bytes, void *stream) {
     Geometry g;
     CLSA_TRY(check_shape(shape, kAttn, &g));
-    if (n_layers < 1) return CLSA_ERR_INVALID_ARG;
+    if (n_layers < 1 || !(shape->softmax_scale > 0.0f)) return CLSA_ERR_INVALID_ARG;
     if (!clsa::kd_target_supported(g, n_layers)) return CLSA_ERR_UNSUPPORTED;
     CLSA_TRY(check_ptr(q_layers, 16));
     CLSA_TRY(check_ptr(k_cache, 16));

@@ -8,12 +8,15 @@
 // keys; lane l supplies row / key (l & 15) for dims (l >> 4) * 8 .. +8 and
 // receives rows 4 * (l >> 4) + r of key (l & 15), so the 16 keys of one row
 // sit in one DPP row of 16 lanes):
-//   * kd_lse_kernel: per (64-row tile, layer, head), an online softmax over the
-//     row's keys gives each row's log-sum-exp (log2 units, in the workspace);
-//   * kd_target_kernel: per (64-row, 64-key) tile, every (layer, head) adds
+//   * kd_lse_kernel: per (64-row tile, layer, up to 4 heads of one KV head), an
+//     online softmax over the row's keys gives each row's log-sum-exp (log2
+//     units, in the workspace); each lane keeps statistics over its own keys
+//     and the 16 lanes of a row are combined once at the end;
+//   * kd_target_kernel: per (16-row, 64-key) tile, every (layer, head) adds
 //     exp(logit - lse) into the tile held in registers; the key operands of a
-//     KV head are loaded once for all layers and heads of its group, and abar
-//     is written once, with no atomics.
+//     KV head are loaded once for all layers and heads of its group, the four
+//     waves of a workgroup share their rows' query operands, and abar is
+//     written once, with no atomics.
 // Eq. 6: P = abar (a constant), Q = softmax(I_t) over the valid keys, I the
 // unscaled index scores of Eq. 3 (computed by the indexer kernels); the loss
 // is the mean over rows with at least one key of KL(P || Q), and
@@ -43,12 +46,17 @@ struct KdArgs {
     const uint16_t *q_layers;  // [L, rows, Hq, 128]
     const uint16_t *k_cache;   // [B, max_len, Hkv, 128] | paged
     const int32_t *page_table, *seq_lens, *q_pos;
-    float *lse2;               // [L, rows, Hq], log2 units
+    float *lse2;               // [L, Hq, rows_pad], log2 units (rows_pad = rows + 16)
     float *abar;               // [rows, max_len]
-    int n_layers, n_q, rows, max_len, page_shift, max_pages, causal;
-    int q_heads, kv_heads, group, row_tiles, key_tiles;
+    int n_layers, batch, n_q, rows, max_len, page_shift, max_pages, causal;
+    int q_heads, kv_heads, group, row_tiles, key_tiles, rows_pad;
     float scale_log2, inv_lh;  // softmax_scale * log2(e), 1 / (L * Hq)
 };
+
+// 2^x by the hardware instruction alone: results below 2^-126 may flush to
+// zero, which is far below every tolerance here (exp2f adds a rescaling for
+// such results, five more VALU operations per call).
+__device__ __forceinline__ float kd_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ bf16x8 kd_ld8(const uint16_t *p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
@@ -77,16 +85,25 @@ __device__ __forceinline__ void kd_load_query(const KdArgs &a, int b, int t0, in
 }
 
 // B operands of keys j0 + 16 * ct + col of KV head g (keys past len clamped to
-// the last one; their logits are masked by the caller).
+// the last one; their logits are masked by the caller).  Paged caches: the four
+// page-table reads are issued together, before the key reads.
+template <bool PAGED>
 __device__ __forceinline__ void kd_load_keys(const KdArgs &a, int b, int j0, int len, int g,
                                              int col, int grp, bf16x8 (&kv)[4][4]) {
+    size_t tok[4];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
         const int j = min(j0 + 16 * ct + col, len - 1);
-        const uint16_t *p = a.k_cache +
-                            token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b, j,
-                                         a.kv_heads * kKdDim) +
-                            g * kKdDim + grp * 8;
+        if (PAGED) {
+            const int page = a.page_table[(size_t)b * a.max_pages + (j >> a.page_shift)];
+            tok[ct] = ((size_t)page << a.page_shift) + (j & ((1 << a.page_shift) - 1));
+        } else {
+            tok[ct] = (size_t)b * a.max_len + j;
+        }
+    }
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+        const uint16_t *p = a.k_cache + (tok[ct] * a.kv_heads + g) * kKdDim + grp * 8;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) kv[ct][kb] = kd_ld8(p + kb * 32);
     }
@@ -115,122 +132,264 @@ __device__ __forceinline__ int kd_groups_min(int v) {
     return min(v, __shfl_xor(v, 32));
 }
 
-// grid: (((b * row_tiles + tile) * L + l) * group + hh) * kv_heads + g, so that
-// the workgroups of one KV head land on the same XCD when kv_heads divides 8.
+// IEEE maximum (gfx950 v_maximum3_f32; no operand canonicalisation).
+__device__ __forceinline__ float kd_max(float x, float y) {
+    return __builtin_elementwise_maximum(x, y);
+}
+
+// Online softmax statistics of the lane's four rows over the lane's own four
+// keys of a tile: m is the largest unscaled logit so far (the scale is > 0, so
+// it keeps the order) and s the sum of 2^(sl * (z - m)); the 16 lanes of a row
+// are combined at the end.
+template <bool FULL>
+__device__ __forceinline__ void kd_stats_update(const f32x4 (&c)[4], float sl, int j0, int col,
+                                                const int (&n)[4], float (&m)[4], float (&s)[4]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float v[4];
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+            v[ct] = FULL || j0 + 16 * ct + col < n[r] ? c[ct][r] : -INFINITY;
+        const float mn = kd_max(kd_max(kd_max(v[0], v[1]), kd_max(v[2], v[3])), m[r]);
+        const float base = FULL ? mn * sl : (mn == -INFINITY ? 0.0f : mn * sl);  // no key yet
+        const float e = (kd_exp2(fmaf(v[0], sl, -base)) + kd_exp2(fmaf(v[1], sl, -base))) +
+                        (kd_exp2(fmaf(v[2], sl, -base)) + kd_exp2(fmaf(v[3], sl, -base)));
+        s[r] = fmaf(s[r], kd_exp2(fmaf(m[r], sl, -base)), e);
+        m[r] = mn;
+    }
+}
+
+constexpr int kStagePitch = kKdDim + 8;  // bf16 per staged row (272 bytes): the 16 rows read
+                                         // by one 16-lane group fall on distinct banks
+
+// Log-sum-exp (log2 units) of every (layer, query head, row): a workgroup holds
+// 64 rows (16 per wave) and HP heads of one KV head, the query operands in
+// registers.  The key tiles of that KV head stream through LDS, double-buffered
+// and shared by the four waves (one barrier per tile); each key tile serves HP
+// heads.  grid: (((b * row_tiles + tile) * L + l) * (group / HP) + head block)
+// * kv_heads + g, so that the workgroups of one KV head land on the same XCD
+// when kv_heads divides 8.
+template <int HP, bool PAGED>
 __global__ __launch_bounds__(256) void kd_lse_kernel(KdArgs a) {
+    __shared__ __align__(16) uint16_t s_k[2][kKdTile][kStagePitch];
+    __shared__ int s_nmax[4];
     int x = blockIdx.x;
     const int g = x % a.kv_heads;
     x /= a.kv_heads;
-    const int hh = x % a.group;
-    x /= a.group;
+    const int hsplit = a.group / HP;
+    const int hs = x % hsplit;
+    x /= hsplit;
     const int l = x % a.n_layers;
     x /= a.n_layers;
     const int tile = x % a.row_tiles, b = x / a.row_tiles;
-    const int h = g * a.group + hh;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int h0 = g * a.group + hs * HP;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 15, grp = lane >> 4;
     const int t0 = tile * kKdTile + wave * 16;
-    if (t0 >= a.n_q) return;  // uniform per wave; no barriers
     const int len = clamp_len(a.seq_lens[b], a.max_len);
     int n[4];
-    kd_row_limits(a, b, t0, grp, n);
+    kd_row_limits(a, b, t0, grp, n);  // 0 for rows past n_q
     const int nmax = kd_groups_max(max(max(n[0], n[1]), max(n[2], n[3])));
-    bf16x8 qa[4];
-    kd_load_query(a, b, t0, l, h, col, grp, qa);
-    float m[4], s[4];
+    const int nmin = kd_groups_min(min(min(n[0], n[1]), min(n[2], n[3])));
+    if (lane == 0) s_nmax[wave] = nmax;
+    bf16x8 q[HP][4];
+    if (t0 < a.n_q) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        m[r] = -INFINITY;
-        s[r] = 0.0f;
+        for (int hh = 0; hh < HP; ++hh) kd_load_query(a, b, t0, l, h0 + hh, col, grp, q[hh]);
     }
-    for (int j0 = 0; j0 < nmax; j0 += kKdTile) {
-        bf16x8 kv[4][4];
-        kd_load_keys(a, b, j0, len, g, col, grp, kv);
-        f32x4 c[4];
-        kd_logits(qa, kv, c);
+    float m[HP][4], s[HP][4];
+#pragma unroll
+    for (int hh = 0; hh < HP; ++hh)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            float tm = -INFINITY;
-#pragma unroll
-            for (int ct = 0; ct < 4; ++ct) {
-                c[ct][r] = j0 + 16 * ct + col < n[r] ? c[ct][r] * a.scale_log2 : -INFINITY;
-                tm = fmaxf(tm, c[ct][r]);
-            }
-            const float mn = fmaxf(m[r], row16_max(tm));
-            const float base = mn == -INFINITY ? 0.0f : mn;  // row without keys so far
-            float ps = 0.0f;
-#pragma unroll
-            for (int ct = 0; ct < 4; ++ct) ps += exp2f(c[ct][r] - base);
-            s[r] = s[r] * exp2f(m[r] - base) + row16_sum(ps);
-            m[r] = mn;
+            m[hh][r] = -INFINITY;
+            s[hh][r] = 0.0f;
         }
-    }
-    if (col == 0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int t = t0 + 4 * grp + r;
-            if (t < a.n_q)
-                a.lse2[((size_t)l * a.rows + (size_t)b * a.n_q + t) * a.q_heads + h] =
-                    n[r] > 0 ? m[r] + log2f(s[r]) : -INFINITY;
-        }
-    }
-}
+    __syncthreads();
+    const int wg_max = max(max(s_nmax[0], s_nmax[1]), max(s_nmax[2], s_nmax[3]));
+    const int tiles = div_up(wg_max, kKdTile);
 
-// grid: (b * row_tiles + tile) * key_tiles + key tile.
-template <bool FULL>
-__device__ __forceinline__ void kd_target_tile(const KdArgs &a, int b, int t0, int j0, int len,
-                                               int col, int grp, const int (&n)[4],
-                                               f32x4 (&acc)[4]) {
-    for (int g = 0; g < a.kv_heads; ++g) {
-        bf16x8 kv[4][4];
-        kd_load_keys(a, b, j0, len, g, col, grp, kv);
-        for (int l = 0; l < a.n_layers; ++l) {
-            for (int hh = 0; hh < a.group; ++hh) {
-                const int h = g * a.group + hh;
-                bf16x8 qa[4];
-                kd_load_query(a, b, t0, l, h, col, grp, qa);
-                float lse[4];
+    // staging: thread -> key row kr of the tile, 16-byte pieces 4 * kq .. 4 * kq + 3
+    const int kr = tid >> 2, kq = tid & 3;
+    auto fetch = [&](int u, u32x4 (&v)[4]) {
+        const int j = min(u * kKdTile + kr, len - 1);
+        size_t tok;
+        if (PAGED) {
+            const int page = a.page_table[(size_t)b * a.max_pages + (j >> a.page_shift)];
+            tok = ((size_t)page << a.page_shift) + (j & ((1 << a.page_shift) - 1));
+        } else {
+            tok = (size_t)b * a.max_len + j;
+        }
+        const uint16_t *p = a.k_cache + (tok * a.kv_heads + g) * kKdDim + kq * 32;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = min(t0 + 4 * grp + r, a.n_q - 1);
-                    lse[r] = a.lse2[((size_t)l * a.rows + (size_t)b * a.n_q + t) * a.q_heads + h];
-                }
+        for (int i = 0; i < 4; ++i) v[i] = *reinterpret_cast<const u32x4 *>(p + i * 8);
+    };
+    auto stage = [&](int buf, const u32x4 (&v)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            *reinterpret_cast<u32x4 *>(&s_k[buf][kr][kq * 32 + i * 8]) = v[i];
+    };
+    u32x4 v[4];
+    if (tiles > 0) {
+        fetch(0, v);
+        stage(0, v);
+    }
+    __syncthreads();
+    for (int u = 0; u < tiles; ++u) {
+        if (u + 1 < tiles) fetch(u + 1, v);
+        const int j0 = u * kKdTile;
+        if (j0 < nmax) {  // uniform per wave
+            const int buf = u & 1;
+            bf16x8 kv[4][4];
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+                    kv[ct][kb] = *reinterpret_cast<const bf16x8 *>(
+                        &s_k[buf][16 * ct + col][kb * 32 + grp * 8]);
+            const bool full = j0 + kKdTile <= nmin;
+#pragma unroll
+            for (int hh = 0; hh < HP; ++hh) {
                 f32x4 c[4];
-                kd_logits(qa, kv, c);
-#pragma unroll
-                for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const float e = exp2f(fmaf(c[ct][r], a.scale_log2, -lse[r]));
-                        if (FULL) acc[ct][r] += e;
-                        else acc[ct][r] += j0 + 16 * ct + col < n[r] ? e : 0.0f;
-                    }
+                kd_logits(q[hh], kv, c);
+                if (full) kd_stats_update<true>(c, a.scale_log2, j0, col, n, m[hh], s[hh]);
+                else kd_stats_update<false>(c, a.scale_log2, j0, col, n, m[hh], s[hh]);
             }
         }
+        if (u + 1 < tiles) stage((u + 1) & 1, v);
+        __syncthreads();
     }
+    if (t0 >= a.n_q) return;
+#pragma unroll
+    for (int hh = 0; hh < HP; ++hh)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float mr = row16_max(m[hh][r]);
+            const float part =
+                m[hh][r] == -INFINITY ? 0.0f : s[hh][r] * exp2f((m[hh][r] - mr) * a.scale_log2);
+            const float sr = row16_sum(part);
+            const int t = t0 + 4 * grp + r;
+            if (col == 0 && t < a.n_q)
+                a.lse2[((size_t)l * a.q_heads + h0 + hh) * a.rows_pad + (size_t)b * a.n_q + t] =
+                    n[r] > 0 ? mr * a.scale_log2 + log2f(sr) : -INFINITY;
+        }
 }
 
+constexpr int kTgtChunk = 4;              // (layer, head) combinations per LDS stage
+
+template <bool FULL>
+__device__ __forceinline__ void kd_accumulate(float sl, const bf16x8 (&qa)[4],
+                                              const float4 &lse, const bf16x8 (&kv)[4][4],
+                                              int j0, int col, const int (&n)[4],
+                                              f32x4 (&acc)[4]) {
+    f32x4 c[4];
+    kd_logits(qa, kv, c);
+    const float lr[4] = {lse.x, lse.y, lse.z, lse.w};
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float e = kd_exp2(fmaf(c[ct][r], sl, -lr[r]));
+            if (FULL) acc[ct][r] += e;
+            else acc[ct][r] += j0 + 16 * ct + col < n[r] ? e : 0.0f;
+        }
+}
+
+// A workgroup covers 16 rows x 256 keys: each of its four waves holds the key
+// operands of one 64-key tile of the current KV head in registers, and the
+// query operands and log-sum-exps of the 16 rows are staged through LDS,
+// kTgtChunk (layer, head) combinations at a time, double-buffered: the next
+// stage's global reads are in flight while the current one is on the matrix
+// cores, one barrier per stage.  Workgroups are dealt to the 8 XCDs in turn;
+// the mapping gives every key block of a row block to the same XCD, one after
+// another, so the 2 MB of query operands of a row block (16 rows x every layer
+// and head) are read from that XCD's L2.
+// grid: ((row block group * key_blocks + key block) * 8 + xcd); row block
+// index over all sequences = row block group * 8 + xcd.
+template <bool PAGED>
 __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
-    int x = blockIdx.x;
-    const int kt = x % a.key_tiles;
-    x /= a.key_tiles;
-    const int tile = x % a.row_tiles, b = x / a.row_tiles;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    __shared__ __align__(16) uint16_t s_q[2][kTgtChunk][16][kStagePitch];
+    __shared__ __align__(16) float s_l[2][kTgtChunk][16];
+    const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+    const int kblk = local % a.key_tiles;
+    const int rb_all = (local / a.key_tiles) * 8 + xcd;
+    if (rb_all >= a.batch * a.row_tiles) return;  // padding of the last group (uniform)
+    const int rblk = rb_all % a.row_tiles, b = rb_all / a.row_tiles;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 15, grp = lane >> 4;
-    const int t0 = tile * kKdTile + wave * 16;
-    const int j0 = kt * kKdTile;
-    if (t0 >= a.n_q) return;  // uniform per wave; no barriers
+    const int t0 = rblk * 16;
+    const int j0 = (kblk * 4 + wave) * kKdTile;
     int n[4];
     kd_row_limits(a, b, t0, grp, n);
     const int nmax = kd_groups_max(max(max(n[0], n[1]), max(n[2], n[3])));
     const int nmin = kd_groups_min(min(min(n[0], n[1]), min(n[2], n[3])));
-    if (j0 >= nmax) return;  // no valid key of these rows in the tile
+    if (kblk * 4 * kKdTile >= nmax) return;  // no valid key in the block (uniform)
+    const bool active = j0 < nmax;            // this wave's tile has valid keys
+    const bool full = j0 + kKdTile <= nmin;
     const int len = clamp_len(a.seq_lens[b], a.max_len);
+
+    // staging: thread -> (row sr, 16-byte piece sd) of every combination of a stage
+    const int sr = tid >> 4, sd = tid & 15;
+    const size_t layer_q = (size_t)a.rows * a.q_heads * kKdDim;
+    const uint16_t *qsrc = a.q_layers +
+                           ((size_t)b * a.n_q + min(t0 + sr, a.n_q - 1)) * a.q_heads * kKdDim +
+                           sd * 8;
+    const int combos = a.n_layers * a.group;
+    const int nchunk = div_up(combos, kTgtChunk);
+    const int stages = a.kv_heads * nchunk;
+    auto fetch = [&](int u, u32x4 (&v)[kTgtChunk], float &lv) {
+        const int g = u / nchunk, c0 = (u % nchunk) * kTgtChunk;
+#pragma unroll
+        for (int c = 0; c < kTgtChunk; ++c) {
+            const int ci = min(c0 + c, combos - 1);
+            const int l = ci / a.group, h = g * a.group + ci % a.group;
+            v[c] = *reinterpret_cast<const u32x4 *>(qsrc + l * layer_q + (size_t)h * kKdDim);
+        }
+        if (tid < kTgtChunk * 16) {
+            const int ci = min(c0 + (tid >> 4), combos - 1);
+            const int l = ci / a.group, h = g * a.group + ci % a.group;
+            lv = a.lse2[((size_t)l * a.q_heads + h) * a.rows_pad + (size_t)b * a.n_q + t0 +
+                        (tid & 15)];
+        }
+    };
+    auto stage = [&](int buf, const u32x4 (&v)[kTgtChunk], float lv) {
+#pragma unroll
+        for (int c = 0; c < kTgtChunk; ++c)
+            *reinterpret_cast<u32x4 *>(&s_q[buf][c][sr][sd * 8]) = v[c];
+        if (tid < kTgtChunk * 16) s_l[buf][tid >> 4][tid & 15] = lv;
+    };
+
     f32x4 acc[4];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (j0 + kKdTile <= nmin) kd_target_tile<true>(a, b, t0, j0, len, col, grp, n, acc);
-    else kd_target_tile<false>(a, b, t0, j0, len, col, grp, n, acc);
+    u32x4 v[kTgtChunk];
+    float lv = 0.0f;
+    fetch(0, v, lv);
+    stage(0, v, lv);
+    __syncthreads();
+    bf16x8 kv[4][4];
+    for (int u = 0; u < stages; ++u) {
+        const int k = u % nchunk;
+        if (k == 0 && active) kd_load_keys<PAGED>(a, b, j0, len, u / nchunk, col, grp, kv);
+        if (u + 1 < stages) fetch(u + 1, v, lv);
+        if (active) {
+            const int buf = u & 1;
+#pragma unroll
+            for (int c = 0; c < kTgtChunk; ++c) {
+                if (k * kTgtChunk + c >= combos) break;  // uniform: short last stage
+                bf16x8 qa[4];
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+                    qa[kb] = *reinterpret_cast<const bf16x8 *>(&s_q[buf][c][col][kb * 32 + grp * 8]);
+                const float4 lse = *reinterpret_cast<const float4 *>(&s_l[buf][c][4 * grp]);
+                if (full) kd_accumulate<true>(a.scale_log2, qa, lse, kv, j0, col, n, acc);
+                else kd_accumulate<false>(a.scale_log2, qa, lse, kv, j0, col, n, acc);
+            }
+        }
+        if (u + 1 < stages) stage((u + 1) & 1, v, lv);
+        __syncthreads();
+    }
+    if (!active) return;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int t = t0 + 4 * grp + r;
@@ -471,14 +630,18 @@ __global__ __launch_bounds__(256) void kd_dk_kernel(KdLossArgs a) {
 
 static bool grid_fits(long long n) { return n >= 1 && n <= 0x7fffffffLL; }
 
+// Row blocks of 16 and key blocks of 256 for the target pass; the lane offsets
+// into one layer's queries must fit 32 bits.
 bool kd_target_supported(const Geometry &g, int n_layers) {
     const long long tiles = (long long)g.batch * div_up(g.n_q, kKdTile);
+    const long long blocks = (long long)g.batch * div_up(g.n_q, 16);
     return n_layers >= 1 && grid_fits(tiles * n_layers * g.q_heads) &&
-           grid_fits(tiles * div_up(g.max_len, kKdTile));
+           grid_fits((blocks + 7) / 8 * 8 * div_up(g.max_len, 4 * kKdTile)) &&
+           (long long)g.rows * g.q_heads * kKdDim * 2 < (1LL << 31);
 }
 
 size_t kd_target_ws_floats(const Geometry &g, int n_layers) {
-    return (size_t)n_layers * g.rows * g.q_heads;
+    return (size_t)n_layers * g.q_heads * ((size_t)g.rows + 16);
 }
 
 hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layers,
@@ -495,6 +658,7 @@ hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layer
     a.lse2 = lse2;
     a.abar = abar;
     a.n_layers = n_layers;
+    a.batch = g.batch;
     a.n_q = g.n_q;
     a.rows = g.rows;
     a.max_len = g.max_len;
@@ -506,11 +670,32 @@ hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layer
     a.group = g.group;
     a.row_tiles = div_up(g.n_q, kKdTile);
     a.key_tiles = div_up(g.max_len, kKdTile);
+    a.rows_pad = g.rows + 16;
     a.scale_log2 = g.softmax_scale * kKdLog2e;
     a.inv_lh = 1.0f / ((float)n_layers * (float)g.q_heads);
     const long long tiles = (long long)g.batch * a.row_tiles;
-    kd_lse_kernel<<<dim3((unsigned)(tiles * n_layers * g.q_heads)), dim3(256), 0, stream>>>(a);
-    kd_target_kernel<<<dim3((unsigned)(tiles * a.key_tiles)), dim3(256), 0, stream>>>(a);
+    // heads per workgroup of the statistics pass (a divisor of the group)
+    const int hp = g.group == 8 ? 4 : g.group;
+    const dim3 lse_grid((unsigned)(tiles * n_layers * (g.group / hp) * g.kv_heads));
+    const bool paged = g.page_shift >= 0;
+#define KD_LSE(HP)                                                              \
+    (paged ? kd_lse_kernel<HP, true><<<lse_grid, dim3(256), 0, stream>>>(a)    \
+           : kd_lse_kernel<HP, false><<<lse_grid, dim3(256), 0, stream>>>(a))
+    switch (hp) {
+        case 1: KD_LSE(1); break;
+        case 2: KD_LSE(2); break;
+        case 4: KD_LSE(4); break;
+        case 5: KD_LSE(5); break;
+        default: return hipErrorInvalidValue;
+    }
+#undef KD_LSE
+    // the target pass: 16-row blocks x 256-key blocks
+    a.row_tiles = div_up(g.n_q, 16);
+    a.key_tiles = div_up(g.max_len, 4 * kKdTile);
+    const long long groups = ((long long)g.batch * a.row_tiles + 7) / 8;
+    const dim3 tgt_grid((unsigned)(groups * a.key_tiles * 8));
+    if (paged) kd_target_kernel<true><<<tgt_grid, dim3(256), 0, stream>>>(a);
+    else kd_target_kernel<false><<<tgt_grid, dim3(256), 0, stream>>>(a);
     return hipGetLastError();
 }
 

@@ -134,7 +134,8 @@ def _lens_uniform(seed: int, batch: int, lo: int, hi: int) -> List[int]:
 
 
 def workload(name: str) -> Workload:
-    """The five named workloads of the long-context decode/prefill study."""
+    """The five named workloads of the long-context decode/prefill study, and the
+    training-side distillation workload."""
     if name == "decode_b1_n4k":
         return Workload(name, 1, 1, [4096], 512, 4)
     if name == "decode_b8_n32k":
@@ -147,11 +148,17 @@ def workload(name: str) -> Workload:
     if name == "decode_b32_ragged_paged":
         return Workload(name, 5, 32, _lens_uniform(5006, 32, 16384, 65536), 2048, 24,
                         page_size=64)
+    if name == "kd_train_t32k":
+        # training side (Section 2.2): one 32,768-token sequence, every token a
+        # causal query row, the target averaged over L = 16 layers x 32 heads
+        return Workload(name, 6, 1, [32768], 2048, 16, n_q=32768, causal=True, q_pos0=[0])
     raise KeyError(name)
 
 
 WORKLOADS = ["decode_b1_n4k", "decode_b8_n32k", "decode_b4_n128k_planted",
              "prefill_t8k_n128k", "decode_b32_ragged_paged"]
+# The distillation workload (not a decode-step configuration).
+KD_WORKLOADS = ["kd_train_t32k"]
 
 
 def page_table_for(w: Workload, seed: int) -> np.ndarray:

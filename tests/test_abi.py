@@ -276,6 +276,9 @@ def test_kd_target_checks(lib):
     assert call(_shape(page_size=64, max_pages=16)) == -1                 # paged needs a table
     assert call(_shape(head_dim=64)) == -2
     assert call(_shape(q_heads=32, kv_heads=3)) == -1
+    neg = _shape()
+    neg.softmax_scale = -0.1
+    assert call(neg) == -1
 
 
 def test_kd_loss_checks(lib):
