@@ -138,24 +138,43 @@ __device__ __forceinline__ float kd_max(float x, float y) {
 }
 
 // Online softmax statistics of the lane's four rows over the lane's own four
-// keys of a tile: m is the largest unscaled logit so far (the scale is > 0, so
-// it keeps the order) and s the sum of 2^(sl * (z - m)); the 16 lanes of a row
-// are combined at the end.
+// keys of a tile, in log2 units: s is the sum of 2^(sl * z - base).  The base
+// follows the running maximum lazily: it moves only when a logit exceeds it by
+// more than 2^16 (then every row of the lane is rebased, on a branch the whole
+// wave takes), so that the steady state needs no rescaling exponential.  Terms
+// up to 2^16 keep the sums far from the fp32 range, and the relative precision
+// of the sum does not depend on the base.
+constexpr float kLazyMargin = 16.0f;
+
 template <bool FULL>
 __device__ __forceinline__ void kd_stats_update(const f32x4 (&c)[4], float sl, int j0, int col,
-                                                const int (&n)[4], float (&m)[4], float (&s)[4]) {
+                                                const int (&n)[4], float (&base)[4],
+                                                float (&s)[4]) {
+    float v[4][4], tm[4];
+    bool over = false;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        float v[4];
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct)
-            v[ct] = FULL || j0 + 16 * ct + col < n[r] ? c[ct][r] : -INFINITY;
-        const float mn = kd_max(kd_max(kd_max(v[0], v[1]), kd_max(v[2], v[3])), m[r]);
-        const float base = FULL ? mn * sl : (mn == -INFINITY ? 0.0f : mn * sl);  // no key yet
-        const float e = (kd_exp2(fmaf(v[0], sl, -base)) + kd_exp2(fmaf(v[1], sl, -base))) +
-                        (kd_exp2(fmaf(v[2], sl, -base)) + kd_exp2(fmaf(v[3], sl, -base)));
-        s[r] = fmaf(s[r], kd_exp2(fmaf(m[r], sl, -base)), e);
-        m[r] = mn;
+            v[r][ct] = FULL || j0 + 16 * ct + col < n[r] ? c[ct][r] : -INFINITY;
+        tm[r] = kd_max(kd_max(v[r][0], v[r][1]), kd_max(v[r][2], v[r][3])) * sl;
+        over |= tm[r] > base[r] + kLazyMargin;
+    }
+    if (__builtin_amdgcn_ballot_w64(over)) {  // rare: rebase every row of the wave
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float nb = kd_max(base[r], tm[r]);
+            if (nb != -INFINITY) {
+                s[r] *= kd_exp2(base[r] - nb);  // base = -inf: s is 0 anyway
+                base[r] = nb;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const float b = base[r] == -INFINITY ? 0.0f : base[r];  // no key of the lane yet
+        s[r] += (kd_exp2(fmaf(v[r][0], sl, -b)) + kd_exp2(fmaf(v[r][1], sl, -b))) +
+                (kd_exp2(fmaf(v[r][2], sl, -b)) + kd_exp2(fmaf(v[r][3], sl, -b)));
     }
 }
 
@@ -197,7 +216,7 @@ __global__ __launch_bounds__(256) void kd_lse_kernel(KdArgs a) {
 #pragma unroll
         for (int hh = 0; hh < HP; ++hh) kd_load_query(a, b, t0, l, h0 + hh, col, grp, q[hh]);
     }
-    float m[HP][4], s[HP][4];
+    float m[HP][4], s[HP][4];  // per head and row: base (log2 units) and sum
 #pragma unroll
     for (int hh = 0; hh < HP; ++hh)
 #pragma unroll
@@ -265,13 +284,12 @@ __global__ __launch_bounds__(256) void kd_lse_kernel(KdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const float mr = row16_max(m[hh][r]);
-            const float part =
-                m[hh][r] == -INFINITY ? 0.0f : s[hh][r] * exp2f((m[hh][r] - mr) * a.scale_log2);
+            const float part = m[hh][r] == -INFINITY ? 0.0f : s[hh][r] * exp2f(m[hh][r] - mr);
             const float sr = row16_sum(part);
             const int t = t0 + 4 * grp + r;
             if (col == 0 && t < a.n_q)
                 a.lse2[((size_t)l * a.q_heads + h0 + hh) * a.rows_pad + (size_t)b * a.n_q + t] =
-                    n[r] > 0 ? mr * a.scale_log2 + log2f(sr) : -INFINITY;
+                    n[r] > 0 ? mr + log2f(sr) : -INFINITY;
         }
 }
 
