@@ -29,8 +29,13 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "CLSA decode-step µs + HBM GB/s (index+top-k+L sparse attn), 128K ctx"
+KD_METRIC = ("CLSA distillation step ms (Eq. 5 multi-layer target + Eq. 6 KL loss and indexer "
+             "gradient), 32K-token sequence")
 HBM_PEAK_GBPS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak
+# exp2 on the vector units: 256 CUs x 4 SIMDs x 8 lanes per clock (v_exp_f32 at
+# half the FMA rate) x 2.4 GHz
+EXP_PEAK_TPS = 256 * 4 * 8 * 2.4e9 / 1e12
 PREFILL_MIN_ROWS = 32            # query rows per sequence from which the indexer uses MFMA
 
 
@@ -66,6 +71,8 @@ def algorithmic_bytes(w, x):
 
 
 KERNEL_SOURCES = {
+    "kd_lse_kernel": ["kd.hip", "device_common.h", "clsa_internal.h"],
+    "kd_target_kernel": ["kd.hip", "device_common.h", "clsa_internal.h"],
     "sparse_attn_kernel": ["sparse_attn.hip", "device_common.h", "clsa_internal.h"],
     "index_decode_kernel": ["index_decode.hip", "device_common.h", "clsa_internal.h"],
     "index_prefill_kernel": ["index_prefill.hip", "device_common.h", "clsa_internal.h"],
@@ -152,6 +159,194 @@ def cpu_baseline(w, x, budget_s: float):
             "sample": sample}
 
 
+def copy_reference(mib: int, dev) -> None:
+    """Three plain device-to-device copies of ``mib`` MiB: a known-size
+    reference for the hardware byte counters."""
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def kd_counts(w, x):
+    """Work of one distillation step: (row, key) pairs, the logit flops of one
+    pass over every (layer, query head, pair) (the statistics and the target
+    pass each make one), the exponentials of one such pass, and the index
+    scores and gradient products of the loss."""
+    n = valid_keys_per_row(w, x)
+    pairs = int(n.sum())
+    lh = w.n_layers * w.q_heads
+    d_idx = w.idx_heads * w.idx_dim
+    return dict(pairs=pairs, logit_flops=2 * w.head_dim * pairs * lh, exps=pairs * lh,
+                index_flops=2 * d_idx * pairs, grad_flops=2 * 2 * d_idx * pairs)
+
+
+def kd_cpu_baseline(w, x, budget_s: float):
+    """The oracle's Eq. 5 target and Eq. 6 loss on the last rows of the sequence
+    (the longest causal rows; same caches and layers), as many rows as fit the
+    budget, scaled to the whole sequence by the ratio of (row, key) pairs."""
+    import dataclasses
+    import oracle as orc
+
+    def run(rows):
+        t0 = w.n_q - rows
+        ws = dataclasses.replace(w, n_q=rows, q_pos0=[int(x["q_pos"][b, t0]) for b in range(w.batch)])
+        sh = orc.shape_of(ws)
+        ql = np.ascontiguousarray(x["q_layers"][:, :, t0:])
+        qi = np.ascontiguousarray(x["q_idx"][:, t0:])
+        qp = np.ascontiguousarray(x["q_pos"][:, t0:])
+        t = time.perf_counter()
+        abar = orc.kd_target(sh, ql, x["k_cache"], x["seq_lens"], qp, x["page_table"], fill=0.0)
+        orc.kd_loss(sh, abar, qi, x["k_idx"], x["seq_lens"], qp, x["page_table"])
+        el = time.perf_counter() - t
+        pairs = int(valid_keys_per_row(ws, {"q_pos": qp}).sum())
+        return el, pairs
+
+    el, pairs = run(1)
+    rows = 1
+    more = int(budget_s / max(el, 1e-6))
+    if more >= 2:
+        rows = min(more, w.n_q)
+        el, pairs = run(rows)
+    scale = kd_counts(w, x)["pairs"] / pairs
+    return {"value": round(el * scale * 1e3, 1), "unit": "ms/step", "cores": 1, "kind": "oracle",
+            "sample": (f"Eq. 5 target + Eq. 6 loss and gradient of the oracle over the last "
+                       f"{rows} of {w.n_q} rows of {w.name} (L={w.n_layers}, {pairs} row-key "
+                       f"pairs), single-threaded C, {el:.1f} s; scaled x{scale:.4g} by row-key "
+                       f"pairs to the whole sequence (extrapolated)")}
+
+
+def run_kd(args, w) -> int:
+    """The training-side distillation step on one sequence: clsa_kd_target (the
+    Eq. 5 target averaged over every layer and query head) and clsa_kd_loss (the
+    indexer scores, the Eq. 6 KL loss and the gradients of the index queries and
+    keys), timed over K steps after W warm-up steps, then once more with the
+    library's phase events for the per-kernel times."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    from paper_2606_06467_amd import inputs
+    log(f"[kd] generating {w.name} ...")
+    t = time.time()
+    x = inputs.make_inputs(w)
+    log(f"[kd] inputs ready in {time.time() - t:.1f} s")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bf = lambda a: B.bf16_from_bits(a, dev)
+    ql, kc = bf(x["q_layers"]), bf(x["k_cache"])
+    qi, ki = bf(x["q_idx"]), bf(x["k_idx"])
+    seq_lens = torch.from_numpy(x["seq_lens"]).to(dev)
+    q_pos = torch.from_numpy(x["q_pos"]).to(dev)
+    pt = None if x["page_table"] is None else torch.from_numpy(x["page_table"]).to(dev)
+    sh = B.make_shape(batch=w.batch, n_q=w.n_q, max_len=w.max_len, top_k=w.top_k,
+                      q_heads=w.q_heads, kv_heads=w.kv_heads, page_size=w.page_size,
+                      max_pages=w.max_pages, causal=w.causal)
+    L = w.n_layers
+    abar = torch.empty((w.batch, w.n_q, w.max_len), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    dq = torch.empty(x["q_idx"].shape, dtype=torch.float32, device=dev)
+    dk = torch.empty(x["k_idx"].shape, dtype=torch.float32, device=dev)
+    ws_t = B.workspace(sh, B.CLSA_OP_KD_TARGET, L, dev)
+    ws_l = B.workspace(sh, B.CLSA_OP_KD_LOSS, 0, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def target():
+        B.clsa_kd_target(sh, L, ql, kc, pt, seq_lens, q_pos, abar, ws_t, stream)
+
+    def kd_loss():
+        B.clsa_kd_loss(sh, abar, qi, ki, pt, seq_lens, q_pos, loss, dq, dk, ws_l, stream)
+
+    log(f"[kd] warmup {args.warmup} ...")
+    for _ in range(args.warmup):
+        target()
+        kd_loss()
+    torch.cuda.synchronize()
+    # ---- timed region: exactly K steps ----
+    log(f"[kd] timing {args.steps} steps ...")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        target()
+        kd_loss()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    # ---- per-kernel times from the library's phase events (a separate pass) ----
+    ev = B.HipEvents(8 * args.steps, timing_only=True)
+    for i in range(args.steps):
+        B.clsa_set_phase_events(ev.handles[8 * i: 8 * i + 4])
+        target()
+        B.clsa_set_phase_events(ev.handles[8 * i + 4: 8 * i + 8])
+        kd_loss()
+    B.clsa_set_phase_events(None)
+    torch.cuda.synchronize()
+    ph = np.array([[ev.elapsed_ms(8 * i, 8 * i + 1), ev.elapsed_ms(8 * i + 1, 8 * i + 2),
+                    ev.elapsed_ms(8 * i + 4, 8 * i + 5), ev.elapsed_ms(8 * i + 5, 8 * i + 6),
+                    ev.elapsed_ms(8 * i + 6, 8 * i + 7)] for i in range(args.steps)])
+    ev.close()
+    lse_ms, tgt_ms, scores_ms, rows_ms, grad_ms = (float(v) for v in ph.mean(axis=0))
+    # ---- the same step when the caller passes the dense forward pass's
+    # log-sum-exps (a training step has them): the statistics pass is skipped.
+    # Timed with stand-in values of the right size, ln(t + 1) + 1/2 (the target
+    # pass does the same work whatever they are). ----
+    lse_fwd = (torch.log(torch.arange(1, w.n_q + 1, device=dev, dtype=torch.float32)) + 0.5)
+    lse_fwd = lse_fwd.view(1, 1, w.n_q, 1).expand(L, w.batch, w.n_q, w.q_heads).contiguous()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        B.clsa_kd_target(sh, L, ql, kc, pt, seq_lens, q_pos, abar, ws_t, stream,
+                         lse_layers=lse_fwd)
+        kd_loss()
+    torch.cuda.synchronize()
+    ms_fwd_lse = (time.perf_counter() - t0) * 1e3 / args.steps
+    del lse_fwd
+    if args.copy_mib > 0:
+        copy_reference(args.copy_mib, dev)
+    cnt = kd_counts(w, x)
+    kern = {"kd_lse_kernel": lse_ms, "kd_target_kernel": tgt_ms}
+    main_k = max(kern, key=kern.get)
+    other_k = min(kern, key=kern.get)
+    exp_rate = cnt["exps"] / (lse_ms * 1e-3) / 1e12
+    res = {
+        "metric": KD_METRIC,
+        "value": round(ms_per_step, 3),
+        "unit": "ms/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "tokens": w.n_q, "context": max(w.lens),
+                   "causal": w.causal, "layers": L, "q_heads": w.q_heads,
+                   "kv_heads": w.kv_heads, "head_dim": w.head_dim,
+                   "index_dim": w.idx_heads * w.idx_dim, "row_key_pairs": cnt["pairs"]},
+        "tokens_per_s": round(w.batch * w.n_q / (ms_per_step * 1e-3), 1),
+        "ms_per_step_with_forward_lse": round(ms_fwd_lse, 3),
+        "phases_ms": {"statistics_kernel": round(lse_ms, 3), "target_kernel": round(tgt_ms, 3),
+                      "index_scores": round(scores_ms, 3), "loss_rows": round(rows_ms, 3),
+                      "gradients": round(grad_ms, 3)},
+        # the kernel with the largest share: both target-pass kernels make one
+        # logit product over every (layer, head, row, key)
+        "roofline": roofline_mfma(main_k, w, cnt["logit_flops"], kern[main_k]),
+        "roofline_other": roofline_mfma(other_k, w, cnt["logit_flops"], kern[other_k]),
+        "exp_rate": {"kernel": "kd_lse_kernel", "achieved": round(exp_rate, 2),
+                     "peak": round(EXP_PEAK_TPS, 2), "unit": "Texp/s",
+                     "frac": round(exp_rate / EXP_PEAK_TPS, 4),
+                     "note": "one exp2 per (layer, head, row, key) at least"},
+    }
+    if args.cpu_budget > 0:
+        log("[kd] CPU oracle baseline ...")
+        res["cpu_baseline"] = kd_cpu_baseline(w, x, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def run_schedules(args, w) -> int:
     """Per-layer decode cost of routing schedules on one workload.
 
@@ -233,6 +428,10 @@ def main() -> int:
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the timed steps, run plain device-to-device copies of this "
                          "many MiB (a known-size reference for hardware byte counters)")
+    ap.add_argument("--kd", action="store_true",
+                    help="instead of the decode step, time the training-side distillation step "
+                         "(Eq. 5 target, Eq. 6 loss and indexer gradient) on the 32K-token "
+                         "sequence workload (one JSON line)")
     ap.add_argument("--schedules", action="store_true",
                     help="instead of the step benchmark, compare routing schedules on the "
                          "workload: one shared index set, a fresh set every 4 layers, a fresh "
@@ -248,6 +447,9 @@ def main() -> int:
     from paper_2606_06467_amd import binding as B
     from paper_2606_06467_amd import inputs
 
+    if args.kd:
+        wl = args.workload if args.workload in inputs.KD_WORKLOADS else inputs.KD_WORKLOADS[0]
+        return run_kd(args, inputs.workload(wl))
     w = inputs.workload(args.workload)
     if args.schedules:
         return run_schedules(args, w)
@@ -336,13 +538,7 @@ def main() -> int:
     attn_first_ms = float(attn[:, 0].mean())
 
     if args.copy_mib > 0:
-        n = args.copy_mib << 20
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_reference(args.copy_mib, dev)
 
     ab = algorithmic_bytes(w, x)
     step_us = ms_per_step * 1e3

@@ -210,12 +210,18 @@ clsa_status clsa_project_append(const clsa_shape *shape, int32_t d_model, const 
  * h / (q_heads / kv_heads).  abar: fp32 [batch, n_q, max_len]; only the valid
  * positions of each row are written (a row without valid keys is left as it
  * is).  bf16 inputs, fp32 logits and softmax.  n_layers >= 1 and
- * softmax_scale > 0; v_cache is not read.  Workspace: CLSA_OP_KD_TARGET with
- * the same n_layers. */
+ * softmax_scale > 0; v_cache is not read.  lse_layers: fp32
+ * [n_layers, batch, n_q, q_heads], the natural-log log-sum-exp of each layer's
+ * scaled logits over the row's valid keys -- what clsa_dense_attn returns as
+ * lse for that layer, i.e. what the dense forward pass of the cross-decoder
+ * already has -- or NULL, and the call computes them itself (one more pass
+ * over every layer's logits).  Workspace: CLSA_OP_KD_TARGET with the same
+ * n_layers. */
 clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void *q_layers,
                            const void *k_cache, const int32_t *page_table,
-                           const int32_t *seq_lens, const int32_t *q_pos, float *abar, void *ws,
-                           size_t ws_bytes, void *stream);
+                           const int32_t *seq_lens, const int32_t *q_pos,
+                           const float *lse_layers, float *abar, void *ws, size_t ws_bytes,
+                           void *stream);
 
 /* Section 2.2, Eq. 6 and its gradient.  With P = abar[b,t,:] (the target,
  * held constant: the stop-gradient of Eq. 6) and Q = softmax(I_t) over the
@@ -246,7 +252,11 @@ const char *clsa_status_string(clsa_status status);
  * the indexer kernel, events[1] after it, events[2] after the top-k and
  * events[3] after the last layer; and for each layer l < m, events[4 + 2l]
  * right before the layer's sparse-attention kernel and events[5 + 2l] right
- * after it (before its split merge, if any).  The handles are kept, not
+ * after it (before its split merge, if any).  clsa_kd_target records
+ * events[0] before its statistics kernel, events[1] between it and the target
+ * kernel and events[2] after the target kernel; clsa_kd_loss records events[0]
+ * before the index scores, events[1] after them, events[2] after the loss
+ * kernels and events[3] after the gradient kernels.  The handles are kept, not
  * copied: they must stay valid while the hook is on.  n == 0 (events may be
  * NULL) switches the hook off.  Any other n, or a NULL handle, is
  * CLSA_ERR_INVALID_ARG and leaves the hook as it was. */

@@ -84,7 +84,7 @@ def lib() -> ctypes.CDLL:
                                            P, P, P, sz, P]),
         "clsa_dense_attn": (i32, [SP, P, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_project_append": (i32, [SP, i32, P, P, P, P, P, P, P, P, P]),
-        "clsa_kd_target": (i32, [SP, i32, P, P, P, P, P, P, P, sz, P]),
+        "clsa_kd_target": (i32, [SP, i32, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_kd_loss": (i32, [SP, P, P, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_status_string": (ctypes.c_char_p, [i32]),
         "clsa_set_phase_events": (i32, [ctypes.POINTER(P), i32]),
@@ -199,13 +199,13 @@ def clsa_project_append(shape, d_model, h, w, pos, page_table, q_idx, k_idx, k_c
 
 
 def clsa_kd_target(shape, n_layers, q_layers, k_cache, page_table, seq_lens, q_pos, abar,
-                   ws=None, stream=None):
+                   ws=None, stream=None, lse_layers=None):
     wsb = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().clsa_kd_target(ctypes.byref(shape), int(n_layers), _ptr(q_layers, "q_layers"),
                                 _ptr(k_cache, "k_cache"), _ptr(page_table, "page_table"),
                                 _ptr(seq_lens, "seq_lens"), _ptr(q_pos, "q_pos"),
-                                _ptr(abar, "abar"), _ptr(ws, "ws"), wsb, _stream(stream)),
-           "clsa_kd_target")
+                                _ptr(lse_layers, "lse_layers"), _ptr(abar, "abar"),
+                                _ptr(ws, "ws"), wsb, _stream(stream)), "clsa_kd_target")
 
 
 def clsa_kd_loss(shape, abar, q_idx, k_idx, page_table, seq_lens, q_pos, loss, dq_idx, dk_idx,

@@ -454,8 +454,9 @@ clsa_status clsa_dense_attn(const clsa_shape *shape, const void *q, const void *
 
 clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void *q_layers,
                            const void *k_cache, const int32_t *page_table,
-                           const int32_t *seq_lens, const int32_t *q_pos, float *abar, void *ws,
-                           size_t ws_bytes, void *stream) {
+                           const int32_t *seq_lens, const int32_t *q_pos,
+                           const float *lse_layers, float *abar, void *ws, size_t ws_bytes,
+                           void *stream) {
     Geometry g;
     CLSA_TRY(check_shape(shape, kAttn, &g));
     if (n_layers < 1 || !(shape->softmax_scale > 0.0f)) return CLSA_ERR_INVALID_ARG;
@@ -464,12 +465,19 @@ clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void
     CLSA_TRY(check_ptr(k_cache, 16));
     CLSA_TRY(check_ptr(seq_lens, 4));
     CLSA_TRY(check_ptr(abar, 4));
+    if (lse_layers) CLSA_TRY(check_ptr(lse_layers, 4));
     CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
     const size_t need = align_up(sizeof(float) * clsa::kd_target_ws_floats(g, n_layers));
     if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
-    return from_hip(clsa::launch_kd_target(g, n_layers, q_layers, k_cache, page_table, seq_lens,
-                                           q_pos, abar, static_cast<float *>(ws),
-                                           static_cast<hipStream_t>(stream)));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool hook = g_hook.on;
+    if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+    CLSA_TRY(from_hip(clsa::launch_kd_target(g, n_layers, q_layers, k_cache, page_table,
+                                             seq_lens, q_pos, lse_layers, abar,
+                                             static_cast<float *>(ws), st,
+                                             hook ? g_hook.ev[1] : nullptr)));
+    if (hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
+    return CLSA_OK;
 }
 
 clsa_status clsa_kd_loss(const clsa_shape *shape, const float *abar, const void *q_idx,
@@ -489,9 +497,15 @@ clsa_status clsa_kd_loss(const clsa_shape *shape, const float *abar, const void 
     CLSA_TRY(check_common(shape, page_table, q_pos, true, true));
     const size_t need = align_up(sizeof(float) * clsa::kd_loss_ws_floats(g));
     if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
-    return from_hip(clsa::launch_kd_loss(g, abar, q_idx, k_idx, page_table, seq_lens, q_pos, loss,
-                                         dq_idx, dk_idx, static_cast<float *>(ws),
-                                         static_cast<hipStream_t>(stream)));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool hook = g_hook.on;
+    if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+    CLSA_TRY(from_hip(clsa::launch_kd_loss(g, abar, q_idx, k_idx, page_table, seq_lens, q_pos,
+                                           loss, dq_idx, dk_idx, static_cast<float *>(ws), st,
+                                           hook ? g_hook.ev[1] : nullptr,
+                                           hook ? g_hook.ev[2] : nullptr)));
+    if (hook && hipEventRecord(g_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
+    return CLSA_OK;
 }
 
 const char *clsa_status_string(clsa_status status) {

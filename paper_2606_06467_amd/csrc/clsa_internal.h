@@ -98,19 +98,25 @@ hipError_t launch_project(const Geometry &g, int d_model, const void *h, const v
                           void *k_idx, void *k_cache, void *v_cache, hipStream_t stream);
 
 // ---- kd.hip ----
-// Eq. 5 target: lse2 workspace of kd_target_ws_floats floats.
+// Eq. 5 target: lse2 workspace of kd_target_ws_floats floats; lse_in, if not
+// null, holds the natural-log log-sum-exp of every (layer, row, query head)
+// and replaces the statistics pass; `between`, if not null, is recorded after
+// the statistics (or import) kernel, before the target kernel.
 bool kd_target_supported(const Geometry &g, int n_layers);
 size_t kd_target_ws_floats(const Geometry &g, int n_layers);
 hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layers,
                             const void *k_cache, const int32_t *page_table,
-                            const int32_t *seq_lens, const int32_t *q_pos, float *abar,
-                            float *lse2, hipStream_t stream);
-// Eq. 6 loss and its gradient: workspace of kd_loss_ws_floats floats.
+                            const int32_t *seq_lens, const int32_t *q_pos, const float *lse_in,
+                            float *abar, float *lse2, hipStream_t stream,
+                            hipEvent_t between = nullptr);
+// Eq. 6 loss and its gradient: workspace of kd_loss_ws_floats floats; the
+// events, if not null, are recorded after the index scores and after the loss.
 bool kd_loss_supported(const Geometry &g);
 size_t kd_loss_ws_floats(const Geometry &g);
 hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_idx,
                           const void *k_idx, const int32_t *page_table, const int32_t *seq_lens,
                           const int32_t *q_pos, float *loss, float *dq, float *dk, float *ws,
-                          hipStream_t stream);
+                          hipStream_t stream, hipEvent_t after_scores = nullptr,
+                          hipEvent_t after_loss = nullptr);
 
 }  // namespace clsa

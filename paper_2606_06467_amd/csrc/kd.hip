@@ -11,7 +11,9 @@
 //   * kd_lse_kernel: per (64-row tile, layer, up to 4 heads of one KV head), an
 //     online softmax over the row's keys gives each row's log-sum-exp (log2
 //     units, in the workspace); each lane keeps statistics over its own keys
-//     and the 16 lanes of a row are combined once at the end;
+//     and the 16 lanes of a row are combined once at the end.  When the caller
+//     already has these log-sum-exps (the dense forward pass of every layer
+//     makes them), kd_lse_import_kernel copies them in instead;
 //   * kd_target_kernel: per (16-row, 64-key) tile, every (layer, head) adds
 //     exp(logit - lse) into the tile held in registers; the key operands of a
 //     KV head are loaded once for all layers and heads of its group, the four
@@ -130,6 +132,19 @@ __device__ __forceinline__ int kd_groups_max(int v) {
 __device__ __forceinline__ int kd_groups_min(int v) {
     v = min(v, __shfl_xor(v, 16));
     return min(v, __shfl_xor(v, 32));
+}
+
+// The log-sum-exps of every (layer, row, query head) supplied by the caller
+// (natural log, [L, rows, Hq], as the dense attention returns them) into the
+// statistics layout [L, Hq, rows_pad] in log2 units.  grid-stride over L*rows*Hq.
+__global__ __launch_bounds__(256) void kd_lse_import_kernel(KdArgs a, const float *lse_in) {
+    const size_t total = (size_t)a.n_layers * a.rows * a.q_heads;
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (size_t)gridDim.x * 256) {
+        const int h = (int)(i % a.q_heads);
+        const size_t lr = i / a.q_heads;
+        const int r = (int)(lr % a.rows), l = (int)(lr / a.rows);
+        a.lse2[((size_t)l * a.q_heads + h) * a.rows_pad + r] = lse_in[i] * kKdLog2e;
+    }
 }
 
 // IEEE maximum (gfx950 v_maximum3_f32; no operand canonicalisation).
@@ -294,6 +309,7 @@ __global__ __launch_bounds__(256) void kd_lse_kernel(KdArgs a) {
 }
 
 constexpr int kTgtChunk = 4;              // (layer, head) combinations per LDS stage
+constexpr int kTgtWaveTiles = 1;          // 64-key tiles per wave in the target pass
 
 template <bool FULL>
 __device__ __forceinline__ void kd_accumulate(float sl, const bf16x8 (&qa)[4],
@@ -313,19 +329,22 @@ __device__ __forceinline__ void kd_accumulate(float sl, const bf16x8 (&qa)[4],
         }
 }
 
-// A workgroup covers 16 rows x 256 keys: each of its four waves holds the key
-// operands of one 64-key tile of the current KV head in registers, and the
-// query operands and log-sum-exps of the 16 rows are staged through LDS,
-// kTgtChunk (layer, head) combinations at a time, double-buffered: the next
-// stage's global reads are in flight while the current one is on the matrix
-// cores, one barrier per stage.  Workgroups are dealt to the 8 XCDs in turn;
-// the mapping gives every key block of a row block to the same XCD, one after
-// another, so the 2 MB of query operands of a row block (16 rows x every layer
-// and head) are read from that XCD's L2.
+// A workgroup covers 16 rows x (4 * kTgtWaveTiles * 64) keys: each of its four
+// waves holds the key operands of kTgtWaveTiles 64-key tiles of the current KV
+// head in registers, and the query operands and log-sum-exps of the 16 rows
+// are staged through LDS, kTgtChunk (layer, head) combinations at a time,
+// double-buffered: the next stage's global reads are in flight while the
+// current one is on the matrix cores, one barrier per stage.  Each staged query
+// tile serves every key tile of the workgroup, so the query traffic per output
+// falls with the keys a workgroup covers.  Workgroups are dealt to the 8 XCDs
+// in turn; the mapping gives every key block of a row block to the same XCD,
+// one after another, so the 2 MB of query operands of a row block (16 rows x
+// every layer and head) are read from that XCD's L2 as far as it holds them.
 // grid: ((row block group * key_blocks + key block) * 8 + xcd); row block
 // index over all sequences = row block group * 8 + xcd.
 template <bool PAGED>
 __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
+    constexpr int KT = kTgtWaveTiles;
     __shared__ __align__(16) uint16_t s_q[2][kTgtChunk][16][kStagePitch];
     __shared__ __align__(16) float s_l[2][kTgtChunk][16];
     const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
@@ -336,14 +355,14 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 15, grp = lane >> 4;
     const int t0 = rblk * 16;
-    const int j0 = (kblk * 4 + wave) * kKdTile;
+    const int jw = (kblk * 4 + wave) * KT * kKdTile;  // this wave's first key
     int n[4];
     kd_row_limits(a, b, t0, grp, n);
     const int nmax = kd_groups_max(max(max(n[0], n[1]), max(n[2], n[3])));
     const int nmin = kd_groups_min(min(min(n[0], n[1]), min(n[2], n[3])));
-    if (kblk * 4 * kKdTile >= nmax) return;  // no valid key in the block (uniform)
-    const bool active = j0 < nmax;            // this wave's tile has valid keys
-    const bool full = j0 + kKdTile <= nmin;
+    if (kblk * 4 * KT * kKdTile >= nmax) return;  // no valid key in the block (uniform)
+    const bool active = jw < nmax;                 // this wave's tiles hold valid keys
+    const bool full = jw + KT * kKdTile <= nmin;
     const int len = clamp_len(a.seq_lens[b], a.max_len);
 
     // staging: thread -> (row sr, 16-byte piece sd) of every combination of a stage
@@ -377,18 +396,24 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
         if (tid < kTgtChunk * 16) s_l[buf][tid >> 4][tid & 15] = lv;
     };
 
-    f32x4 acc[4];
+    f32x4 acc[KT][4];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) acc[kt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     u32x4 v[kTgtChunk];
     float lv = 0.0f;
     fetch(0, v, lv);
     stage(0, v, lv);
     __syncthreads();
-    bf16x8 kv[4][4];
+    bf16x8 kv[KT][4][4];
     for (int u = 0; u < stages; ++u) {
         const int k = u % nchunk;
-        if (k == 0 && active) kd_load_keys<PAGED>(a, b, j0, len, u / nchunk, col, grp, kv);
+        if (k == 0 && active) {
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+                kd_load_keys<PAGED>(a, b, jw + kt * kKdTile, len, u / nchunk, col, grp, kv[kt]);
+        }
         if (u + 1 < stages) fetch(u + 1, v, lv);
         if (active) {
             const int buf = u & 1;
@@ -400,8 +425,15 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
                 for (int kb = 0; kb < 4; ++kb)
                     qa[kb] = *reinterpret_cast<const bf16x8 *>(&s_q[buf][c][col][kb * 32 + grp * 8]);
                 const float4 lse = *reinterpret_cast<const float4 *>(&s_l[buf][c][4 * grp]);
-                if (full) kd_accumulate<true>(a.scale_log2, qa, lse, kv, j0, col, n, acc);
-                else kd_accumulate<false>(a.scale_log2, qa, lse, kv, j0, col, n, acc);
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt) {
+                    if (full)
+                        kd_accumulate<true>(a.scale_log2, qa, lse, kv[kt], jw + kt * kKdTile, col,
+                                            n, acc[kt]);
+                    else
+                        kd_accumulate<false>(a.scale_log2, qa, lse, kv[kt], jw + kt * kKdTile,
+                                             col, n, acc[kt]);
+                }
             }
         }
         if (u + 1 < stages) stage((u + 1) & 1, v, lv);
@@ -413,10 +445,12 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
         const int t = t0 + 4 * grp + r;
         float *row = a.abar + ((size_t)b * a.n_q + t) * a.max_len;
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
-            const int j = j0 + 16 * ct + col;
-            if (j < n[r]) row[j] = acc[ct][r] * a.inv_lh;
-        }
+        for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                const int j = jw + kt * kKdTile + 16 * ct + col;
+                if (j < n[r]) row[j] = acc[kt][ct][r] * a.inv_lh;
+            }
     }
 }
 
@@ -654,7 +688,7 @@ bool kd_target_supported(const Geometry &g, int n_layers) {
     const long long tiles = (long long)g.batch * div_up(g.n_q, kKdTile);
     const long long blocks = (long long)g.batch * div_up(g.n_q, 16);
     return n_layers >= 1 && grid_fits(tiles * n_layers * g.q_heads) &&
-           grid_fits((blocks + 7) / 8 * 8 * div_up(g.max_len, 4 * kKdTile)) &&
+           grid_fits((blocks + 7) / 8 * 8 * div_up(g.max_len, 4 * kTgtWaveTiles * kKdTile)) &&
            (long long)g.rows * g.q_heads * kKdDim * 2 < (1LL << 31);
 }
 
@@ -664,8 +698,8 @@ size_t kd_target_ws_floats(const Geometry &g, int n_layers) {
 
 hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layers,
                             const void *k_cache, const int32_t *page_table,
-                            const int32_t *seq_lens, const int32_t *q_pos, float *abar,
-                            float *lse2, hipStream_t stream) {
+                            const int32_t *seq_lens, const int32_t *q_pos, const float *lse_in,
+                            float *abar, float *lse2, hipStream_t stream, hipEvent_t between) {
     if (!kd_target_supported(g, n_layers)) return hipErrorInvalidValue;
     KdArgs a;
     a.q_layers = static_cast<const uint16_t *>(q_layers);
@@ -696,20 +730,28 @@ hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layer
     const int hp = g.group == 8 ? 4 : g.group;
     const dim3 lse_grid((unsigned)(tiles * n_layers * (g.group / hp) * g.kv_heads));
     const bool paged = g.page_shift >= 0;
+    if (lse_in) {  // the caller's log-sum-exps: no statistics pass
+        const size_t total = (size_t)n_layers * g.rows * g.q_heads;
+        const size_t blocks = (total + 255) / 256;
+        kd_lse_import_kernel<<<dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0,
+                               stream>>>(a, lse_in);
+    } else {
 #define KD_LSE(HP)                                                              \
     (paged ? kd_lse_kernel<HP, true><<<lse_grid, dim3(256), 0, stream>>>(a)    \
            : kd_lse_kernel<HP, false><<<lse_grid, dim3(256), 0, stream>>>(a))
-    switch (hp) {
-        case 1: KD_LSE(1); break;
-        case 2: KD_LSE(2); break;
-        case 4: KD_LSE(4); break;
-        case 5: KD_LSE(5); break;
-        default: return hipErrorInvalidValue;
-    }
+        switch (hp) {
+            case 1: KD_LSE(1); break;
+            case 2: KD_LSE(2); break;
+            case 4: KD_LSE(4); break;
+            case 5: KD_LSE(5); break;
+            default: return hipErrorInvalidValue;
+        }
 #undef KD_LSE
-    // the target pass: 16-row blocks x 256-key blocks
+    }
+    if (between && hipEventRecord(between, stream) != hipSuccess) return hipErrorUnknown;
+    // the target pass: 16-row blocks x (4 waves x kTgtWaveTiles x 64)-key blocks
     a.row_tiles = div_up(g.n_q, 16);
-    a.key_tiles = div_up(g.max_len, 4 * kKdTile);
+    a.key_tiles = div_up(g.max_len, 4 * kTgtWaveTiles * kKdTile);
     const long long groups = ((long long)g.batch * a.row_tiles + 7) / 8;
     const dim3 tgt_grid((unsigned)(groups * a.key_tiles * 8));
     if (paged) kd_target_kernel<true><<<tgt_grid, dim3(256), 0, stream>>>(a);
@@ -729,7 +771,7 @@ size_t kd_loss_ws_floats(const Geometry &g) {
 hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_idx,
                           const void *k_idx, const int32_t *page_table, const int32_t *seq_lens,
                           const int32_t *q_pos, float *loss, float *dq, float *dk, float *ws,
-                          hipStream_t stream) {
+                          hipStream_t stream, hipEvent_t after_scores, hipEvent_t after_loss) {
     if (!kd_loss_supported(g)) return hipErrorInvalidValue;
     KdLossArgs a;
     a.abar = abar;
@@ -759,8 +801,10 @@ hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_id
                        : launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
                                              nullptr, stream);
     if (e != hipSuccess) return e;
+    if (after_scores && hipEventRecord(after_scores, stream) != hipSuccess) return hipErrorUnknown;
     kd_rows_kernel<<<dim3(g.rows), dim3(256), 0, stream>>>(a);
     kd_loss_kernel<<<dim3(1), dim3(256), 0, stream>>>(a);
+    if (after_loss && hipEventRecord(after_loss, stream) != hipSuccess) return hipErrorUnknown;
     kd_dq_kernel<<<dim3((unsigned)(g.batch * a.row_tiles * 4)), dim3(256), 0, stream>>>(a);
     kd_dk_kernel<<<dim3((unsigned)(g.batch * a.key_tiles * 4)), dim3(256), 0, stream>>>(a);
     return hipGetLastError();

@@ -38,6 +38,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kMaxSplits = 128;  // splits per (row, KV head): the merge's largest shape
 
+// The fields every workgroup reads first come first: the kernel's prologue
+// then fetches them in one batch of scalar loads (a field pushed past them
+// costs one more dependent round trip per workgroup, measurable in a kernel
+// of a few microseconds).  The dense-only fields come last.
 struct AttnArgs {
     const uint16_t *q;
     const uint16_t *k;
@@ -45,15 +49,15 @@ struct AttnArgs {
     const int32_t *page_table;
     const int32_t *idx;      // sparse: [rows, top_k] selected positions
     const int32_t *n_sel;    // sparse: [rows] their count
-    const int32_t *seq_lens; // dense: [batch]
-    const int32_t *q_pos;    // dense, causal: [rows]
     uint16_t *out;
     float *lse;          // may be null
     float *part_o;       // [rows, Hq, splits, 128]
     float *part_ml;      // [rows, Hq, splits, 2]
     int n_q, max_len, page_shift, max_pages, top_k, kv_heads, q_heads, splits, chunks_per_split;
-    int causal;
     float scale_log2;    // softmax_scale * log2(e)
+    const int32_t *seq_lens; // dense: [batch]
+    const int32_t *q_pos;    // dense, causal: [rows]
+    int causal;
 };
 
 __host__ __device__ constexpr int pow2_at_least(int x) {

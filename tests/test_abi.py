@@ -257,8 +257,9 @@ def test_project_append_checks(lib):
 
 def test_kd_target_checks(lib):
     from paper_2606_06467_amd import binding as B
-    def call(sh, L=4, ws=A, wsb=1 << 30, ql=A, kc=A, sl=A, qp=None, ab=A):
-        return lib.clsa_kd_target(ctypes.byref(sh), L, ql, kc, None, sl, qp, ab, ws, wsb, None)
+    def call(sh, L=4, ws=A, wsb=1 << 30, ql=A, kc=A, sl=A, qp=None, ab=A, lse=None):
+        return lib.clsa_kd_target(ctypes.byref(sh), L, ql, kc, None, sl, qp, lse, ab, ws, wsb,
+                                  None)
     sh = _shape(n_q=128, max_len=4096)
     need = B.clsa_workspace_bytes(sh, B.CLSA_OP_KD_TARGET, 4)
     assert need >= 4 * 128 * 32 * 4                       # one lse per (layer, row, head)
@@ -272,6 +273,7 @@ def test_kd_target_checks(lib):
     assert call(sh, kc=None) == -1
     assert call(sh, sl=None) == -1
     assert call(sh, ab=None) == -1
+    assert call(sh, lse=MIS) == -1                         # optional lse: 4-byte aligned
     assert call(_shape(n_q=128, max_len=4096, causal=True)) == -1        # causal needs q_pos
     assert call(_shape(page_size=64, max_pages=16)) == -1                 # paged needs a table
     assert call(_shape(head_dim=64)) == -2

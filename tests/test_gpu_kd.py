@@ -51,8 +51,10 @@ def _cache_index(w, x, b, j):
     return (b, j)
 
 
-def _target_tol(w, x, n_layers, abar_ref, nvalid):
-    """Per-element bound on |abar_gpu - abar_oracle| (see the module docstring)."""
+def _target_tol(w, x, n_layers, abar_ref, nvalid, lse_sum_terms=0):
+    """Per-element bound on |abar_gpu - abar_oracle| (see the module docstring).
+    lse_sum_terms: when the log-sum-exps come from elsewhere, the length of the
+    fp32 sums that made them (their rounding adds to every probability)."""
     scale = w.softmax_scale
     ql = _f64(x["q_layers"]).reshape(n_layers, w.batch, w.n_q, w.q_heads, w.head_dim)
     qn = np.sqrt((ql ** 2).sum(-1)).max(axis=(0, 3))           # [B, T]
@@ -67,12 +69,28 @@ def _target_tol(w, x, n_layers, abar_ref, nvalid):
             dz = scale * _gamma(w.head_dim) * qn[b, t] * kn
             zb = scale * qn[b, t] * kn + np.log(n)
             rel = (2 * dz + U32 * (n / 16 + 64 + n_layers * w.q_heads)
-                   + 16 * U32 * (zb * LOG2E + 1))
+                   + 16 * U32 * (zb * LOG2E + 1) + U32 * lse_sum_terms * (n > 0))
             tol[b, t, :n] = abar_ref[b, t, :n] * rel
     return tol + 1e-30
 
 
-def _target_case(w, what):
+def _oracle_lse(w, x):
+    """The natural-log log-sum-exp of every (layer, row, query head) over the
+    row's valid keys, from the oracle's attention over every valid key."""
+    sh = orc.shape_of(w, top_k=w.max_len)
+    n = orc.valid_lens(sh, x["seq_lens"], x["q_pos"])
+    idx = np.full((w.batch, w.n_q, w.max_len), -1, np.int32)
+    for b in range(w.batch):
+        for t in range(w.n_q):
+            idx[b, t, :n[b, t]] = np.arange(n[b, t], dtype=np.int32)
+    return np.stack([orc.sparse_attn(sh, x["q_layers"][l], x["k_cache"], x["v_cache"], idx,
+                                     n.astype(np.int32), x["page_table"])[1]
+                     for l in range(w.n_layers)])
+
+
+def _target_case(w, what, lse_from=None):
+    """lse_from: None (the call computes the log-sum-exps), "oracle" (the
+    oracle's, rounded to fp32) or "dense" (clsa_dense_attn's, per layer)."""
     import torch
     from paper_2606_06467_amd import binding as B
     x = inputs.make_inputs(w)
@@ -81,10 +99,20 @@ def _target_case(w, what):
     sh = U.shape_of(w)
     abar = torch.full((w.batch, w.n_q, w.max_len), float("nan"), device="cuda")
     ws = B.workspace(sh, B.CLSA_OP_KD_TARGET, L)
+    lse = None
+    if lse_from == "oracle":
+        lse = torch.from_numpy(_oracle_lse(w, x).astype(np.float32)).cuda()
+    elif lse_from == "dense":
+        lse = torch.empty((L, w.batch, w.n_q, w.q_heads), device="cuda")
+        out = torch.empty(x["q_layers"].shape[1:], dtype=torch.bfloat16, device="cuda")
+        wsd = B.workspace(sh, B.CLSA_OP_DENSE)
+        for l in range(L):
+            B.clsa_dense_attn(sh, d["q_layers"][l], d["k_cache"], d["v_cache"], d["page_table"],
+                              d["seq_lens"], d["q_pos"], out, lse[l], wsd)
     U.log(f"  kd_target {what}: B={w.batch} T={w.n_q} max_len={w.max_len} L={L} "
-          f"Hq={w.q_heads} Hkv={w.kv_heads} paged={w.page_size}")
+          f"Hq={w.q_heads} Hkv={w.kv_heads} paged={w.page_size} lse={lse_from}")
     B.clsa_kd_target(sh, L, d["q_layers"], d["k_cache"], d["page_table"], d["seq_lens"],
-                     d["q_pos"], abar, ws)
+                     d["q_pos"], abar, ws, lse_layers=lse)
     torch.cuda.synchronize()
     got = abar.cpu().numpy().astype(np.float64)
     osh = orc.shape_of(w)
@@ -94,7 +122,8 @@ def _target_case(w, what):
     valid = np.arange(w.max_len)[None, None, :] < nvalid[:, :, None]
     assert np.all(np.isnan(got[~valid])), "positions outside the valid keys were written"
     assert np.isfinite(got[valid]).all()
-    tol = _target_tol(w, x, L, np.nan_to_num(ref), nvalid)
+    tol = _target_tol(w, x, L, np.nan_to_num(ref), nvalid,
+                      lse_sum_terms=w.max_len if lse_from == "dense" else 0)
     err = np.abs(got - ref)
     worst = float((err[valid] / tol[valid]).max(initial=0.0))
     U.log(f"    max|d|={float(err[valid].max(initial=0)):.3e}  worst err/bound={worst:.3f}")
@@ -104,6 +133,21 @@ def _target_case(w, what):
     sums[~valid] = 0.0
     np.testing.assert_allclose(sums.sum(-1)[rows], 1.0, rtol=0, atol=1e-5)
     return x, ref, nvalid
+
+
+@pytest.mark.parametrize("lse_from", ["oracle", "dense"])
+@pytest.mark.parametrize("case", ["causal_tiles", "paged_gqa5"])
+def test_target_with_supplied_lse(case, lse_from):
+    """The target pass alone, on log-sum-exps the caller supplies: the oracle's
+    (rounded to fp32), or the dense attention's of every layer (the forward
+    pass of a training step)."""
+    if case == "causal_tiles":
+        w = inputs.small_workload(batch=2, lens=(700, 450), n_q=150, causal=True,
+                                  q_pos0=(550, 300), n_layers=2, wid=82)
+    else:
+        w = inputs.small_workload(batch=3, lens=(500, 0, 260), n_q=2, page_size=64, q_heads=20,
+                                  kv_heads=4, n_layers=3, wid=83)
+    _target_case(w, case, lse_from=lse_from)
 
 
 @pytest.mark.parametrize("case", ["noncausal", "causal_tiles", "paged_gqa5", "single_key_row"])
@@ -221,3 +265,110 @@ def test_loss(case):
     else:                                 # no row has a key: loss 0, dq 0, dk untouched
         w = inputs.small_workload(batch=2, lens=(0, 0), n_q=3, n_layers=1, wid=88)
     _loss_case(w, case)
+
+
+def _rows_subproblem(w, x, rows):
+    """The oracle's view of query rows ``rows`` (sorted) of sequence 0 alone:
+    the same caches and layers, n_q = len(rows), q_pos of those rows."""
+    import dataclasses
+    ws = dataclasses.replace(w, batch=1, n_q=len(rows), q_pos0=None, lens=[w.lens[0]])
+    xs = dict(x)
+    xs["q_layers"] = np.ascontiguousarray(x["q_layers"][:, :1, rows])
+    xs["q_idx"] = np.ascontiguousarray(x["q_idx"][:1, rows])
+    xs["q_pos"] = np.ascontiguousarray(x["q_pos"][:1, rows])
+    xs["seq_lens"] = np.ascontiguousarray(x["seq_lens"][:1])
+    return ws, xs
+
+
+def test_full_size_training_sequence_sampled_rows():
+    """The 32,768-token distillation workload (16 layers x 32 heads, causal), in
+    the launch configuration the benchmark times: the target rows of a few
+    positions against the oracle on those rows alone; the index-query gradient
+    of the same rows against the oracle's loss over those rows (rescaled to the
+    whole sequence's row count); the index-key gradient of the last two keys,
+    which only the last two rows see, against the same oracle loss; and every
+    index-key gradient through the identity sum_t <dq_t, q_t> = sum_j <dk_j, k_j>
+    (both are sum dL/dI * I), as a coarse check of the rest."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    w = inputs.workload("kd_train_t32k")
+    U.log(f"  generating {w.name} ...")
+    x = inputs.make_inputs(w)
+    d = U.to_dev(x)
+    sh = U.shape_of(w)
+    T, L = w.n_q, w.n_layers
+    abar = torch.full((1, T, w.max_len), float("nan"), device="cuda")
+    loss = torch.full((1,), float("nan"), device="cuda")
+    dq = torch.full(x["q_idx"].shape, float("nan"), device="cuda")
+    dk = torch.full(x["k_idx"].shape, float("nan"), device="cuda")
+    U.log("  kd_target + kd_loss at full size ...")
+    B.clsa_kd_target(sh, L, d["q_layers"], d["k_cache"], None, d["seq_lens"], d["q_pos"], abar,
+                     B.workspace(sh, B.CLSA_OP_KD_TARGET, L))
+    B.clsa_kd_loss(sh, abar, d["q_idx"], d["k_idx"], None, d["seq_lens"], d["q_pos"], loss, dq,
+                   dk, B.workspace(sh, B.CLSA_OP_KD_LOSS))
+    torch.cuda.synchronize()
+    rows = [0, 4099, T - 2, T - 1]
+    keys = [T - 2, T - 1]  # seen only by rows T - 2 and T - 1
+    g_abar = abar[0, rows].cpu().numpy().astype(np.float64)
+    g_dq = dq.reshape(1, T, -1)[0, rows].cpu().numpy().astype(np.float64)
+    g_dk = dk.reshape(1, T, -1)[0, keys].cpu().numpy().astype(np.float64)
+    g_loss = float(loss.item())
+    dq_all = dq.reshape(T, -1).double()
+    dk_all = dk.reshape(T, -1).double()
+    qi_all = torch.from_numpy(_f64(x["q_idx"]).reshape(T, -1)).cuda()
+    ki_all = torch.from_numpy(_f64(x["k_idx"]).reshape(T, -1)).cuda()
+    lhs = float((dq_all * qi_all).sum())
+    rhs = float((dk_all * ki_all).sum())
+    assert torch.isfinite(dk_all).all() and torch.isfinite(dq_all).all()
+    del abar, dq, dk, d
+    torch.cuda.empty_cache()
+
+    U.log(f"  oracle on rows {rows} ...")
+    ws, xs = _rows_subproblem(w, x, rows)
+    osh = orc.shape_of(ws)
+    ref = orc.kd_target(osh, xs["q_layers"], xs["k_cache"], xs["seq_lens"], xs["q_pos"])
+    nval = orc.valid_lens(osh, xs["seq_lens"], xs["q_pos"])
+    tol = _target_tol(ws, xs, L, np.nan_to_num(ref), nval)
+    for i, t in enumerate(rows):
+        n = int(nval[0, i])
+        assert np.all(np.isnan(g_abar[i, n:])), t
+        err = np.abs(g_abar[i, :n] - ref[0, i, :n])
+        U.log(f"    target row {t}: {n} keys, worst err/bound "
+              f"{float((err / tol[0, i, :n]).max()):.3f}")
+        assert np.all(err <= tol[0, i, :n]), t
+    # dq of the sampled rows: the oracle's loss over these rows normalises by
+    # their count; the GPU's by every row of the sequence (each has a key).
+    r_loss, r_dq, r_dk = orc.kd_loss(osh, ref, xs["q_idx"], xs["k_idx"], xs["seq_lens"],
+                                     xs["q_pos"])
+    scale = len(rows) / T
+    r_dq = r_dq.reshape(len(rows), -1) * scale
+    e_loss, e_dq, e_dk = _loss_bounds(ws, xs, ref, nval)
+    qa_rows = np.abs(_f64(xs["q_idx"]).reshape(len(rows), -1))
+    for i, j in enumerate(keys):
+        # the GPU's own target of the rows that see key j differs by at most tol
+        e = (e_dk[0, j] * scale + sum(tol[0, r, j] * qa_rows[r] for r in range(len(rows))
+                                      if j < nval[0, r]) / T
+             + 4 * U32 * np.abs(r_dk[0, j].reshape(-1) * scale) + 1e-30)
+        dd = np.abs(g_dk[i] - r_dk[0, j].reshape(-1) * scale)
+        U.log(f"    dk key {j}: max|d| {float(dd.max()):.2e}, worst err/bound "
+              f"{float((dd / e).max()):.3f}")
+        assert np.all(dd <= e), j
+    kb = np.abs(_f64(x["k_idx"]).reshape(T, -1))
+    for i, t in enumerate(rows):
+        n = int(nval[0, i])
+        # the GPU's own target differs from the oracle's by at most tol
+        e = e_dq[0, i] * scale + (tol[0, i, :n] @ kb[:n]) / T + 4 * U32 * np.abs(r_dq[i]) + 1e-30
+        dd = np.abs(g_dq[i] - r_dq[i])
+        U.log(f"    dq row {t}: max|d| {float(dd.max()):.2e}, worst err/bound "
+              f"{float((dd / e).max()):.3f}")
+        assert np.all(dd <= e), t
+    # identity between the two gradients: both accumulate the same fp32 dL/dI,
+    # so they differ by their own fp32 accumulation errors only; |dL/dI_t|
+    # sums to at most 2 per row.
+    qa = np.abs(_f64(x["q_idx"]).reshape(T, -1))
+    kmax = kb.max(axis=0)
+    bound = 2 * _gamma(T + 1) * float((2 * (qa @ kmax)).sum()) / T + 1e-12
+    U.log(f"    sum<dq,q>={lhs:.6e} sum<dk,k>={rhs:.6e} |d|={abs(lhs - rhs):.2e} "
+          f"bound={bound:.2e}; loss={g_loss:.6f}")
+    assert abs(lhs - rhs) <= bound
+    assert np.isfinite(g_loss) and g_loss >= -1e-6
