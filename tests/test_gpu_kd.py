@@ -135,6 +135,15 @@ def _target_case(w, what, lse_from=None):
     return x, ref, nvalid
 
 
+@pytest.mark.parametrize("qh,kvh", [(8, 8), (16, 8), (64, 8)])
+def test_target_gqa_groups(qh, kvh):
+    """Groups of 1, 2 and 8 query heads per KV head (the statistics pass takes
+    1, 2 and 2 x 4 heads per workgroup), causal rows across a tile boundary."""
+    w = inputs.small_workload(batch=1, lens=(333,), n_q=70, causal=True, q_pos0=(263,),
+                              q_heads=qh, kv_heads=kvh, n_layers=1, wid=89)
+    _target_case(w, f"Hq={qh} Hkv={kvh}")
+
+
 @pytest.mark.parametrize("lse_from", ["oracle", "dense"])
 @pytest.mark.parametrize("case", ["causal_tiles", "paged_gqa5"])
 def test_target_with_supplied_lse(case, lse_from):
