@@ -28,8 +28,8 @@
 //   * kd_loss_kernel: n_rows and the mean of the row terms (summed in double
 //     in a fixed order);
 //   * kd_dq_kernel / kd_dk_kernel: dq = dL/dI K_idx and dk = dL/dI^T Q_idx,
-//     fp32 products tiled through LDS (64 x 64 outputs per workgroup, 4 x 4
-//     per thread, 32-deep steps).
+//     fp32 matrix-core products tiled through LDS (64 x 64 outputs per
+//     workgroup, 32-deep steps).
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -459,6 +459,7 @@ struct KdLossArgs {
     float *dI;                 // [rows, max_len]: index scores in, Q - P out
     float *row_kl;             // [rows]
     float *stats;              // [0] = 1 / n_rows (0 when none), [1] = n_rows
+    int32_t *step_max;         // [B, ceil(n_q / 32)]: most keys of any row of each 32-row step
     float *loss;
     const uint16_t *q_idx;     // [rows, 256]
     const uint16_t *k_idx;     // index-key cache
@@ -544,8 +545,11 @@ __global__ __launch_bounds__(256) void kd_loss_kernel(KdLossArgs a) {
     }
 }
 
-constexpr int kGemmDepth = 32;      // contraction steps per LDS stage
-constexpr int kGemmPitch = 64 + 4;  // LDS row pitch (floats)
+constexpr int kGemmDepth = 32;  // contraction steps per LDS stage
+constexpr int kRowPitch = 36;   // [row][key] staging: the MFMA reads (16 rows x 4 keys) and the
+                                // row-contiguous stores both fall on distinct banks
+constexpr int kColPitch = 80;   // [k][column] staging: the MFMA reads (4 k x 16 columns) fall
+                                // on distinct banks
 
 // 8 bf16 -> 8 floats stored at dst (16-byte aligned).
 __device__ __forceinline__ void kd_store8(float *dst, u32x4 v) {
@@ -555,33 +559,38 @@ __device__ __forceinline__ void kd_store8(float *dst, u32x4 v) {
     *reinterpret_cast<float4 *>(dst + 4) = hi;
 }
 
-__device__ __forceinline__ void kd_fma_tile(const float (*As)[kGemmPitch],
-                                            const float (*Bs)[kGemmPitch], int ty, int tx,
-                                            float (&acc)[4][4]) {
-#pragma unroll 8
-    for (int k = 0; k < kGemmDepth; ++k) {
-        const float4 av = *reinterpret_cast<const float4 *>(&As[k][ty * 4]);
-        const float4 bv = *reinterpret_cast<const float4 *>(&Bs[k][tx * 4]);
-        const float ar[4] = {av.x, av.y, av.z, av.w};
-        const float br[4] = {bv.x, bv.y, bv.z, bv.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], br[j], acc[i][j]);
-    }
+// The gradient products run on v_mfma_f32_16x16x4_f32 (fp32 operands, so the
+// bf16 keys and queries enter exactly and dL/dI keeps its fp32 bits): lane l
+// supplies A[l & 15][l >> 4] and B[l >> 4][l & 15] and receives C rows
+// 4 * (l >> 4) + r of column l & 15.  A workgroup computes 64 x 64 outputs,
+// each wave 16 rows x 64 columns (four column tiles), 32 contraction steps per
+// LDS stage.
+
+// step_max[b, s] = the most valid keys of any row of rows 32 s .. 32 s + 31 of
+// sequence b.  One thread per (sequence, step).
+__global__ __launch_bounds__(256) void kd_step_max_kernel(KdLossArgs a, int total) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= total) return;
+    const int nsteps = div_up(a.n_q, kGemmDepth);
+    const int b = i / nsteps, r0 = (i % nsteps) * kGemmDepth;
+    int m = 0;
+    for (int k = 0; k < kGemmDepth && r0 + k < a.n_q; ++k)
+        m = max(m, valid_keys(a.seq_lens, a.q_pos, a.causal, b, b * a.n_q + r0 + k, a.max_len));
+    a.step_max[i] = m;
 }
 
 // dq[b,t,c] = (1 / n_rows) sum_{j < n(b,t)} dI[b,t,j] k_idx[b,j,c].
 // grid: ((b * row_tiles + tile) * 4 + column tile), 64 rows x 64 columns each.
 __global__ __launch_bounds__(256) void kd_dq_kernel(KdLossArgs a) {
-    __shared__ __align__(16) float As[kGemmDepth][kGemmPitch];  // [key][row]
-    __shared__ __align__(16) float Bs[kGemmDepth][kGemmPitch];  // [key][column]
+    __shared__ __align__(16) float As[64][kRowPitch];           // [row][key]
+    __shared__ __align__(16) float Bs[kGemmDepth][kColPitch];   // [key][column]
     __shared__ int s_n[64];
     int x = blockIdx.x;
     const int c0 = (x & 3) * 64;
     x >>= 2;
     const int tile = x % a.row_tiles, b = x / a.row_tiles;
-    const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int col = lane & 15, kq = lane >> 4;
     const int t0 = tile * 64;
     if (tid < 64) {
         const int t = t0 + tid;
@@ -591,92 +600,148 @@ __global__ __launch_bounds__(256) void kd_dq_kernel(KdLossArgs a) {
     __syncthreads();
     int nmax = 0;
     for (int i = 0; i < 64; ++i) nmax = max(nmax, s_n[i]);
-    float acc[4][4] = {};
+    f32x4 acc[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int ak = tid & 31, ai = tid >> 5;        // A loads: key ak, rows ai + 8 * step
     const int bk = tid >> 3, bc = (tid & 7) * 8;   // B loads: key bk, columns bc .. bc + 7
-    for (int j0 = 0; j0 < nmax; j0 += kGemmDepth) {
+    int nrow[8];
+#pragma unroll
+    for (int st = 0; st < 8; ++st) nrow[st] = s_n[ai + 8 * st];
+    // one stage's operands, read into registers a stage ahead of their use
+    float av_n[8];
+    u32x4 kv_n;
+    auto fetch = [&](int j0) {
         const int j = j0 + ak;
 #pragma unroll
-        for (int st = 0; st < 8; ++st) {
-            const int i = ai + 8 * st;
-            As[ak][i] = j < s_n[i] ? a.dI[((size_t)b * a.n_q + t0 + i) * a.max_len + j] : 0.0f;
-        }
+        for (int st = 0; st < 8; ++st)
+            av_n[st] = j < nrow[st]
+                           ? a.dI[((size_t)b * a.n_q + t0 + ai + 8 * st) * a.max_len + j]
+                           : 0.0f;
         const int jb = j0 + bk;
-        u32x4 kv = u32x4{0u, 0u, 0u, 0u};
+        kv_n = u32x4{0u, 0u, 0u, 0u};
         if (jb < nmax)
-            kv = *reinterpret_cast<const u32x4 *>(
+            kv_n = *reinterpret_cast<const u32x4 *>(
                 a.k_idx + token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b, jb,
                                        kIdxDim) +
                 c0 + bc);
-        kd_store8(&Bs[bk][bc], kv);
+    };
+    if (nmax > 0) fetch(0);
+    for (int j0 = 0; j0 < nmax; j0 += kGemmDepth) {
+#pragma unroll
+        for (int st = 0; st < 8; ++st) As[ai + 8 * st][ak] = av_n[st];
+        kd_store8(&Bs[bk][bc], kv_n);
         __syncthreads();
-        kd_fma_tile(As, Bs, ty, tx, acc);
+        if (j0 + kGemmDepth < nmax) fetch(j0 + kGemmDepth);
+#pragma unroll
+        for (int kk = 0; kk < kGemmDepth; kk += 4) {
+            const float av = As[wave * 16 + col][kk + kq];
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct)
+                acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Bs[kk + kq][ct * 16 + col],
+                                                               acc[ct], 0, 0, 0);
+        }
         __syncthreads();
     }
     const float inv_n = a.stats[0];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int t = t0 + ty * 4 + i;
-        if (t < a.n_q)
-            *reinterpret_cast<float4 *>(a.dq + ((size_t)b * a.n_q + t) * kIdxDim + c0 + tx * 4) =
-                make_float4(acc[i][0] * inv_n, acc[i][1] * inv_n, acc[i][2] * inv_n,
-                            acc[i][3] * inv_n);
+    for (int r = 0; r < 4; ++r) {
+        const int t = t0 + wave * 16 + 4 * kq + r;
+        if (t < a.n_q) {
+            float *dst = a.dq + ((size_t)b * a.n_q + t) * kIdxDim + c0 + col;
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) dst[ct * 16] = acc[ct][r] * inv_n;
+        }
     }
 }
 
 // dk[b,j,c] = (1 / n_rows) sum_{t : j < n(b,t)} dI[b,t,j] q_idx[b,t,c], for j < seq_lens[b].
 // grid: ((b * key_tiles + tile) * 4 + column tile), 64 keys x 64 columns each.
 __global__ __launch_bounds__(256) void kd_dk_kernel(KdLossArgs a) {
-    __shared__ __align__(16) float As[kGemmDepth][kGemmPitch];  // [row][key]
-    __shared__ __align__(16) float Bs[kGemmDepth][kGemmPitch];  // [row][column]
-    __shared__ int s_n[kGemmDepth];
+    __shared__ __align__(16) float As[kGemmDepth][kColPitch];  // [row][key]
+    __shared__ __align__(16) float Bs[kGemmDepth][kColPitch];  // [row][column]
     int x = blockIdx.x;
     const int c0 = (x & 3) * 64;
     x >>= 2;
     const int tile = x % a.key_tiles, b = x / a.key_tiles;
-    const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int col = lane & 15, kq = lane >> 4;
     const int j0 = tile * 64;
     const int len = clamp_len(a.seq_lens[b], a.max_len);
     if (j0 >= len) return;  // uniform: no token of this tile is written
-    float acc[4][4] = {};
+    f32x4 acc[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int ai = tid & 63, ak = tid >> 6;        // A loads: key ai, rows ak + 4 * step
     const int bk = tid >> 3, bc = (tid & 7) * 8;   // B loads: row bk, columns bc .. bc + 7
-    for (int r0 = 0; r0 < a.n_q; r0 += kGemmDepth) {
-        if (tid < kGemmDepth) {
-            const int t = r0 + tid;
-            s_n[tid] = t < a.n_q
-                           ? valid_keys(a.seq_lens, a.q_pos, a.causal, b, b * a.n_q + t, a.max_len)
-                           : 0;
-        }
-        // Skip the step when no row of it sees a key of the tile.
-        if (!__syncthreads_or(tid < kGemmDepth && s_n[tid] > j0)) continue;
+    // one step's operands (32 rows from r0), read into registers a step ahead
+    float av_n[8];
+    u32x4 qv_n;
+    auto fetch = [&](int r0) {
 #pragma unroll
         for (int st = 0; st < 8; ++st) {
-            const int k = ak + 4 * st;
-            As[k][ai] = j0 + ai < s_n[k]
-                            ? a.dI[((size_t)b * a.n_q + r0 + k) * a.max_len + j0 + ai]
-                            : 0.0f;
+            const int t = r0 + ak + 4 * st;
+            const int nk = t < a.n_q ? valid_keys(a.seq_lens, a.q_pos, a.causal, b, b * a.n_q + t,
+                                                  a.max_len)
+                                     : 0;
+            av_n[st] = j0 + ai < nk ? a.dI[((size_t)b * a.n_q + t) * a.max_len + j0 + ai] : 0.0f;
         }
         const int t = r0 + bk;
-        u32x4 qv = u32x4{0u, 0u, 0u, 0u};
+        qv_n = u32x4{0u, 0u, 0u, 0u};
         if (t < a.n_q)
-            qv = *reinterpret_cast<const u32x4 *>(a.q_idx + ((size_t)b * a.n_q + t) * kIdxDim + c0 +
-                                                  bc);
-        kd_store8(&Bs[bk][bc], qv);
+            qv_n = *reinterpret_cast<const u32x4 *>(a.q_idx + ((size_t)b * a.n_q + t) * kIdxDim +
+                                                    c0 + bc);
+    };
+    // Only the steps with a row that sees one of the tile's keys contribute
+    // (in a causal sequence, those from the tile's own position on): 256 steps
+    // at a time, their per-step key maxima give an ordered list of the useful
+    // ones (wave ballots, so the summation order is fixed), and the loop runs
+    // over that list with the next step's operands in flight.
+    __shared__ int s_list[256];
+    __shared__ int s_wcnt[4];
+    const int nsteps = div_up(a.n_q, kGemmDepth);
+    const int32_t *smax = a.step_max + (size_t)b * nsteps;
+    for (int s0 = 0; s0 < nsteps; s0 += 256) {
+        const int st_i = s0 + tid;
+        const bool useful = st_i < nsteps && smax[st_i] > j0;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(useful);
+        const int before = __builtin_popcountll(m & ((1ull << lane) - 1ull));
+        if (lane == 0) s_wcnt[wave] = __builtin_popcountll(m);
         __syncthreads();
-        kd_fma_tile(As, Bs, ty, tx, acc);
+        int off = 0;
+        for (int w = 0; w < wave; ++w) off += s_wcnt[w];
+        const int cnt = s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
+        if (useful) s_list[off + before] = st_i;
         __syncthreads();
+        if (cnt > 0) fetch(s_list[0] * kGemmDepth);
+        for (int i = 0; i < cnt; ++i) {
+#pragma unroll
+            for (int st = 0; st < 8; ++st) As[ak + 4 * st][ai] = av_n[st];
+            kd_store8(&Bs[bk][bc], qv_n);
+            __syncthreads();
+            if (i + 1 < cnt) fetch(s_list[i + 1] * kGemmDepth);
+#pragma unroll
+            for (int kk = 0; kk < kGemmDepth; kk += 4) {
+                const float av = As[kk + kq][wave * 16 + col];
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct)
+                    acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Bs[kk + kq][ct * 16 + col],
+                                                                   acc[ct], 0, 0, 0);
+            }
+            __syncthreads();  // As / Bs and s_list are rewritten next
+        }
     }
     const float inv_n = a.stats[0];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int j = j0 + ty * 4 + i;
-        if (j < len)
-            *reinterpret_cast<float4 *>(
-                a.dk + token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b, j,
-                                    kIdxDim) +
-                c0 + tx * 4) = make_float4(acc[i][0] * inv_n, acc[i][1] * inv_n,
-                                           acc[i][2] * inv_n, acc[i][3] * inv_n);
+    for (int r = 0; r < 4; ++r) {
+        const int j = j0 + wave * 16 + 4 * kq + r;
+        if (j < len) {
+            float *dst = a.dk + token_offset(a.page_table, a.page_shift, a.max_pages, a.max_len, b,
+                                             j, kIdxDim) +
+                         c0 + col;
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) dst[ct * 16] = acc[ct][r] * inv_n;
+        }
     }
 }
 
@@ -765,7 +830,8 @@ bool kd_loss_supported(const Geometry &g) {
 }
 
 size_t kd_loss_ws_floats(const Geometry &g) {
-    return (size_t)g.rows * g.max_len + g.rows + 2;
+    // scores / dL/dI, row terms, 2 statistics, per-step key maxima (int32)
+    return (size_t)g.rows * g.max_len + g.rows + 2 + (size_t)g.batch * div_up(g.n_q, 32);
 }
 
 hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_idx,
@@ -778,6 +844,7 @@ hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_id
     a.dI = ws;
     a.row_kl = ws + (size_t)g.rows * g.max_len;
     a.stats = a.row_kl + g.rows;
+    a.step_max = reinterpret_cast<int32_t *>(a.stats + 2);
     a.loss = loss;
     a.q_idx = static_cast<const uint16_t *>(q_idx);
     a.k_idx = static_cast<const uint16_t *>(k_idx);
@@ -805,6 +872,8 @@ hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_id
     kd_rows_kernel<<<dim3(g.rows), dim3(256), 0, stream>>>(a);
     kd_loss_kernel<<<dim3(1), dim3(256), 0, stream>>>(a);
     if (after_loss && hipEventRecord(after_loss, stream) != hipSuccess) return hipErrorUnknown;
+    const int steps_total = g.batch * div_up(g.n_q, kGemmDepth);
+    kd_step_max_kernel<<<dim3(div_up(steps_total, 256)), dim3(256), 0, stream>>>(a, steps_total);
     kd_dq_kernel<<<dim3((unsigned)(g.batch * a.row_tiles * 4)), dim3(256), 0, stream>>>(a);
     kd_dk_kernel<<<dim3((unsigned)(g.batch * a.key_tiles * 4)), dim3(256), 0, stream>>>(a);
     return hipGetLastError();
