@@ -174,7 +174,10 @@ def test_workspace_sizes(lib):
     # many rows: one workgroup per row, everything in LDS
     many = _shape(batch=1, n_q=4096, max_len=131072, top_k=2048, causal=True)
     assert B.clsa_workspace_bytes(many, B.CLSA_OP_TOPK) == 0
-    assert B.clsa_workspace_bytes(many, B.CLSA_OP_ATTN) == 0       # one split per row
+    # many rows: every index list in 8 stretches, fp32 (o, m, l) partials per stretch
+    assert B.clsa_workspace_bytes(many, B.CLSA_OP_ATTN) >= 4096 * 32 * 8 * 130 * 4
+    few = _shape(batch=1, n_q=64, max_len=131072, top_k=2048, causal=True)
+    assert B.clsa_workspace_bytes(few, B.CLSA_OP_ATTN) > 0           # split over the list
     dec = B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 16)
     assert dec >= 4 * 131072 * 4 + 4 * 2048 * 4
     assert dec == B.clsa_workspace_bytes(sh, B.CLSA_OP_DECODE, 1)   # layers reuse buffers

@@ -75,6 +75,14 @@ def test_single_split_many_rows():
     _case(w, 4, what="300 rows, one split each")
 
 
+def test_many_rows_split_by_key_range():
+    """Over 4096 (row, KV head) units: each index list is cut into stretches that
+    are issued stretch by stretch over all rows, then merged."""
+    w = inputs.small_workload(batch=1, lens=(4000,), n_q=520, causal=True, q_pos0=(3480,),
+                              top_k=512, q_heads=8, kv_heads=8, n_layers=1, wid=87)
+    _case(w, 5, what="520 rows x 8 KV heads, split by key range")
+
+
 def test_paged():
     w = inputs.small_workload(batch=3, lens=(3000, 64, 5000), top_k=512, page_size=64, n_layers=1,
                               wid=85)

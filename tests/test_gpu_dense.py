@@ -59,6 +59,13 @@ def test_causal_rows():
     _case(w, "dense causal rows")
 
 
+def test_many_rows_split_by_key_range():
+    """Dense attention over 4096+ (row, KV head) units, split by key range."""
+    w = inputs.small_workload(batch=1, lens=(1500,), n_q=520, causal=True, q_pos0=(980,),
+                              q_heads=8, kv_heads=8, n_layers=1, wid=75)
+    _case(w, "dense 520 causal rows x 8 KV heads")
+
+
 def test_many_splits_one_row():
     """One long row: the most splits the merge supports."""
     w = inputs.small_workload(batch=1, lens=(20000,), n_layers=1, wid=74)
