@@ -342,7 +342,7 @@ __device__ __forceinline__ void kd_accumulate(float sl, const bf16x8 (&qa)[4],
 // every layer and head) are read from that XCD's L2 as far as it holds them.
 // grid: ((row block group * key_blocks + key block) * 8 + xcd); row block
 // index over all sequences = row block group * 8 + xcd.
-template <bool PAGED>
+template <int G, bool PAGED>  // G: query heads per KV head
 __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
     constexpr int KT = kTgtWaveTiles;
     __shared__ __align__(16) uint16_t s_q[2][kTgtChunk][16][kStagePitch];
@@ -371,20 +371,21 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
     const uint16_t *qsrc = a.q_layers +
                            ((size_t)b * a.n_q + min(t0 + sr, a.n_q - 1)) * a.q_heads * kKdDim +
                            sd * 8;
-    const int combos = a.n_layers * a.group;
+    // Combination ci = l * G + hh of KV head g is (layer l, query head g * G + hh);
+    // a stage holds kTgtChunk consecutive combinations of one KV head.  G is a
+    // compile-time constant, so the index arithmetic has no division.
+    const int combos = a.n_layers * G;
     const int nchunk = div_up(combos, kTgtChunk);
-    const int stages = a.kv_heads * nchunk;
-    auto fetch = [&](int u, u32x4 (&v)[kTgtChunk], float &lv) {
-        const int g = u / nchunk, c0 = (u % nchunk) * kTgtChunk;
+    auto fetch = [&](int g, int c0, u32x4 (&v)[kTgtChunk], float &lv) {
 #pragma unroll
         for (int c = 0; c < kTgtChunk; ++c) {
             const int ci = min(c0 + c, combos - 1);
-            const int l = ci / a.group, h = g * a.group + ci % a.group;
+            const int l = ci / G, h = g * G + ci % G;
             v[c] = *reinterpret_cast<const u32x4 *>(qsrc + l * layer_q + (size_t)h * kKdDim);
         }
         if (tid < kTgtChunk * 16) {
             const int ci = min(c0 + (tid >> 4), combos - 1);
-            const int l = ci / a.group, h = g * a.group + ci % a.group;
+            const int l = ci / G, h = g * G + ci % G;
             lv = a.lse2[((size_t)l * a.q_heads + h) * a.rows_pad + (size_t)b * a.n_q + t0 +
                         (tid & 15)];
         }
@@ -403,20 +404,22 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
         for (int ct = 0; ct < 4; ++ct) acc[kt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     u32x4 v[kTgtChunk];
     float lv = 0.0f;
-    fetch(0, v, lv);
+    fetch(0, 0, v, lv);
     stage(0, v, lv);
     __syncthreads();
     bf16x8 kv[KT][4][4];
-    for (int u = 0; u < stages; ++u) {
-        const int k = u % nchunk;
+    // stage u = (KV head g, block k of kTgtChunk combinations), walked in order
+    int g = 0, k = 0, buf = 0;
+    for (;;) {
         if (k == 0 && active) {
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
-                kd_load_keys<PAGED>(a, b, jw + kt * kKdTile, len, u / nchunk, col, grp, kv[kt]);
+                kd_load_keys<PAGED>(a, b, jw + kt * kKdTile, len, g, col, grp, kv[kt]);
         }
-        if (u + 1 < stages) fetch(u + 1, v, lv);
+        const int k1 = k + 1 == nchunk ? 0 : k + 1, g1 = k + 1 == nchunk ? g + 1 : g;
+        const bool more = g1 < a.kv_heads;
+        if (more) fetch(g1, k1 * kTgtChunk, v, lv);
         if (active) {
-            const int buf = u & 1;
 #pragma unroll
             for (int c = 0; c < kTgtChunk; ++c) {
                 if (k * kTgtChunk + c >= combos) break;  // uniform: short last stage
@@ -436,8 +439,12 @@ __global__ __launch_bounds__(256) void kd_target_kernel(KdArgs a) {
                 }
             }
         }
-        if (u + 1 < stages) stage((u + 1) & 1, v, lv);
+        if (more) stage(buf ^ 1, v, lv);
         __syncthreads();
+        if (!more) break;
+        g = g1;
+        k = k1;
+        buf ^= 1;
     }
     if (!active) return;
 #pragma unroll
@@ -819,8 +826,18 @@ hipError_t launch_kd_target(const Geometry &g, int n_layers, const void *q_layer
     a.key_tiles = div_up(g.max_len, 4 * kTgtWaveTiles * kKdTile);
     const long long groups = ((long long)g.batch * a.row_tiles + 7) / 8;
     const dim3 tgt_grid((unsigned)(groups * a.key_tiles * 8));
-    if (paged) kd_target_kernel<true><<<tgt_grid, dim3(256), 0, stream>>>(a);
-    else kd_target_kernel<false><<<tgt_grid, dim3(256), 0, stream>>>(a);
+#define KD_TGT(G)                                                                  \
+    (paged ? kd_target_kernel<G, true><<<tgt_grid, dim3(256), 0, stream>>>(a)     \
+           : kd_target_kernel<G, false><<<tgt_grid, dim3(256), 0, stream>>>(a))
+    switch (g.group) {
+        case 1: KD_TGT(1); break;
+        case 2: KD_TGT(2); break;
+        case 4: KD_TGT(4); break;
+        case 5: KD_TGT(5); break;
+        case 8: KD_TGT(8); break;
+        default: return hipErrorInvalidValue;
+    }
+#undef KD_TGT
     return hipGetLastError();
 }
 
