@@ -428,6 +428,9 @@ def main() -> int:
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the timed steps, run plain device-to-device copies of this "
                          "many MiB (a known-size reference for hardware byte counters)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured in a HIP graph and replayed "
+                         "(graph_us_per_step; one cache copy)")
     ap.add_argument("--kd", action="store_true",
                     help="instead of the decode step, time the training-side distillation step "
                          "(Eq. 5 target, Eq. 6 loss and indexer gradient) on the 32K-token "
@@ -523,8 +526,8 @@ def main() -> int:
         B.clsa_set_phase_events(None)
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t) * 1e3 / args.steps
-        ph = np.array([[ev.elapsed_ms(ne * i + a, ne * i + a + 1) for a in range(3)]
-                       for i in range(args.steps)])
+        ph = np.array([[ev.elapsed_ms(ne * i + a, ne * i + a + 1) for a in range(3)] +
+                       [ev.elapsed_ms(ne * i, ne * i + 3)] for i in range(args.steps)])
         attn = (np.array([[ev.elapsed_ms(ne * i + 4 + 2 * l, ne * i + 5 + 2 * l)
                            for l in range(L)] for i in range(args.steps)])
                 if per_layer else None)
@@ -533,7 +536,27 @@ def main() -> int:
 
     _, ph, _ = event_pass(False)
     ms_per_step_events, ph_layers, attn = event_pass(True)
-    index_ms, topk_ms, layers_ms = (float(v) for v in ph.mean(axis=0))
+    index_ms, topk_ms, layers_ms = (float(v) for v in ph[:, :3].mean(axis=0))
+    step_pct = np.percentile(ph[:, 3], [10, 50, 90]) * 1e3  # per step, from the phase pass
+
+    graph_us = None
+    if args.graph:
+        # the same step captured in a HIP graph (one cache copy), replayed K times
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            ki, kc, vc = caches[0]
+            B.clsa_decode_step(sh, q_idx, ki, kc, vc, pt, seq_lens, q_pos, q_layers, out, lse,
+                               idx, ns, ws)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        graph_us = (time.perf_counter() - t) * 1e6 / args.steps
+        del g
     attn_ms = float(attn.mean())
     attn_first_ms = float(attn[:, 0].mean())
 
@@ -562,6 +585,7 @@ def main() -> int:
                    "paged": bool(w.page_size), "planted": w.planted},
         "tokens_per_s": round(w.batch * w.n_q / (ms_per_step * 1e-3), 1),
         "hbm_GBps": round(ab["step"] / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_us_p10_p50_p90": [round(float(v), 2) for v in step_pct],
         "phases_us": {"index": round(index_ms * 1e3, 2), "topk": round(topk_ms * 1e3, 2),
                       "layers": round(layers_ms * 1e3, 2),
                       "per_layer": round(layers_ms * 1e3 / max(L, 1), 2),
@@ -574,6 +598,8 @@ def main() -> int:
                            if w.n_q >= PREFILL_MIN_ROWS else
                            roofline("index_decode_kernel", w, ab["index"], index_ms)),
     }
+    if graph_us is not None:
+        res["graph_us_per_step"] = round(graph_us, 2)
     if args.cpu_budget > 0:
         log("[bench] CPU oracle baseline ...")
         res["cpu_baseline"] = cpu_baseline(w, x, args.cpu_budget)
