@@ -11,8 +11,8 @@ namespace {
 
 using clsa::Geometry;
 
-constexpr int kMaxTopK = 8192;
-constexpr int kMaxLen = 262144;
+using clsa::kMaxTopK;
+using clsa::kMaxLen;
 constexpr size_t kAlign = 256;
 
 constexpr int kHookLayers = 64;  // layers whose attention kernel the hook can bracket
@@ -128,16 +128,17 @@ struct TopkWs {
     size_t zero_count = 0;
 };
 
-// Multi-workgroup top-k state: [hist | counters] (cleared per call), bitmaps, candidates.
+// Multi-workgroup top-k state: the coarse histogram (cleared per call), the
+// bitmap, the candidate regions and their counts.
 void carve_topk(const Geometry &g, Carver &c, TopkWs &t) {
     if (!clsa::topk_uses_wide(g)) return;
     const clsa::TopkWideLayout L = clsa::topk_wide_layout(g);
-    t.zero_count = L.hist_u32 + L.counters_u32;
+    t.zero_count = L.hist_u32;
     t.zero = c.take<uint32_t>(t.zero_count);
     t.buf.hist = t.zero;
-    t.buf.counters = t.zero ? t.zero + L.hist_u32 : nullptr;
-    t.buf.bitmaps = c.take<uint32_t>(2 * L.bitmap_u32);
-    t.buf.cands = c.take<uint32_t>(2 * L.cand_u32);
+    t.buf.bitmaps = c.take<uint32_t>(L.bitmap_u32);
+    t.buf.cands = c.take<uint32_t>(L.cand_u32);
+    t.buf.counts = c.take<uint32_t>(L.count_u32);
 }
 
 struct AttnWs {
@@ -150,7 +151,7 @@ void carve_attn(const Geometry &g, Carver &c, AttnWs &w, bool dense = false) {
 
 struct DecodeWs {
     float *scores = nullptr;
-    uint32_t *zero = nullptr;  // [coarse histogram | top-k counters], cleared per step
+    uint32_t *zero = nullptr;  // coarse histogram, cleared per step
     size_t zero_count = 0;
     clsa::TopkBuffers topk{};
     float *partials = nullptr;
@@ -163,18 +164,14 @@ struct DecodeWs {
 size_t carve_decode(const Geometry &g, void *base, DecodeWs &w) {
     Carver c{static_cast<char *>(base)};
     w.scores = c.take<float>((size_t)g.rows * g.max_len);
-    const size_t hist = (size_t)g.rows * clsa::kCoarseBins;
-    const size_t counters = (size_t)g.rows * 2;
-    w.zero_count = hist + counters;
+    w.zero_count = (size_t)g.rows * clsa::kCoarseBins;
     w.zero = c.take<uint32_t>(w.zero_count);
-    if (w.zero) {
-        w.topk.hist = w.zero;
-        w.topk.counters = w.zero + hist;
-    }
+    w.topk.hist = w.zero;
     if (clsa::topk_uses_wide(g)) {
         const clsa::TopkWideLayout L = clsa::topk_wide_layout(g);
-        w.topk.bitmaps = c.take<uint32_t>(2 * L.bitmap_u32);
-        w.topk.cands = c.take<uint32_t>(2 * L.cand_u32);
+        w.topk.bitmaps = c.take<uint32_t>(L.bitmap_u32);
+        w.topk.cands = c.take<uint32_t>(L.cand_u32);
+        w.topk.counts = c.take<uint32_t>(L.count_u32);
     }
     w.partials = c.take<float>(clsa::attn_partial_floats(g));
     return c.off;
@@ -338,7 +335,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
     const bool hook = g_hook.on;
     // Many query rows per sequence (chunked prefill): scores on the matrix cores,
     // without the coarse histogram, which the top-k then makes itself.  The
-    // histogram and counters need clearing unless that top-k is the per-row one.
+    // histogram needs clearing unless that top-k is the per-row one.
     const bool mfma = clsa::index_uses_mfma(g);
     const size_t q_stride = (size_t)g.rows * g.q_heads * 128;  // bf16 elements per layer
     const size_t lse_stride = (size_t)g.rows * g.q_heads;

@@ -20,6 +20,9 @@ struct Geometry {
     float softmax_scale;
 };
 
+// Longest supported sequence capacity (max_len) and largest top_k.
+constexpr int kMaxLen = 262144;
+constexpr int kMaxTopK = 8192;
 // Tokens scored by one indexer workgroup (4 waves x 32 tokens).
 constexpr int kIndexTile = 128;
 // Bins of the coarse score histogram made by the indexer (top 11 key bits,
@@ -30,8 +33,6 @@ constexpr int kCoarseBins = 1 << (32 - kCoarseShift);
 constexpr int kTopkCandCap = 8192;
 // Rows up to which the top-k splits each row over many workgroups.
 constexpr int kTopkWideMaxRows = 128;
-// Candidate list capacity per row of the multi-workgroup top-k (global memory).
-constexpr int kTopkWideCandCap = 16384;
 
 __host__ __device__ inline int div_up(int a, int b) { return (a + b - 1) / b; }
 
@@ -53,14 +54,14 @@ hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void
 
 // ---- topk.hip ----
 struct TopkWideLayout {
-    int words_max, cand_cap;
-    size_t hist_u32, counters_u32, bitmap_u32, cand_u32;  // per buffer, all rows
+    int words_max, regions;  // per row: bitmap words, 1024-key candidate regions
+    size_t hist_u32, bitmap_u32, cand_u32, count_u32;  // per buffer, all rows
 };
 struct TopkBuffers {
     uint32_t *hist;      // [rows, kCoarseBins]; zero on entry unless already filled
-    uint32_t *counters;  // [rows, 2]; zero on entry (wide path), left zero
-    uint32_t *bitmaps;   // 2 x bitmap_u32 (wide path)
-    uint32_t *cands;     // 2 x cand_u32 (wide path)
+    uint32_t *bitmaps;   // bitmap_u32: keys above the coarse bin (wide path)
+    uint32_t *cands;     // cand_u32: candidate regions (wide path)
+    uint32_t *counts;    // count_u32: candidates per region (wide path)
 };
 bool topk_uses_wide(const Geometry &g);
 TopkWideLayout topk_wide_layout(const Geometry &g);

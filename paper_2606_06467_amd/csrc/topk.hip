@@ -20,14 +20,16 @@
 //   * topk_row_kernel: one 1024-thread workgroup per row, bitmaps and the
 //     candidate list in LDS -- for many rows (chunked prefill);
 //   * for the few, long rows of decode, step 2 is spread over many 256-thread
-//     workgroups (topk_filter_kernel, 4096 keys each, global bitmaps and a
-//     global candidate list) and a second launch with one workgroup per row
-//     (topk_finish_kernel) does steps 3-5 with the bitmaps copied to LDS.  The
-//     hand-off goes through the kernel boundary: a ticket taken by the last
-//     filter workgroup would need an agent-scope release fence, which on this
-//     chip writes back the whole L2 of the XCD from every workgroup.
-// If a candidate list overflows (very flat score rows), steps 3-4 re-read the
-// row instead: slower, same result.
+//     workgroups (topk_filter_kernel, 4096 keys each, writing a global bitmap
+//     and, per wave, its candidates into a region of its own) and a second
+//     launch with one workgroup per row (topk_finish_kernel) does steps 3-5
+//     with the bitmaps in LDS and the candidates in registers.  The hand-off
+//     goes through the kernel boundary: a ticket taken by the last filter
+//     workgroup would need an agent-scope release fence, which on this chip
+//     writes back the whole L2 of the XCD from every workgroup.
+// If the per-row kernel's candidate list overflows (very flat score rows),
+// steps 3-4 re-read the row instead: slower, same result.  The regions of the
+// wide path hold every key of their wave, so they never overflow.
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -42,157 +44,208 @@ constexpr int kWideThreads = 256;
 constexpr int kWideChunk = 4096;  // keys filtered by one wide workgroup (16 per thread)
 constexpr int kRowThreads = 1024;
 
+// Inclusive prefix sum over the 64 lanes of a wave (every lane active): DPP
+// row shifts by 1, 2, 4 and 8 inside each row of 16 lanes (a lane whose source
+// lies outside its row adds 0), then the totals of the rows below are read
+// with v_readlane.  No LDS round trips.
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t t = __shfl_up(v, d);
-        if (lane >= d) v += t;
-    }
-    return v;
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 31);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 47);
+    const int row = lane >> 4;
+    return v + (row > 0 ? r0 : 0u) + (row > 1 ? r1 : 0u) + (row > 2 ? r2 : 0u);
 }
 
-// Exclusive prefix over the workgroup of one value per thread; also returns the total.
-// s_wave needs 2 * NT/64 + 1 entries.
+// Exclusive prefix sums over the workgroup of two values per thread, and their
+// totals.  s_wave: 2 * NT / 64 entries.  One barrier to publish the wave totals
+// (each thread then adds those of the waves before its own) and one before
+// s_wave may be reused.
 template <int NT>
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *s_wave, uint32_t &total) {
+__device__ __forceinline__ void block_excl_scan2(uint32_t x, uint32_t y, uint32_t *s_wave,
+                                                 uint32_t &x_before, uint32_t &y_before,
+                                                 uint32_t &x_total, uint32_t &y_total) {
     constexpr int NW = NT / 64;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const uint32_t inc = wave_incl_scan(v, lane);
-    if (lane == 63) s_wave[wave] = inc;
-    __syncthreads();
-    if (wave == 0) {
-        const uint32_t w = lane < NW ? s_wave[lane] : 0u;
-        const uint32_t wi = wave_incl_scan(w, lane);
-        if (lane < NW) s_wave[NW + lane] = wi - w;
-        if (lane == NW - 1) s_wave[2 * NW] = wi;
+    const uint32_t xi = wave_incl_scan(x, lane), yi = wave_incl_scan(y, lane);
+    if (lane == 63) {
+        s_wave[wave] = xi;
+        s_wave[NW + wave] = yi;
     }
     __syncthreads();
-    const uint32_t r = s_wave[NW + wave] + inc - v;
-    total = s_wave[2 * NW];
+    uint32_t xo = 0, yo = 0, xs = 0, ys = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        const uint32_t u = s_wave[w], v = s_wave[NW + w];
+        xs += u;
+        ys += v;
+        xo += w < wave ? u : 0u;
+        yo += w < wave ? v : 0u;
+    }
+    x_before = xo + xi - x;
+    y_before = yo + yi - y;
+    x_total = xs;
+    y_total = ys;
     __syncthreads();
-    return r;
 }
 
-// Given hist[nbins] in LDS, find the bin b with suffix(b) >= need > suffix(b+1),
-// suffix(x) = sum of the bins >= x.  Writes b and suffix(b+1) to out[0..1]
-// (0, 0 if no bin qualifies, which consistent counts never produce).
-template <int NT>
-__device__ void find_threshold_bin(const uint32_t *hist, int nbins, uint32_t need,
-                                   uint32_t *s_wave, uint32_t *out) {
-    const int per = nbins / NT > 0 ? nbins / NT : 1;
-    if (threadIdx.x == 0) {
-        out[0] = 0u;
-        out[1] = 0u;
-    }
-    // thread t owns bins [nbins - (t+1)*per, nbins - t*per): thread 0 owns the top
-    // bins, so an exclusive prefix over threads is a suffix over bins.
-    const int hi = nbins - (int)threadIdx.x * per;
-    const int lo = hi - per;
-    uint32_t s = 0;
-    if (lo >= 0)
-        for (int x = lo; x < hi; ++x) s += hist[x];
-    uint32_t total;
-    const uint32_t above = block_excl_scan<NT>(s, s_wave, total);  // keys in bins >= hi
-    if (lo >= 0 && above < need && above + s >= need) {
-        uint32_t acc = above;
-        for (int x = hi - 1; x >= lo; --x) {
-            const uint32_t c = hist[x];
-            if (acc + c >= need) {
-                out[0] = (uint32_t)x;
-                out[1] = acc;
-                break;
+// Given hist[NBINS] in LDS, find the bin b with suffix(b) >= need > suffix(b+1),
+// suffix(x) = the keys in bins >= x, and write b and suffix(b+1) to out[0..1]
+// ((0, 0) if no bin qualifies, which consistent counts never produce).  One
+// wave searches in two levels: lane l sums the NBINS/64 bins just below
+// NBINS - l * NBINS/64, so an inclusive prefix over lanes is a suffix over
+// bins and the first lane whose prefix reaches `need` holds b; then lane i
+// takes that lane's i-th bin from the top, and a second prefix and ballot
+// locate b itself.  Every thread of the workgroup calls this (it ends with a
+// barrier).
+template <int NBINS>
+__device__ __forceinline__ void find_threshold_bin(const uint32_t *hist, uint32_t need,
+                                                   uint32_t *out) {
+    constexpr int PER = NBINS / 64;
+    static_assert(PER % 4 == 0 && PER <= 64, "bins are read four at a time, one per lane");
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        uint32_t sum = 0;
+#pragma unroll
+        for (int i = 0; i < PER; i += 4) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(hist + NBINS - (lane + 1) * PER + i);
+            sum += (v.x + v.y) + (v.z + v.w);
+        }
+        const uint32_t inc = wave_incl_scan(sum, lane);
+        const uint64_t reach = __ballot(inc >= need);
+        if (reach == 0) {
+            if (lane == 0) {
+                out[0] = 0u;
+                out[1] = 0u;
             }
-            acc += c;
+        } else {
+            const int owner = __builtin_ctzll(reach);
+            const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)(inc - sum), owner);
+            const int top = NBINS - owner * PER - 1;  // the owner's highest bin
+            const uint32_t c = lane < PER ? hist[top - lane] : 0u;
+            const uint32_t sfx = above + wave_incl_scan(c, lane);  // suffix(top - lane)
+            const int i = __builtin_ctzll(__ballot(sfx >= need));
+            if (lane == i) {
+                out[0] = (uint32_t)(top - i);
+                out[1] = sfx - c;
+            }
         }
     }
     __syncthreads();
 }
 
 // Steps 3 and 4 for the keys of coarse bin b1 (visited by `visit(fn)`, which
-// calls fn(key, position) for every such key).  hist: LDS [kHistWords].
+// calls fn(key, position) for every such key).  hist: LDS [kMidBins], low: LDS
+// [kLowBins]; both are cleared here, together, so that the second digit's
+// histogram needs no barrier of its own before it is filled.
 template <int NT, class Visit>
 __device__ void refine_and_mark(Visit visit, uint32_t b1, uint32_t need1, uint32_t *hist,
-                                uint32_t *s_wave, uint32_t *s_res, uint32_t *sure, uint32_t *tie,
+                                uint32_t *low, uint32_t *s_res, uint32_t *sure, uint32_t *tie,
                                 uint32_t &r_ties) {
     for (int x = threadIdx.x; x < kMidBins; x += NT) hist[x] = 0u;
+    for (int x = threadIdx.x; x < kLowBins; x += NT) low[x] = 0u;
     __syncthreads();
     visit([&](uint32_t key, uint32_t) {
         atomicAdd(&hist[(key >> kMidShift) & (kMidBins - 1)], 1u);
     });
     __syncthreads();
-    find_threshold_bin<NT>(hist, kMidBins, need1, s_wave, s_res);
+    find_threshold_bin<kMidBins>(hist, need1, s_res);
     const uint32_t b2 = s_res[0];
     const uint32_t need2 = need1 - s_res[1];
-    __syncthreads();
     const uint32_t pref = (b1 << (kCoarseShift - kMidShift)) | b2;  // key >> kMidShift
-    for (int x = threadIdx.x; x < kLowBins; x += NT) hist[x] = 0u;
-    __syncthreads();
     visit([&](uint32_t key, uint32_t) {
-        if ((key >> kMidShift) == pref) atomicAdd(&hist[key & (kLowBins - 1)], 1u);
+        if ((key >> kMidShift) == pref) atomicAdd(&low[key & (kLowBins - 1)], 1u);
     });
-    __syncthreads();
-    find_threshold_bin<NT>(hist, kLowBins, need2, s_wave, s_res);
+    __syncthreads();  // also: every thread has read s_res before it is rewritten
+    find_threshold_bin<kLowBins>(low, need2, s_res);
     const uint32_t tau = (pref << kMidShift) | s_res[0];
     r_ties = need2 - s_res[1];  // keys equal to tau that are taken (>= 1)
-    __syncthreads();
     visit([&](uint32_t key, uint32_t j) {
         if (key > tau) atomicOr(&sure[j >> 5], 1u << (j & 31));
         else if (key == tau) atomicOr(&tie[j >> 5], 1u << (j & 31));
     });
 }
 
-// Step 5: ordered output from the bitmaps (words [0, words)).
+// Step 5: ordered output from the bitmaps (words [0, words), a multiple of 4).
+// Per slice of 4 * NT words, each thread owns 4 consecutive words (one 16-byte
+// LDS read per bitmap); a workgroup-wide prefix of the sure and tie counts
+// gives each thread its first output slot, and of the ties only the first
+// r_ties in position order are kept (ties go to the lowest index).  A thread
+// then emits its positions in one loop over the set bits of its 128 positions.
 template <int NT>
 __device__ void compact_bitmaps(const uint32_t *sure, const uint32_t *tie, int words,
                                 uint32_t r_ties, int k, int32_t *out, uint32_t *s_wave) {
-    const int per = div_up(words, NT);
-    const int w0 = threadIdx.x * per;
-    const int w1 = min(words, w0 + per);
-    uint32_t cs = 0, ct = 0;
-    for (int w = w0; w < w1; ++w) {
-        cs += __popc(sure[w]);
-        ct += __popc(tie[w]);
-    }
-    uint32_t tot_s, tot_t;
-    uint32_t sure_before = block_excl_scan<NT>(cs, s_wave, tot_s);
-    uint32_t tie_before = block_excl_scan<NT>(ct, s_wave, tot_t);
-    for (int w = w0; w < w1; ++w) {
-        const uint32_t sw = sure[w];
-        uint32_t sel = sw;
-        uint32_t tw = tie[w];
-        uint32_t pos = sure_before + min(tie_before, r_ties);
-        uint32_t take = tie_before < r_ties ? r_ties - tie_before : 0u;
-        tie_before += __popc(tw);
-        sure_before += __popc(sw);
-        while (tw && take) {  // the lowest-index ties are the ones kept
-            const uint32_t low = tw & (0u - tw);
-            sel |= low;
-            tw ^= low;
-            --take;
+    uint32_t sure_done = 0, tie_done = 0;  // counts of the slices before
+    for (int s0 = 0; s0 < words; s0 += 4 * NT) {  // uniform
+        const int w0 = s0 + 4 * (int)threadIdx.x;
+        uint4 sv = make_uint4(0u, 0u, 0u, 0u), tv = make_uint4(0u, 0u, 0u, 0u);
+        if (w0 < words) {
+            sv = *reinterpret_cast<const uint4 *>(sure + w0);
+            tv = *reinterpret_cast<const uint4 *>(tie + w0);
         }
-        while (sel && pos < (uint32_t)k) {
-            const int bit = __ffs(sel) - 1;
-            sel &= sel - 1;
-            out[pos++] = w * 32 + bit;
+        uint64_t a = sv.x | ((uint64_t)sv.y << 32), b = sv.z | ((uint64_t)sv.w << 32);
+        uint64_t ta = tv.x | ((uint64_t)tv.y << 32), tb = tv.z | ((uint64_t)tv.w << 32);
+        const uint32_t cs = __popcll(a) + __popcll(b), ct = __popcll(ta) + __popcll(tb);
+        uint32_t sure_before, tie_before, sure_total, tie_total;
+        block_excl_scan2<NT>(cs, ct, s_wave, sure_before, tie_before, sure_total, tie_total);
+        sure_before += sure_done;
+        tie_before += tie_done;
+        sure_done += sure_total;
+        tie_done += tie_total;
+        uint32_t take = tie_before < r_ties ? r_ties - tie_before : 0u;  // ties kept here
+        if (take >= ct) {
+            a |= ta;
+            b |= tb;
+        } else {
+            for (; take; --take) {  // the one thread that keeps only part of its ties
+                if (ta) {
+                    a |= ta & (0ull - ta);
+                    ta &= ta - 1;
+                } else {
+                    b |= tb & (0ull - tb);
+                    tb &= tb - 1;
+                }
+            }
+        }
+        uint32_t pos = sure_before + min(tie_before, r_ties);
+        const int p0 = w0 * 32;
+        while (a | b) {
+            const bool lo = a != 0;
+            const uint64_t m = lo ? a : b;
+            const int bit = __builtin_ctzll(m) + (lo ? 0 : 64);
+            if (lo) a &= a - 1;
+            else b &= b - 1;
+            if (pos < (uint32_t)k) out[pos] = p0 + bit;
+            ++pos;
         }
     }
 }
 
 // One wave's share of the filter pass: 1024 keys starting at `base`, lane-strided
-// so that each ballot is exactly two bitmap words.  Keys past n are neither
-// selected nor candidates.  Candidate slots come from `*cand_count`.
-template <class AppendFn>
-__device__ __forceinline__ void filter_1024(const float *srow, int base, int n, uint32_t b1,
-                                            uint32_t *sure_words, uint32_t *tie_words,
-                                            uint32_t *cand_count, AppendFn append) {
+// so that each ballot is exactly two bitmap words.  filter_load_1024 reads them
+// (positions clamped to `last`, which must be readable); filter_classify_1024
+// marks the keys above bin b1 in the bitmap words and returns, per 64 keys, the
+// ballot of those in it; filter_append_1024 hands those candidates, in position
+// order, to `append` from slot `slot` on.  Keys past n are neither selected nor
+// candidates.
+__device__ __forceinline__ void filter_load_1024(const float *srow, int base, int last,
+                                                 uint32_t (&key)[16]) {
     const int lane = threadIdx.x & 63;
-    uint32_t key[16];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-        const int j = min(base + u * 64 + lane, n - 1);
-        key[u] = score_key(__builtin_nontemporal_load(srow + j));
-    }
-    uint64_t cmask[16];
+    for (int u = 0; u < 16; ++u)
+        key[u] = score_key(__builtin_nontemporal_load(srow + min(base + u * 64 + lane, last)));
+}
+
+// Returns the wave's candidate count.
+__device__ __forceinline__ uint32_t filter_classify_1024(const uint32_t (&key)[16], int base,
+                                                         int n, uint32_t b1,
+                                                         uint32_t *sure_words,
+                                                         uint32_t *tie_words,
+                                                         uint64_t (&cmask)[16]) {
+    const int lane = threadIdx.x & 63;
     uint32_t ccount = 0;
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
@@ -203,12 +256,17 @@ __device__ __forceinline__ void filter_1024(const float *srow, int base, int n, 
         ccount += __popcll(cmask[u]);
         if (lane < 2) {
             sure_words[2 * u + lane] = lane ? (uint32_t)(sm >> 32) : (uint32_t)sm;
-            tie_words[2 * u + lane] = 0u;
+            if (tie_words) tie_words[2 * u + lane] = 0u;
         }
     }
-    uint32_t slot = 0;
-    if (lane == 0 && ccount) slot = atomicAdd(cand_count, ccount);
-    slot = __shfl(slot, 0);
+    return ccount;
+}
+
+template <class AppendFn>
+__device__ __forceinline__ void filter_append_1024(const uint32_t (&key)[16], int base,
+                                                   const uint64_t (&cmask)[16], uint32_t slot,
+                                                   AppendFn append) {
+    const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
         const uint64_t lower = lane ? (cmask[u] << (64 - lane)) : 0ull;
@@ -236,8 +294,8 @@ struct TopkRowArgs {
 template <bool HAVE_HIST>
 __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
     constexpr int NW = kRowThreads / 64;
-    extern __shared__ uint32_t lds[];
-    __shared__ uint32_t s_wave[2 * NW + 1];
+    extern __shared__ __align__(16) uint32_t lds[];
+    __shared__ uint32_t s_wave[2 * NW];
     __shared__ uint32_t s_res[2];
     __shared__ uint32_t s_cand_count;
 
@@ -254,7 +312,8 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
     }
     const float *srow = a.scores + (size_t)row * a.max_len;
     uint32_t *hist = lds;                // kHistWords
-    uint32_t *sure = hist + kHistWords;  // words_max
+    uint32_t *low = hist + kHistWords;   // kLowBins
+    uint32_t *sure = low + kLowBins;     // words_max
     uint32_t *tie = sure + a.words_max;  // words_max
     uint32_t *ckey = tie + a.words_max;  // cand_cap
     uint32_t *cidx = ckey + a.cand_cap;  // cand_cap
@@ -276,20 +335,27 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
         }
         __syncthreads();
     }
-    find_threshold_bin<kRowThreads>(hist, kCoarseBins, (uint32_t)k, s_wave, s_res);
+    find_threshold_bin<kCoarseBins>(hist, (uint32_t)k, s_res);
     const uint32_t b1 = s_res[0];
     const uint32_t need1 = (uint32_t)k - s_res[1];
-    __syncthreads();
 
     const uint32_t cap = (uint32_t)a.cand_cap;
-    for (int c = wave; c < nchunks; c += NW)
-        filter_1024(srow, c * 1024, n, b1, sure + c * 32, tie + c * 32, &s_cand_count,
-                    [&](uint32_t at, uint32_t key, uint32_t j) {
-                        if (at < cap) {
-                            ckey[at] = key;
-                            cidx[at] = j;
-                        }
-                    });
+    for (int c = wave; c < nchunks; c += NW) {
+        uint32_t key[16];
+        filter_load_1024(srow, c * 1024, n - 1, key);
+        uint64_t cmask[16];
+        const uint32_t cnt =
+            filter_classify_1024(key, c * 1024, n, b1, sure + c * 32, tie + c * 32, cmask);
+        uint32_t slot = 0;
+        if (lane == 0 && cnt) slot = atomicAdd(&s_cand_count, cnt);
+        filter_append_1024(key, c * 1024, cmask, __shfl(slot, 0),
+                           [&](uint32_t at, uint32_t kv, uint32_t j) {
+                               if (at < cap) {
+                                   ckey[at] = kv;
+                                   cidx[at] = j;
+                               }
+                           });
+    }
     __syncthreads();
     const uint32_t ncand = s_cand_count;
     auto visit = [&](auto &&fn) {
@@ -303,7 +369,7 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
         }
     };
     uint32_t r_ties;
-    refine_and_mark<kRowThreads>(visit, b1, need1, hist, s_wave, s_res, sure, tie, r_ties);
+    refine_and_mark<kRowThreads>(visit, b1, need1, hist, low, s_res, sure, tie, r_ties);
     __syncthreads();
     compact_bitmaps<kRowThreads>(sure, tie, nchunks * 32, r_ties, k, out, s_wave);
     if (tid == 0) a.n_sel[row] = k;
@@ -316,75 +382,114 @@ struct TopkWideArgs {
     const float *scores;
     const int32_t *seq_lens;
     const int32_t *q_pos;
-    const uint32_t *hist;   // [rows, 256], complete
-    uint32_t *counters;     // [rows, 2]: candidate count (zero on entry), spare
-    uint32_t *sure;         // [rows, words_max]
-    uint32_t *tie;          // [rows, words_max]
-    uint32_t *ckey;         // [rows, cand_cap]
-    uint32_t *cidx;         // [rows, cand_cap]
+    const uint32_t *hist;   // [rows, kCoarseBins], complete
+    uint32_t *sure;         // [rows, words_max]: keys above the coarse bin
+    uint32_t *cands;        // [rows, regions, 1024]: candidate entries per region
+    uint32_t *counts;       // [rows, regions]: their number
     int32_t *idx;
     int32_t *n_sel;
-    int n_q, max_len, causal, top_k, chunks_per_row, words_max, cand_cap;
+    int n_q, max_len, causal, top_k, chunks_per_row, words_max, regions;
 };
 
-// b1 (the coarse bin of the k-th key) and k minus the keys above it, from the
-// row's complete coarse histogram.  hist: LDS scratch of kCoarseBins words.
-template <int NT>
-__device__ __forceinline__ void coarse_threshold(const uint32_t *ghist, int k, uint32_t *hist,
-                                                 uint32_t *s_wave, uint32_t *s_res,
-                                                 uint32_t &b1, uint32_t &need1) {
-    for (int x = threadIdx.x; x < kCoarseBins; x += NT) hist[x] = ghist[x];
-    __syncthreads();
-    find_threshold_bin<NT>(hist, kCoarseBins, (uint32_t)k, s_wave, s_res);
-    b1 = s_res[0];
-    need1 = (uint32_t)k - s_res[1];
-    __syncthreads();
+// Candidate entries of the wide path.  Region r of a row holds the candidates
+// among keys [1024 r, 1024 r + 1024) (one wave's share of the filter), in
+// position order; an entry packs the key bits below the coarse digit (the
+// coarse digit is b1 for every candidate) and the position inside the region.
+constexpr uint32_t kCandLowMask = (1u << kCoarseShift) - 1u;
+static_assert(kCoarseShift + 10 <= 32, "an entry holds the low key bits and 10 position bits");
+__device__ __forceinline__ uint32_t cand_entry(uint32_t key, uint32_t j) {
+    return ((key & kCandLowMask) << 10) | (j & 1023u);
 }
 
-// Step 2 for 4096 keys of one row.
+// Step 2 for 4096 keys of one row.  The loads that do not depend on the row's
+// length (its coarse histogram, 8 bins per thread, and the chunk's scores,
+// clamped to the row's capacity) are issued before that length is known, so
+// the workgroup waits for memory once before its threshold search.  Each wave
+// writes its candidates to its own region and their number beside it: no
+// atomics (one shared counter per row, taken by every wave or workgroup of the
+// row, serialised at the memory side and cost up to 5 us at 128K keys).
 __global__ __launch_bounds__(kWideThreads) void topk_filter_kernel(TopkWideArgs a) {
     constexpr int NW = kWideThreads / 64;
-    __shared__ uint32_t hist[kCoarseBins];
-    __shared__ uint32_t s_wave[2 * NW + 1];
+    constexpr int HPT = kCoarseBins / kWideThreads;
+    static_assert(kWideChunk == NW * 1024, "one region per wave");
+    __shared__ __align__(16) uint32_t hist[kCoarseBins];
     __shared__ uint32_t s_res[2];
 
     const int row = blockIdx.x / a.chunks_per_row;
     const int c = blockIdx.x - row * a.chunks_per_row;
+    const int tid = threadIdx.x, wave = tid >> 6;
+    const uint32_t *ghist = a.hist + (size_t)row * kCoarseBins;
+    uint32_t hv[HPT];
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) hv[u] = ghist[u * kWideThreads + tid];
+    const float *srow = a.scores + (size_t)row * a.max_len;
+    const int base = c * kWideChunk + wave * 1024;
+    uint32_t key[16];
+    filter_load_1024(srow, base, a.max_len - 1, key);
+
     const int b = row / a.n_q;
     const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
     if (n <= a.top_k || c * kWideChunk >= n) return;  // uniform
-    const int wave = threadIdx.x >> 6;
-    uint32_t b1, need1;
-    coarse_threshold<kWideThreads>(a.hist + (size_t)row * kCoarseBins, a.top_k, hist, s_wave,
-                                   s_res, b1, need1);
-    const float *srow = a.scores + (size_t)row * a.max_len;
-    uint32_t *ckey = a.ckey + (size_t)row * a.cand_cap;
-    uint32_t *cidx = a.cidx + (size_t)row * a.cand_cap;
-    const uint32_t cap = (uint32_t)a.cand_cap;
-    const int base = c * kWideChunk + wave * 1024;
-    filter_1024(srow, base, n, b1, a.sure + (size_t)row * a.words_max + base / 32,
-                a.tie + (size_t)row * a.words_max + base / 32, a.counters + 2 * (size_t)row,
-                [&](uint32_t at, uint32_t key, uint32_t j) {
-                    if (at < cap) {
-                        ckey[at] = key;
-                        cidx[at] = j;
-                    }
-                });
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) hist[u * kWideThreads + tid] = hv[u];
+    __syncthreads();
+    find_threshold_bin<kCoarseBins>(hist, (uint32_t)a.top_k, s_res);
+    const uint32_t b1 = s_res[0];
+    uint64_t cmask[16];
+    const uint32_t cnt = filter_classify_1024(
+        key, base, n, b1, a.sure + (size_t)row * a.words_max + base / 32, nullptr, cmask);
+    const size_t region = (size_t)row * a.regions + (size_t)(base >> 10);
+    if ((tid & 63) == 0) a.counts[region] = cnt;
+    uint32_t *rc = a.cands + region * 1024;
+    filter_append_1024(key, base, cmask, 0u,
+                       [&](uint32_t at, uint32_t kv, uint32_t j) { rc[at] = cand_entry(kv, j); });
 }
 
-// Steps 3-5 for one row; the bitmaps are copied to LDS (dynamic, 2 x words_max).
+constexpr int kFinishRegCands = 8;   // region entries per thread loaded in the first batch
+constexpr int kFinishRegWords = 8;   // bitmap words per thread loaded in the first batch
+static_assert(kFinishRegWords * kRowThreads * 32 >= kMaxLen, "one batch holds the whole bitmap");
+static_assert(kRowThreads / (kMaxLen / 1024) >= 1, "every region has a thread");
+
+// Steps 3-5 for one row.  The first batch of loads needs nothing but the row
+// number: the coarse histogram (two bins per thread), the "sure" bitmap
+// (kFinishRegWords words per thread: the whole bitmap of the longest supported
+// row) and the candidate regions -- T = kRowThreads / regions threads per
+// region, each loading its region's count and entries q, q + T, ... of the
+// first kFinishRegCands.  The refinement visits the candidates in registers;
+// only a region with more than T * kFinishRegCands candidates has the rest
+// read from memory.  The bitmaps live in LDS (dynamic, 2 x words_max); the
+// tie bitmap starts empty.
 __global__ __launch_bounds__(kRowThreads) void topk_finish_kernel(TopkWideArgs a) {
     constexpr int NW = kRowThreads / 64;
-    extern __shared__ uint32_t lds[];
-    __shared__ uint32_t hist[kHistWords];
-    __shared__ uint32_t s_wave[2 * NW + 1];
+    constexpr int HPT = kCoarseBins / kRowThreads;
+    extern __shared__ __align__(16) uint32_t lds[];
+    __shared__ __align__(16) uint32_t hist[kHistWords];
+    __shared__ __align__(16) uint32_t low[kLowBins];
+    __shared__ uint32_t s_wave[2 * NW];
     __shared__ uint32_t s_res[2];
 
     const int row = blockIdx.x;
-    const int b = row / a.n_q;
-    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
     const int k = a.top_k;
     const int tid = threadIdx.x;
+    const int nr = a.regions;
+    const int tpr = kRowThreads / nr;  // threads per region
+    const int r = min(tid / tpr, nr - 1), q = tid - (tid / tpr) * tpr;
+    const bool owner = tid / tpr < nr;
+    const uint32_t *ghist = a.hist + (size_t)row * kCoarseBins;
+    const uint32_t *gs = a.sure + (size_t)row * a.words_max;
+    const uint32_t *rc = a.cands + ((size_t)row * nr + r) * 1024;
+    uint32_t hv[HPT], sv[kFinishRegWords], ent[kFinishRegCands];
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) hv[u] = ghist[u * kRowThreads + tid];
+    const uint32_t rcount = a.counts[(size_t)row * nr + r];
+#pragma unroll
+    for (int u = 0; u < kFinishRegWords; ++u)
+        sv[u] = gs[min(u * kRowThreads + tid, a.words_max - 1)];
+#pragma unroll
+    for (int u = 0; u < kFinishRegCands; ++u) ent[u] = rc[min(q + u * tpr, 1023)];
+
+    const int b = row / a.n_q;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
     int32_t *out = a.idx + (size_t)row * k;
     if (n <= k) {  // every valid key is selected
         for (int i = tid; i < k; i += kRowThreads) out[i] = i < n ? i : -1;
@@ -392,34 +497,37 @@ __global__ __launch_bounds__(kRowThreads) void topk_finish_kernel(TopkWideArgs a
         return;
     }
     const int words = div_up(n, kWideChunk) * (kWideChunk / 32);
+    // regions the filter wrote (every wave of every chunk that holds keys)
+    const uint32_t cnt = owner && r < words / 32 ? min(rcount, 1024u) : 0u;
     uint32_t *sure = lds;
     uint32_t *tie = lds + a.words_max;
-    const uint32_t *gs = a.sure + (size_t)row * a.words_max;
-    const uint32_t *gt = a.tie + (size_t)row * a.words_max;
-    for (int w = tid; w < words; w += kRowThreads) {
-        sure[w] = gs[w];
-        tie[w] = gt[w];
+#pragma unroll
+    for (int u = 0; u < kFinishRegWords; ++u) {
+        const int w = u * kRowThreads + tid;
+        if (w < words) {
+            sure[w] = sv[u];
+            tie[w] = 0u;
+        }
     }
-    uint32_t b1, need1;
-    coarse_threshold<kRowThreads>(a.hist + (size_t)row * kCoarseBins, k, hist, s_wave, s_res, b1,
-                                  need1);
-    const float *srow = a.scores + (size_t)row * a.max_len;
-    const uint32_t *ckey = a.ckey + (size_t)row * a.cand_cap;
-    const uint32_t *cidx = a.cidx + (size_t)row * a.cand_cap;
-    const uint32_t ncand = a.counters[2 * (size_t)row];
-    const uint32_t cap = (uint32_t)a.cand_cap;
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) hist[u * kRowThreads + tid] = hv[u];
+    __syncthreads();
+    find_threshold_bin<kCoarseBins>(hist, (uint32_t)k, s_res);
+    const uint32_t b1 = s_res[0];
+    const uint32_t need1 = (uint32_t)k - s_res[1];
+    const uint32_t key_hi = b1 << kCoarseShift;
+    const uint32_t pos0 = (uint32_t)r * 1024u;
     auto visit = [&](auto &&fn) {
-        if (ncand <= cap) {
-            for (uint32_t i = tid; i < ncand; i += kRowThreads) fn(ckey[i], cidx[i]);
-        } else {
-            for (int j = tid; j < n; j += kRowThreads) {
-                const uint32_t key = score_key(srow[j]);
-                if ((key >> kCoarseShift) == b1) fn(key, (uint32_t)j);
-            }
+#pragma unroll
+        for (int u = 0; u < kFinishRegCands; ++u)
+            if ((uint32_t)(q + u * tpr) < cnt) fn(key_hi | (ent[u] >> 10), pos0 + (ent[u] & 1023u));
+        for (uint32_t i = q + kFinishRegCands * tpr; i < cnt; i += tpr) {
+            const uint32_t e = rc[i];
+            fn(key_hi | (e >> 10), pos0 + (e & 1023u));
         }
     };
     uint32_t r_ties;
-    refine_and_mark<kRowThreads>(visit, b1, need1, hist, s_wave, s_res, sure, tie, r_ties);
+    refine_and_mark<kRowThreads>(visit, b1, need1, hist, low, s_res, sure, tie, r_ties);
     __syncthreads();
     compact_bitmaps<kRowThreads>(sure, tie, words, r_ties, k, out, s_wave);
     if (tid == 0) a.n_sel[row] = k;
@@ -475,25 +583,25 @@ static int wide_words(int max_len) { return div_up(max_len, kWideChunk) * (kWide
 bool topk_uses_wide(const Geometry &g) { return g.rows <= kTopkWideMaxRows; }
 
 static size_t row_kernel_lds(int max_len) {
-    return sizeof(uint32_t) * ((size_t)kHistWords + 2 * (size_t)row_words(max_len) +
+    return sizeof(uint32_t) * ((size_t)kHistWords + kLowBins + 2 * (size_t)row_words(max_len) +
                                2 * (size_t)kTopkCandCap);
 }
 
 size_t topk_lds_bytes(const Geometry &g) {
-    if (topk_uses_wide(g))  // finish kernel: static fine histogram + two bitmaps
-        return sizeof(uint32_t) * ((size_t)kHistWords + 2 * (size_t)wide_words(g.max_len));
+    if (topk_uses_wide(g))  // finish kernel: static histograms + two bitmaps
+        return sizeof(uint32_t) * ((size_t)kHistWords + kLowBins + 2 * (size_t)wide_words(g.max_len));
     return row_kernel_lds(g.max_len);
 }
 
 TopkWideLayout topk_wide_layout(const Geometry &g) {
     TopkWideLayout L;
     L.words_max = wide_words(g.max_len);
-    L.cand_cap = kTopkWideCandCap;
+    L.regions = L.words_max / 32;
     const size_t rows = (size_t)g.rows;
     L.hist_u32 = rows * kCoarseBins;
-    L.counters_u32 = rows * 2;
     L.bitmap_u32 = rows * L.words_max;
-    L.cand_u32 = rows * (size_t)L.cand_cap;
+    L.cand_u32 = rows * L.regions * 1024;
+    L.count_u32 = rows * L.regions;
     return L;
 }
 
@@ -517,11 +625,9 @@ hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *se
         a.seq_lens = seq_lens;
         a.q_pos = q_pos;
         a.hist = buf.hist;
-        a.counters = buf.counters;
         a.sure = buf.bitmaps;
-        a.tie = buf.bitmaps + L.bitmap_u32;
-        a.ckey = buf.cands;
-        a.cidx = buf.cands + L.cand_u32;
+        a.cands = buf.cands;
+        a.counts = buf.counts;
         a.idx = idx;
         a.n_sel = n_sel;
         a.n_q = g.n_q;
@@ -530,7 +636,7 @@ hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *se
         a.top_k = g.top_k;
         a.chunks_per_row = cpr;
         a.words_max = L.words_max;
-        a.cand_cap = L.cand_cap;
+        a.regions = L.regions;
         topk_filter_kernel<<<dim3((unsigned)blocks), dim3(kWideThreads), 0, stream>>>(a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
