@@ -60,8 +60,9 @@ def test_scattered_ties():
 
 
 def test_all_equal_row_overflows_candidate_list():
-    """Every key falls in one coarse bin: the LDS candidate list overflows and the
-    kernel must fall back to re-reading the row."""
+    """Every key falls in one coarse bin: every candidate region of the
+    multi-workgroup path is full (1024 entries, most of them visited from memory
+    rather than registers)."""
     s = np.full((2, 1, 40000), 0.375, np.float32)
     s[1, 0, ::3] = -0.0
     s[1, 0, 1::3] = 0.0
@@ -106,3 +107,28 @@ def test_many_rows_prefill_like():
     s = inputs.random_scores(80, T, 16384)[None]
     q_pos = (16384 - T + np.arange(T, dtype=np.int32))[None]
     _check(s, 2048, [16384], q_pos=q_pos, what="256 causal rows")
+
+
+def test_all_equal_many_rows_per_row_kernel():
+    """Many rows (the one-workgroup-per-row kernel): all-equal rows overflow its
+    LDS candidate list, so it re-reads the row; ordinary rows in the same launch."""
+    s = inputs.random_scores(81, 160, 12000)[None]
+    s[0, ::3] = 0.75
+    s[0, 1::7] = -0.0
+    q_pos = (12000 - 160 + np.arange(160, dtype=np.int32))[None]
+    _check(s, 2048, [12000], q_pos=q_pos, what="160 rows, every third all-equal")
+
+
+def test_candidate_regions_at_register_boundary():
+    """Multi-workgroup path, 131072 keys: the finish kernel holds 8 threads x 8
+    entries of each 1024-key candidate region in registers.  Regions with 64,
+    65 and 1024 candidates (exactly fitting, one over, full), candidates tied
+    (row 0) or distinct inside one coarse bin (row 1), above-bin keys elsewhere."""
+    n, k = 131072, 1000
+    s = np.full((2, 1, n), -1.0, np.float32)
+    for row in range(2):
+        pos = np.concatenate([5 * 1024 + np.arange(64), 6 * 1024 + 3 + np.arange(65) * 2,
+                              7 * 1024 + np.arange(1024)])
+        s[row, 0, pos] = 0.5 if row == 0 else (0.5 + pos * 1e-7).astype(np.float32)
+        s[row, 0, 9 * 1024 + np.arange(100) * 7] = 2.0
+    _check(s, k, [n, n], what="regions with 64 / 65 / 1024 candidates")
