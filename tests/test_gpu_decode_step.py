@@ -110,6 +110,33 @@ def test_full_decode_b4_n128k_planted():
     assert frac > 0.5
 
 
+def test_tie_band_statistics_128k_planted_many_seeds():
+    """Index sets of the 128K planted step over 16 input seeds (64 rows; the index
+    pass and the top-k of clsa_decode_step, with no layers): every row outside
+    the tie band matches the oracle exactly; the rows inside it are counted and,
+    where they differ, checked to hold a valid top-k of the exact scores."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    w = inputs.workload("decode_b4_n128k_planted")
+    sh, shg = orc.shape_of(w), U.shape_of(w)
+    ws = B.workspace(shg, B.CLSA_OP_DECODE, 0)
+    tot = np.zeros(3, np.int64)
+    for s in range(16):
+        x = inputs.make_inputs(w, seed_base=1000 * w.wid + 30000 * (s + 1), index_only=True)
+        d = U.to_dev(x)
+        idx = torch.full((w.batch, w.n_q, w.top_k), -7, dtype=torch.int32, device="cuda")
+        ns = torch.full((w.batch, w.n_q), -7, dtype=torch.int32, device="cuda")
+        B.clsa_decode_step(shg, d["q_idx"], d["k_idx"], None, None, d["page_table"],
+                           d["seq_lens"], d["q_pos"], None, None, None, idx, ns, ws)
+        torch.cuda.synchronize()
+        scores = orc.index_scores(sh, x["q_idx"], x["k_idx"], x["seq_lens"], x["q_pos"],
+                                  x["page_table"])
+        tot += U.check_index_sets(w, sh, scores, idx.cpu().numpy(), ns.cpu().numpy(),
+                                  x["seq_lens"], x["q_pos"], bound=U.higham_bound(w, x))
+    U.log(f"  tie band, 128K planted, 16 seeds: {tot[0]} rows, {tot[1]} in the band, "
+          f"{tot[2]} of them differ, 0 differ outside it")
+
+
 def test_full_decode_b8_n32k():
     w = inputs.workload("decode_b8_n32k")
     x = inputs.make_inputs(w)
