@@ -11,16 +11,15 @@
 // Key-stationary work split: a workgroup owns 256 consecutive keys of one
 // sequence (each of its 4 waves holds 64 of them, all 256 dims, as A operands
 // in registers for the whole kernel) and streams that sequence's queries 16 at
-// a time (the B operands: 8 loads of 16 bytes per lane, the next tile's loads
-// issued before the current tile's products).  The keys are read from HBM
-// exactly once; the queries (512 bytes each, 4 MiB for 8192 of them) are read
-// by every workgroup and stay in the L2.  Query tiles whose rows all end
-// before the block's first key (causal) are skipped.  The score block is
-// written once, non-temporally (the top-k reads it back), which bounds the
-// kernel by HBM writes (4 bytes per 512 FLOP) rather than by the matrix cores;
-// each query tile's 16 x 256 scores are therefore staged in LDS and written as
-// whole 1 KiB row segments (direct 16-byte stores of 64-byte row pieces
-// reached only about 3 TB/s).
+// a time as B operands.  Each query tile is loaded once per workgroup (a
+// quarter per wave, a tile ahead) and shared through LDS; the keys are read
+// from HBM exactly once and the queries (512 bytes each, 4 MiB for 8192 of
+// them) from the L2.  Query tiles whose rows all end before the block's first
+// key (causal) are skipped.  The score block is written once,
+// non-temporally (the top-k reads it back): each tile's 16 x 256 scores are
+// staged in LDS and written as whole 1 KiB row segments (direct 16-byte stores
+// of 64-byte row pieces reached only about 3 TB/s), one tile later, after the
+// next wait, so that waiting for loads never waits for fresh stores.
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -49,46 +48,56 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t *p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
 }
 
-// B operands of query tile qt: lane (col, grp) reads dims kb*32 + grp*8 .. +8
-// of query qt*16 + col (clamped to the last query; extra rows are not stored).
-__device__ __forceinline__ void load_queries(const PrefillArgs &a, int b, int qt, int col,
-                                             int grp, bf16x8 (&qv)[8]) {
-    const int t = min(qt * 16 + col, a.n_q - 1);
-    const uint16_t *p = a.q_idx + ((size_t)b * a.n_q + t) * kIdxDim + grp * 8;
-#pragma unroll
-    for (int kb = 0; kb < 8; ++kb) qv[kb] = load_bf16x8(p + kb * 32);
-}
-
-// Number of keys query t may see (0 past the last query).  Branch-free: the
-// position load is unconditional (clamped), so no wait is placed inside a branch.
+// Number of keys query t may see (0 past the last query), in two steps so that
+// the position load can be issued a tile ahead and its result used only after
+// the next wait: key_pos loads the raw position (clamped index: no branch),
+// key_limit turns it into the limit.
 template <bool CAUSAL>
-__device__ __forceinline__ int key_limit(const int32_t *qpos, int len, int n_q, int t) {
-    int n = len;
-    if (CAUSAL) n = min(len, max(qpos[min(t, n_q - 1)] + 1, 0));
+__device__ __forceinline__ int key_pos(const int32_t *qpos, int n_q, int t) {
+    return CAUSAL ? qpos[min(t, n_q - 1)] : 0;
+}
+template <bool CAUSAL>
+__device__ __forceinline__ int key_limit(int pos, int len, int n_q, int t) {
+    const int n = CAUSAL ? min(len, max(pos + 1, 0)) : len;
     return t < n_q ? n : 0;
 }
 
 // LDS staging of one query tile's scores: 16 rows x the workgroup's 256 keys
 // (padded rows against bank conflicts), two buffers used alternately.
 constexpr int kTileStride = kPfKeys + 4;
+// Query tile rows in LDS: 256 bf16 + 8 of padding (528 bytes), so that the 16
+// rows read by one operand load fall on different banks.
+constexpr int kQStride = kIdxDim + 8;
 
-// Scores of query tile qt against the workgroup's 256 keys.  Each wave writes
-// its 16 x 64 part into the LDS tile; after a barrier each wave stores four
-// whole rows (one 1 KiB row segment per store instruction).  n: key limit of
-// this lane's query (qt*16 + (lane & 15)).  The early exit is uniform over the
-// workgroup (every wave holds the same 16 queries); it still passes a barrier
-// so that a buffer is never rewritten while another wave reads it.
-__device__ __forceinline__ void score_tile(const PrefillArgs &a, const bf16x8 (&kv)[4][8],
-                                           const bf16x8 (&qv)[8], int n, int b, int qt, int jg,
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt in
+// 6:4, lgkmcnt in 11:8; a field at its maximum does not wait).
+constexpr int kPfWaitLgkm0 = 0xC07F;  // lgkmcnt(0)
+constexpr int kPfWaitVm0 = 0x0F70;    // vmcnt(0)
+
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations,
+// not for its global loads and stores in flight (which __syncthreads would
+// also wait for), with compiler fences so that no LDS access moves across it.
+__device__ __forceinline__ void pf_lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(kPfWaitLgkm0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Largest key limit over the 16 queries of a tile (every lane gets it; the same
+// in every wave of the workgroup, which holds the same queries).
+__device__ __forceinline__ int tile_limit(int n) {
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) n = max(n, __shfl_xor(n, m));
+    return n;
+}
+
+// Scores of one query tile against the workgroup's 256 keys into the LDS tile:
+// each wave writes its 16 x 64 part (lane holds keys wave*64 + 16*kt + 4*grp + r
+// of query col).
+__device__ __forceinline__ void score_tile(const bf16x8 (&kv)[4][8], const bf16x8 (&qv)[8],
                                            int wave, int lane, float (*tile)[kTileStride]) {
     const int col = lane & 15, grp = lane >> 4;
-    int nmax = n;
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) nmax = max(nmax, __shfl_xor(nmax, m));
-    if (nmax <= jg) {  // no query of the tile reaches the workgroup's keys
-        __syncthreads();
-        return;
-    }
     f32x4 c[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) c[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -97,16 +106,21 @@ __device__ __forceinline__ void score_tile(const PrefillArgs &a, const bf16x8 (&
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
             c[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv[kt][kb], qv[kb], c[kt], 0, 0, 0);
-    // lane holds keys wave*64 + 16*kt + 4*grp + r (r = 0..3) of query col
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
         *reinterpret_cast<f32x4 *>(&tile[col][wave * kPfWaveKeys + 16 * kt + 4 * grp]) = c[kt];
-    __syncthreads();
+}
+
+// Stores of a staged tile: each wave writes four whole rows (one 1 KiB row
+// segment per store instruction).  n: key limit of this lane's query of that
+// tile (lane rr holds query rr's).
+__device__ __forceinline__ void store_tile(const PrefillArgs &a, const float (*tile)[kTileStride],
+                                           int n, int b, int qt, int jg, int wave, int lane) {
     const int j0 = jg + 4 * lane;  // this lane's 4 keys of every row
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int rr = wave * 4 + i;
-        const int nr = __builtin_amdgcn_readlane(n, rr);  // lane rr holds query rr's limit
+        const int nr = __builtin_amdgcn_readlane(n, rr);
         if (j0 >= nr) continue;
         const f32x4 v = *reinterpret_cast<const f32x4 *>(&tile[rr][4 * lane]);
         float *dst = a.scores + ((size_t)b * a.n_q + qt * 16 + rr) * a.max_len + j0;
@@ -120,6 +134,16 @@ __device__ __forceinline__ void score_tile(const PrefillArgs &a, const bf16x8 (&
     }
 }
 
+// Workgroup: 256 keys of one sequence against all of its query tiles.  Per
+// tile qt, in this order: (a) wait for every global access issued so far --
+// the tile's queries (loaded one tile ahead) and the stores of tile qt-2,
+// issued a whole tile earlier; (b) store tile qt-1 from LDS; (c) load tile
+// qt+1's key limits and queries; (d) products of tile qt into LDS; (e) LDS-only
+// barrier.  Stores and loads both count in vmcnt and need not complete in
+// order with each other, so a wait for a load also waits for every store
+// before it; issuing a tile's stores only after the next tile's queries have
+// arrived keeps the stores' completion out of the wait.  Tiles whose rows all
+// end before the workgroup's first key (causal) compute and store nothing.
 template <bool PAGED, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int b = blockIdx.x / a.kblocks;
@@ -131,6 +155,7 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int jw = jg + wave * kPfWaveKeys;              // first key of this wave
     if (jg >= len) return;                               // uniform over the workgroup
     __shared__ float tile[2][16][kTileStride];
+    __shared__ __align__(16) uint16_t s_q[2][16][kQStride];  // query tiles (bf16)
 
     // the wave's 64 keys as A operands: key tile kt, row col = key jw + 16*kt + col
     bf16x8 kv[4][8];
@@ -148,28 +173,58 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
         for (int kb = 0; kb < 8; ++kb) kv[kt][kb] = load_bf16x8(a.k_idx + off + grp * 8 + kb * 32);
     }
 
-    // Tile qt+1's inputs (its queries' key limits, then its queries) are loaded
-    // before tile qt is computed.  The limit load is issued first: loads
-    // complete in order, so waiting for it must not wait for the queries.  The
-    // loop is unrolled by two so that both query buffers keep fixed registers.
     const int ntiles = div_up(a.n_q, 16);
     const int32_t *qpos = CAUSAL ? a.q_pos + (size_t)b * a.n_q : nullptr;
-    bf16x8 qa[8], qb[8];
-    int n_a = key_limit<CAUSAL>(qpos, len, a.n_q, col), n_b = 0;
-    load_queries(a, b, 0, col, grp, qa);
-    for (int qt = 0; qt < ntiles; qt += 2) {
-        if (qt + 1 < ntiles) {
-            n_b = key_limit<CAUSAL>(qpos, len, a.n_q, (qt + 1) * 16 + col);
-            load_queries(a, b, qt + 1, col, grp, qb);
+    // Query tiles go through LDS, each loaded once per workgroup: wave w loads
+    // queries 4w .. 4w+3 of a tile (lane: 32 bytes of query 4w + (lane >> 4)),
+    // a tile ahead, and writes them to s_q after the next wait.
+    const int sq_row = wave * 4 + (lane >> 4), sq_col = (lane & 15) * 16;
+    u32x4 qs[2];
+    auto load_quarter = [&](int qt) {
+        const int t = min(qt * 16 + sq_row, a.n_q - 1);  // rows past n_q: never stored
+        const uint16_t *p = a.q_idx + ((size_t)b * a.n_q + t) * kIdxDim + sq_col;
+        qs[0] = *reinterpret_cast<const u32x4 *>(p);
+        qs[1] = *reinterpret_cast<const u32x4 *>(p + 8);
+    };
+    auto stage_quarter = [&](int buf) {
+        *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col]) = qs[0];
+        *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col + 8]) = qs[1];
+    };
+    int p_cur = key_pos<CAUSAL>(qpos, a.n_q, col);  // raw positions, a tile ahead
+    load_quarter(0);
+    __builtin_amdgcn_s_waitcnt(kPfWaitVm0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    stage_quarter(0);
+    if (ntiles > 1) load_quarter(1);
+    pf_lds_barrier();
+    int n_prev = 0;       // key limits of the tile staged in LDS, not yet stored
+    bool staged = false;
+    for (int qt = 0; qt < ntiles; ++qt) {
+        int p_next = 0;
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(kPfWaitVm0);                         // (a)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_sched_barrier(0);
+        const int n_cur = key_limit<CAUSAL>(p_cur, len, a.n_q, qt * 16 + col);
+        if (qt + 1 < ntiles) stage_quarter((qt + 1) & 1);               // tile qt+1's queries
+        if (staged) store_tile(a, tile[(qt - 1) & 1], n_prev, b, qt - 1, jg, wave, lane);  // (b)
+        if (qt + 1 < ntiles) p_next = key_pos<CAUSAL>(qpos, a.n_q, (qt + 1) * 16 + col);  // (c)
+        if (qt + 2 < ntiles) load_quarter(qt + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        staged = tile_limit(n_cur) > jg;                                // uniform
+        if (staged) {                                                   // (d)
+            bf16x8 qv[8];
+#pragma unroll
+            for (int kb = 0; kb < 8; ++kb)
+                qv[kb] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4 *>(&s_q[qt & 1][col][kb * 32 + grp * 8]));
+            score_tile(kv, qv, wave, lane, tile[qt & 1]);
         }
-        score_tile(a, kv, qa, n_a, b, qt, jg, wave, lane, tile[0]);
-        if (qt + 1 >= ntiles) break;
-        if (qt + 2 < ntiles) {
-            n_a = key_limit<CAUSAL>(qpos, len, a.n_q, (qt + 2) * 16 + col);
-            load_queries(a, b, qt + 2, col, grp, qa);
-        }
-        score_tile(a, kv, qb, n_b, b, qt + 1, jg, wave, lane, tile[1]);
+        n_prev = n_cur;
+        p_cur = p_next;
+        pf_lds_barrier();                                               // (e)
     }
+    if (staged) store_tile(a, tile[(ntiles - 1) & 1], n_prev, b, ntiles - 1, jg, wave, lane);
 }
 
 bool index_uses_mfma(const Geometry &g) { return g.n_q >= kPrefillMinRows; }
