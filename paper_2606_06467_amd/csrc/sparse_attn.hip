@@ -33,11 +33,15 @@
 
 namespace clsa {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kHeadDim = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kMaxSplits = 128;  // splits per (row, KV head): the merge's largest shape
 constexpr int kManyUnits = 4096; // (row, KV head) units from which splits go by key range
+constexpr int kKtPitch = 17;     // 16-byte pieces per staged K row (one of padding)
 constexpr int kManySplits = 8;   // splits per unit then (measured best of 1, 2, 4, 8, 16)
 
 // The fields every workgroup reads first come first: the kernel's prologue
@@ -75,7 +79,7 @@ __device__ __forceinline__ int row_keys(const AttnArgs &a, int row) {
     return min(max(a.n_sel[row], 0), a.top_k);
 }
 
-template <int G, bool PAGED, bool DENSE>
+template <int G, bool PAGED, bool DENSE, bool MQK>
 __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
     constexpr int NO = pow2_at_least(8 * G);   // accumulators per lane before the reduction
@@ -83,6 +87,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     __shared__ float s_scale[G];               // per-head rescale factor of this chunk
     __shared__ float s_ml[G][2];               // running max (log2 domain) and denominator
     __shared__ float red[4][G * kHeadDim];     // cross-wave reduction of the accumulators
+    // MQK: per wave, its 16 gathered K rows (16 x 16 pieces of 16 bytes, padded)
+    __shared__ __align__(16) u32x4 s_kt[MQK ? 4 : 1][MQK ? 16 : 1][MQK ? kKtPitch : 1];
 
     // flattened grid, few (row, KV head) units: (row * kv_heads + g) * splits + split;
     // many units (kManyUnits or more): split * units + (row * kv_heads + g), so that
@@ -124,11 +130,22 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     if (split >= nsplit) return;  // uniform; the merge masks splits past the last one
     const int tok_end = min(n, tok_begin + span);
 
-    uint4 qv[G];
+    uint4 qv[MQK ? 1 : G];
+    bf16x8 qb[4];  // MQK: B operands, Q^T (32 dims x 16 head columns, heads >= G zero)
+    if (!MQK) {
 #pragma unroll
-    for (int h = 0; h < G; ++h)
-        qv[h] = *reinterpret_cast<const uint4 *>(a.q + ((size_t)row * Hq + g * G + h) * kHeadDim +
-                                                 sub * 8);
+        for (int h = 0; h < G; ++h)
+            qv[h] = *reinterpret_cast<const uint4 *>(
+                a.q + ((size_t)row * Hq + g * G + h) * kHeadDim + sub * 8);
+    } else {
+        const int hq = min(sub, G - 1);
+        const uint16_t *qp = a.q + ((size_t)row * Hq + g * G + hq) * kHeadDim + qq * 8;
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(qp + 32 * s4);
+            qb[s4] = __builtin_bit_cast(bf16x8, sub < G ? v : u32x4{0u, 0u, 0u, 0u});
+        }
+    }
     if (tid < G) {
         s_ml[tid][0] = -INFINITY;
         s_ml[tid][1] = 0.0f;
@@ -170,25 +187,50 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         // this the scheduler sinks the V loads below the logits, which costs a
         // second memory round trip per chunk).
         __builtin_amdgcn_sched_barrier(0);
-        // logits: value index i*G + h, transpose-reduced over the 16 lanes of the quarter
-        float p[NV];
+        if (MQK) {
+            // Logits on the matrix cores: C = K_w (16 tokens x 128) x Q^T (128 x 16
+            // head columns).  The wave's 16 K rows (gathered as above: token slot
+            // r = 4i + qq is chunk token 16i + 4w + qq) go through this wave's LDS
+            // rows to reach the operand layout: lane (qq, sub) supplies slot sub,
+            // dims 8qq + 32s of step s, and receives slots 4qq + r of head sub.
+            u32x4 *sk = &s_kt[wave][0][0];
 #pragma unroll
-        for (int v = 0; v < NV; ++v) p[v] = 0.0f;
+            for (int i = 0; i < 4; ++i)
+                sk[(i * 4 + qq) * kKtPitch + sub] = u32x4{kr[i].x, kr[i].y, kr[i].z, kr[i].w};
+            f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const bf16x8 ka = __builtin_bit_cast(bf16x8, sk[sub * kKtPitch + qq + 4 * s4]);
+                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[s4], c, 0, 0, 0);
+            }
+            if (sub < G) {
 #pragma unroll
-            for (int h = 0; h < G; ++h) p[i * G + h] = dot8_bf16(kr[i], qv[h], 0.0f);
-        transpose_reduce<NV, 8, 1, NV>(p, sub);
-        // lane `sub` now holds value indices [sub*NV/16, sub*NV/16 + NV/16) (NV >= 16)
-        // or index sub / (16/NV) (NV < 16).
-        constexpr int PER = NV >= 16 ? NV / 16 : 1;
+                for (int r = 0; r < 4; ++r) {
+                    const int tl = qq * 16 + wave * 4 + r;  // slot 4qq + r
+                    zs[sub][tl] = c0 + tl < tok_end ? c[r] * a.scale_log2 : -INFINITY;
+                }
+            }
+        } else {
+            // logits: value index i*G + h, transpose-reduced over the 16 lanes of the quarter
+            float p[NV];
 #pragma unroll
-        for (int v = 0; v < PER; ++v) {
-            const int orig = NV >= 16 ? sub * PER + v : sub / (16 / NV);
-            if (orig < 4 * G) {
-                const int i = orig / G, h = orig - i * G;
-                const int tl = i * 16 + wave * 4 + qq;
-                zs[h][tl] = c0 + tl < tok_end ? p[v] * a.scale_log2 : -INFINITY;
+            for (int v = 0; v < NV; ++v) p[v] = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int h = 0; h < G; ++h) p[i * G + h] = dot8_bf16(kr[i], qv[h], 0.0f);
+            transpose_reduce<NV, 8, 1, NV>(p, sub);
+            // lane `sub` now holds value indices [sub*NV/16, sub*NV/16 + NV/16) (NV >= 16)
+            // or index sub / (16/NV) (NV < 16).
+            constexpr int PER = NV >= 16 ? NV / 16 : 1;
+#pragma unroll
+            for (int v = 0; v < PER; ++v) {
+                const int orig = NV >= 16 ? sub * PER + v : sub / (16 / NV);
+                if (orig < 4 * G) {
+                    const int i = orig / G, h = orig - i * G;
+                    const int tl = i * 16 + wave * 4 + qq;
+                    zs[h][tl] = c0 + tl < tok_end ? p[v] * a.scale_log2 : -INFINITY;
+                }
             }
         }
         __syncthreads();
@@ -378,8 +420,14 @@ size_t attn_partial_floats(const Geometry &g, bool dense) {
 template <int G, bool DENSE>
 static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int units,
                                 hipStream_t stream, hipEvent_t split_done) {
-    if (paged) sparse_attn_kernel<G, true, DENSE><<<grid, dim3(256), 0, stream>>>(a);
-    else sparse_attn_kernel<G, false, DENSE><<<grid, dim3(256), 0, stream>>>(a);
+    // Many units (chunked prefill): logits on the matrix cores.  The grids of
+    // decode (few units, latency-bound) keep the vector-unit logits, which were
+    // measured faster there.
+    const bool mqk = grid.x / a.splits >= (unsigned)kManyUnits;
+    if (paged && mqk) sparse_attn_kernel<G, true, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
+    else if (paged) sparse_attn_kernel<G, true, DENSE, false><<<grid, dim3(256), 0, stream>>>(a);
+    else if (mqk) sparse_attn_kernel<G, false, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false, DENSE, false><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1) return e;
