@@ -13,7 +13,9 @@
 //   * the G query heads of the GQA group share those rows: each lane dots its
 //     8 key values with the matching 8 values of every head (v_dot2_f32_bf16),
 //     a transpose-reduction over the 16 lanes leaves one (head, token) logit
-//     per lane, and the logits go to LDS;
+//     per lane, and the logits go to LDS.  With thousands of units (chunked
+//     prefill, where the kernel is bound by its vector instructions) the
+//     logits come from the matrix cores instead (MQK);
 //   * one wave per head takes the chunk maximum and sum (base-2 exponentials),
 //     updates the running max / denominator and rescales its accumulators
 //     (online softmax), so a split of any length needs one pass;
