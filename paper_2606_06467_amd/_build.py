@@ -26,9 +26,13 @@ COMMON_FLAGS = [
 ]
 
 
-# Per-source flags.  kd.hip: matrix-core results in ordinary VGPRs (no
-# accumulator-register copies before the exponentials that consume them).
-SOURCE_FLAGS = {"kd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# Per-source flags: matrix-core results in ordinary VGPRs.  kd.hip: no
+# accumulator-register copies before the exponentials that consume them;
+# sparse_attn.hip: the chunked-prefill (matrix-core logits) form of the paged
+# layer kernel fits four waves per SIMD (the decode forms, which use no matrix
+# instructions, compile to the same code either way).
+SOURCE_FLAGS = {"kd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+                "sparse_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:
