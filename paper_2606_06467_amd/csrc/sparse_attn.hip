@@ -259,19 +259,31 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
         }
+        // weight x V with the lane's tokens in pairs (rounds 0, 1 and 2, 3): bf16
+        // weights and values into v_dot2_f32_bf16, fp32 accumulation
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int tl = i * 16 + wave * 4 + qq;
-            float vf[8];
-            vf[0] = bf16_lo(vr[i].x); vf[1] = bf16_hi(vr[i].x);
-            vf[2] = bf16_lo(vr[i].y); vf[3] = bf16_hi(vr[i].y);
-            vf[4] = bf16_lo(vr[i].z); vf[5] = bf16_hi(vr[i].z);
-            vf[6] = bf16_lo(vr[i].w); vf[7] = bf16_hi(vr[i].w);
+        for (int pr = 0; pr < 2; ++pr) {
+            const int tla = (2 * pr) * 16 + wave * 4 + qq, tlb = tla + 16;
+            bf16x2 wp[G];
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float w = zs[h][tl];  // 0 for positions past the end
+            for (int h = 0; h < G; ++h)  // 0 for positions past the end
+                wp[h] = bf16x2{(__bf16)zs[h][tla], (__bf16)zs[h][tlb]};
+            const uint32_t va[4] = {vr[2 * pr].x, vr[2 * pr].y, vr[2 * pr].z, vr[2 * pr].w};
+            const uint32_t vb[4] = {vr[2 * pr + 1].x, vr[2 * pr + 1].y, vr[2 * pr + 1].z,
+                                    vr[2 * pr + 1].w};
 #pragma unroll
-                for (int d = 0; d < 8; ++d) acc[h][d] = fmaf(w, vf[d], acc[h][d]);
+            for (int c2 = 0; c2 < 4; ++c2) {
+                // dims 2c2 and 2c2+1 of both tokens: {va.lo, vb.lo} and {va.hi, vb.hi}
+                const bf16x2 lo =
+                    __builtin_bit_cast(bf16x2, __builtin_amdgcn_perm(vb[c2], va[c2], 0x05040100u));
+                const bf16x2 hi =
+                    __builtin_bit_cast(bf16x2, __builtin_amdgcn_perm(vb[c2], va[c2], 0x07060302u));
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    acc[h][2 * c2] = __builtin_amdgcn_fdot2_f32_bf16(wp[h], lo, acc[h][2 * c2], false);
+                    acc[h][2 * c2 + 1] =
+                        __builtin_amdgcn_fdot2_f32_bf16(wp[h], hi, acc[h][2 * c2 + 1], false);
+                }
             }
         }
         __syncthreads();  // zs / s_scale are rewritten by the next chunk
