@@ -62,7 +62,10 @@
  * Supported shapes (CLSA_ERR_UNSUPPORTED otherwise; there is no fallback):
  *   idx_heads * idx_dim == 256, head_dim == 128,
  *   q_heads / kv_heads in {1, 2, 4, 5, 8}, 1 <= top_k <= 8192,
- *   max_len <= 262144, page_size 0 or a power of two in [16, 4096].
+ *   max_len <= 262144, page_size 0 or a power of two in [16, 4096];
+ *   contiguous key/value caches (page_size 0): one sequence's cache below
+ *   4 GiB, i.e. max_len * kv_heads * 256 bytes < 2^32 (the attention kernels
+ *   address it with 32-bit offsets; the paged layout has no such limit).
  */
 #ifndef CLSA_H
 #define CLSA_H

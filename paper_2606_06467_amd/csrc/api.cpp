@@ -52,6 +52,10 @@ clsa_status check_shape(const clsa_shape *s, unsigned needs, Geometry *g) {
     }
     if ((needs & kAttn) && !isfinite(s->softmax_scale)) return CLSA_ERR_INVALID_ARG;
     if ((needs & kAttn) && s->q_heads % s->kv_heads != 0) return CLSA_ERR_INVALID_ARG;
+    // contiguous caches: one sequence's K (or V) cache is addressed with 32-bit offsets
+    if ((needs & kAttn) && s->page_size == 0 &&
+        (int64_t)s->max_len * s->kv_heads * 256 >= ((int64_t)1 << 32))
+        return CLSA_ERR_UNSUPPORTED;
     if ((needs & kIndex) && s->idx_heads * s->idx_dim != 256) return CLSA_ERR_UNSUPPORTED;
     if (needs & kAttn) {
         const int grp = s->q_heads / s->kv_heads;

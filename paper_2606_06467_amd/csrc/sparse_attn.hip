@@ -81,6 +81,13 @@ __device__ __forceinline__ int row_keys(const AttnArgs &a, int row) {
     return min(max(a.n_sel[row], 0), a.top_k);
 }
 
+// Index entry `pos` of a row's list: a 32-bit byte offset from the list's base
+// (uniform over the workgroup), so that the load takes the scalar-base form.
+__device__ __forceinline__ int sel_at(const int32_t *sel, int pos) {
+    return *reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(sel) +
+                                              (uint32_t)pos * 4u);
+}
+
 template <int G, bool PAGED, bool DENSE, bool MQK>
 __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
@@ -109,6 +116,10 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     const int span = a.chunks_per_split * 64;
     const int tok_begin = split * span;
     const int row_elems = a.kv_heads * kHeadDim;
+    const char *kseq = reinterpret_cast<const char *>(
+        a.k + ((size_t)b * a.max_len * a.kv_heads + g) * kHeadDim);
+    const char *vseq = reinterpret_cast<const char *>(
+        a.v + ((size_t)b * a.max_len * a.kv_heads + g) * kHeadDim);
     const int32_t *sel = DENSE ? nullptr : a.idx + (size_t)row * a.top_k;
 
     // Index loads of the first chunk do not wait for n_sel: the index list has
@@ -117,7 +128,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
         jpre[i] = DENSE ? tok_begin + i * 16 + wave * 4 + qq
-                        : sel[min(tok_begin + i * 16 + wave * 4 + qq, a.top_k - 1)];
+                        : sel_at(sel, min(tok_begin + i * 16 + wave * 4 + qq, a.top_k - 1));
     const int n = row_keys<DENSE>(a, row);
     const int nsplit = div_up(n, span);  // splits that hold tokens
 
@@ -170,21 +181,33 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
                 const int page = a.page_table[(size_t)b * a.max_pages + (jr[i] >> a.page_shift)];
                 trow[i] = ((uint32_t)page << a.page_shift) + (jr[i] & ((1 << a.page_shift) - 1));
             } else {
-                trow[i] = (uint32_t)b * a.max_len + jr[i];
+                trow[i] = 0;  // unused: contiguous caches use byte offsets from kseq / vseq
             }
         }
         uint4 kr[4], vr[4];
+        if (PAGED) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const size_t off = (size_t)trow[i] * row_elems + (size_t)g * kHeadDim + sub * 8;
-            kr[i] = *reinterpret_cast<const uint4 *>(a.k + off);
-            vr[i] = *reinterpret_cast<const uint4 *>(a.v + off);
+            for (int i = 0; i < 4; ++i) {
+                const size_t off = (size_t)trow[i] * row_elems + (size_t)g * kHeadDim + sub * 8;
+                kr[i] = *reinterpret_cast<const uint4 *>(a.k + off);
+                vr[i] = *reinterpret_cast<const uint4 *>(a.v + off);
+            }
+        } else {
+            // contiguous caches: a 32-bit byte offset inside the row's sequence
+            // (one sequence's cache is below 4 GiB, checked at the boundary) from
+            // a base that is the same for the whole workgroup
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t off = (uint32_t)jr[i] * (uint32_t)(row_elems * 2) + (uint32_t)(sub * 16);
+                kr[i] = *reinterpret_cast<const uint4 *>(kseq + off);
+                vr[i] = *reinterpret_cast<const uint4 *>(vseq + off);
+            }
         }
         // prefetch the next chunk's indices (clamped, so always readable)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             jpre[i] = DENSE ? c0 + 64 + i * 16 + wave * 4 + qq
-                            : sel[min(c0 + 64 + i * 16 + wave * 4 + qq, a.top_k - 1)];
+                            : sel_at(sel, min(c0 + 64 + i * 16 + wave * 4 + qq, a.top_k - 1));
         // All K and V gathers of the chunk are in flight before any math (without
         // this the scheduler sinks the V loads below the logits, which costs a
         // second memory round trip per chunk).

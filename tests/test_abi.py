@@ -124,6 +124,9 @@ def test_index_rejects_bad_pointers(lib):
     (dict(head_dim=64), -2), (dict(q_heads=32, kv_heads=5), -1), (dict(q_heads=48, kv_heads=8), -2),
     (dict(q_heads=20, kv_heads=4), None), (dict(softmax_scale=float("nan")), -1),
     (dict(softmax_scale=float("inf")), -1),
+    # one contiguous sequence's cache of 4 GiB: beyond the 32-bit offsets
+    (dict(max_len=262144, q_heads=64, kv_heads=64), -2),
+    (dict(max_len=262143, q_heads=64, kv_heads=64), None),
 ])
 def test_attn_rejects_bad_shapes(lib, kw, code):
     from paper_2606_06467_amd import binding as B
