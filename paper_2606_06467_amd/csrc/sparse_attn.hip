@@ -81,6 +81,20 @@ __device__ __forceinline__ int row_keys(const AttnArgs &a, int row) {
     return min(max(a.n_sel[row], 0), a.top_k);
 }
 
+// Maximum / sum over the four rows (lanes l, l ^ 16, l ^ 32, l ^ 48) of a wave.
+__device__ __forceinline__ float rows4_max(float x) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float rows4_sum(float x) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Index entry `pos` of a row's list: a 32-bit byte offset from the list's base
 // (uniform over the workgroup), so that the load takes the scalar-base form.
 __device__ __forceinline__ int sel_at(const int32_t *sel, int pos) {
@@ -98,6 +112,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     __shared__ float red[4][G * kHeadDim];     // cross-wave reduction of the accumulators
     // MQK: per wave, its 16 gathered K rows (16 x 16 pieces of 16 bytes, padded)
     __shared__ __align__(16) u32x4 s_kt[MQK ? 4 : 1][MQK ? 16 : 1][MQK ? kKtPitch : 1];
+    __shared__ __align__(16) float zw[MQK ? 4 : 1][MQK ? G : 1][16];  // MQK: weights per wave
+    __shared__ float s_wml[MQK ? 4 : 1][G][2];  // MQK: each wave's (max, sum) per head
 
     // flattened grid, few (row, KV head) units: (row * kv_heads + g) * splits + split;
     // many units (kManyUnits or more): split * units + (row * kv_heads + g), so that
@@ -168,6 +184,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.0f;
+    float m_run = -INFINITY, l_run = 0.0f;  // MQK: head sub's running max / sum (this wave)
 
     for (int c0 = tok_begin; c0 < tok_end; c0 += 64) {
         int jr[4];
@@ -212,6 +229,36 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         // this the scheduler sinks the V loads below the logits, which costs a
         // second memory round trip per chunk).
         __builtin_amdgcn_sched_barrier(0);
+        // weight x V with the lane's tokens in pairs (rounds 0, 1 and 2, 3): bf16
+        // weights and values into v_dot2_f32_bf16, fp32 accumulation.  weight(h, i):
+        // the weight of head h for this lane's round-i token (0 past the end).
+        auto weighted_v = [&](auto weight) {
+#pragma unroll
+            for (int pr = 0; pr < 2; ++pr) {
+                bf16x2 wp[G];
+#pragma unroll
+                for (int h = 0; h < G; ++h)
+                    wp[h] = bf16x2{(__bf16)weight(h, 2 * pr), (__bf16)weight(h, 2 * pr + 1)};
+                const uint32_t va[4] = {vr[2 * pr].x, vr[2 * pr].y, vr[2 * pr].z, vr[2 * pr].w};
+                const uint32_t vb[4] = {vr[2 * pr + 1].x, vr[2 * pr + 1].y, vr[2 * pr + 1].z,
+                                        vr[2 * pr + 1].w};
+#pragma unroll
+                for (int c2 = 0; c2 < 4; ++c2) {
+                    // dims 2c2 and 2c2+1 of both tokens: {va.lo, vb.lo} and {va.hi, vb.hi}
+                    const bf16x2 lo = __builtin_bit_cast(
+                        bf16x2, __builtin_amdgcn_perm(vb[c2], va[c2], 0x05040100u));
+                    const bf16x2 hi = __builtin_bit_cast(
+                        bf16x2, __builtin_amdgcn_perm(vb[c2], va[c2], 0x07060302u));
+#pragma unroll
+                    for (int h = 0; h < G; ++h) {
+                        acc[h][2 * c2] =
+                            __builtin_amdgcn_fdot2_f32_bf16(wp[h], lo, acc[h][2 * c2], false);
+                        acc[h][2 * c2 + 1] =
+                            __builtin_amdgcn_fdot2_f32_bf16(wp[h], hi, acc[h][2 * c2 + 1], false);
+                    }
+                }
+            }
+        };
         if (MQK) {
             // Logits on the matrix cores: C = K_w (16 tokens x 128) x Q^T (128 x 16
             // head columns).  The wave's 16 K rows (gathered as above: token slot
@@ -228,13 +275,36 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
                 const bf16x8 ka = __builtin_bit_cast(bf16x8, sk[sub * kKtPitch + qq + 4 * s4]);
                 c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[s4], c, 0, 0, 0);
             }
-            if (sub < G) {
+            // Online softmax per wave over its own 16 slots (no workgroup barrier):
+            // lane (qq, sub) keeps the running maximum and sum of head sub; the
+            // four lanes of a head (one per row) combine with permlane swaps.
+            float z[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int tl = qq * 16 + wave * 4 + r;  // slot 4qq + r
-                    zs[sub][tl] = c0 + tl < tok_end ? c[r] * a.scale_log2 : -INFINITY;
-                }
+            for (int r = 0; r < 4; ++r) {
+                const int tl = qq * 16 + wave * 4 + r;  // slot 4qq + r
+                z[r] = sub < G && c0 + tl < tok_end ? c[r] * a.scale_log2 : -INFINITY;
             }
+            const float mx = rows4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
+            const float m_new = fmaxf(m_run, mx);
+            const float base = m_new == -INFINITY ? 0.0f : m_new;  // no valid slot yet
+            float w[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) w[r] = __builtin_amdgcn_exp2f(z[r] - base);  // -inf -> 0
+            const float scl = __builtin_amdgcn_exp2f(m_run - base);  // m_run = -inf -> 0
+            l_run = l_run * scl + rows4_sum((w[0] + w[1]) + (w[2] + w[3]));
+            m_run = m_new;
+            if (sub < G)
+                *reinterpret_cast<float4 *>(&zw[wave][sub][4 * qq]) = make_float4(w[0], w[1], w[2], w[3]);
+            // head h's rescale factor is held by lane h (row 0)
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const float sc = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, scl), h));
+#pragma unroll
+                for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
+            }
+            // this lane's tokens 16i + 4w + qq are slots 4i + qq of the wave
+            weighted_v([&](int h, int i) { return zw[wave][h][4 * i + qq]; });
         } else {
             // logits: value index i*G + h, transpose-reduced over the 16 lanes of the quarter
             float p[NV];
@@ -258,6 +328,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
                 }
             }
         }
+        if (!MQK) {
         __syncthreads();
         // per-head chunk statistics and online-softmax update
         for (int h = wave; h < G; h += 4) {
@@ -282,34 +353,9 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
         }
-        // weight x V with the lane's tokens in pairs (rounds 0, 1 and 2, 3): bf16
-        // weights and values into v_dot2_f32_bf16, fp32 accumulation
-#pragma unroll
-        for (int pr = 0; pr < 2; ++pr) {
-            const int tla = (2 * pr) * 16 + wave * 4 + qq, tlb = tla + 16;
-            bf16x2 wp[G];
-#pragma unroll
-            for (int h = 0; h < G; ++h)  // 0 for positions past the end
-                wp[h] = bf16x2{(__bf16)zs[h][tla], (__bf16)zs[h][tlb]};
-            const uint32_t va[4] = {vr[2 * pr].x, vr[2 * pr].y, vr[2 * pr].z, vr[2 * pr].w};
-            const uint32_t vb[4] = {vr[2 * pr + 1].x, vr[2 * pr + 1].y, vr[2 * pr + 1].z,
-                                    vr[2 * pr + 1].w};
-#pragma unroll
-            for (int c2 = 0; c2 < 4; ++c2) {
-                // dims 2c2 and 2c2+1 of both tokens: {va.lo, vb.lo} and {va.hi, vb.hi}
-                const bf16x2 lo =
-                    __builtin_bit_cast(bf16x2, __builtin_amdgcn_perm(vb[c2], va[c2], 0x05040100u));
-                const bf16x2 hi =
-                    __builtin_bit_cast(bf16x2, __builtin_amdgcn_perm(vb[c2], va[c2], 0x07060302u));
-#pragma unroll
-                for (int h = 0; h < G; ++h) {
-                    acc[h][2 * c2] = __builtin_amdgcn_fdot2_f32_bf16(wp[h], lo, acc[h][2 * c2], false);
-                    acc[h][2 * c2 + 1] =
-                        __builtin_amdgcn_fdot2_f32_bf16(wp[h], hi, acc[h][2 * c2 + 1], false);
-                }
-            }
-        }
+        weighted_v([&](int h, int i) { return zs[h][i * 16 + wave * 4 + qq]; });
         __syncthreads();  // zs / s_scale are rewritten by the next chunk
+        }
     }
 
     // ---- reduce the accumulators over the 4 quarters of each wave (lanes ^16, ^32) ----
@@ -330,27 +376,53 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             red[wave][h * kHeadDim + sub * 8 + d] = o[v];
         }
     }
+    if (MQK && qq == 0 && sub < G) {  // this wave's (max, sum) of head sub
+        s_wml[wave][sub][0] = m_run;
+        s_wml[wave][sub][1] = l_run;
+    }
     __syncthreads();
+    // (max, sum, weighted V) of head h over the workgroup: with per-wave softmax
+    // states (MQK) the four waves combine by the log-sum-exp rule
+    auto combine = [&](int h, int e, float &m, float &l, float &sum) {
+        if (MQK) {
+            m = fmaxf(fmaxf(s_wml[0][h][0], s_wml[1][h][0]), fmaxf(s_wml[2][h][0], s_wml[3][h][0]));
+            l = 0.0f;
+            sum = 0.0f;
+#pragma unroll
+            for (int w4 = 0; w4 < 4; ++w4) {
+                const float mw = s_wml[w4][h][0];
+                const float f = mw == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mw - m);
+                l = fmaf(f, s_wml[w4][h][1], l);
+                sum = fmaf(f, red[w4][e], sum);
+            }
+        } else {
+            m = s_ml[h][0];
+            l = s_ml[h][1];
+            sum = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+        }
+    };
     if (a.splits == 1) {
         for (int e = tid; e < G * kHeadDim; e += 256) {
             const int h = e / kHeadDim, dim = e - h * kHeadDim;
-            const float sum = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+            float m, l, sum;
+            combine(h, e, m, l, sum);
             const int hq = g * G + h;
-            const float l = s_ml[h][1];
             a.out[((size_t)row * Hq + hq) * kHeadDim + dim] =
                 (uint16_t)f32_to_bf16_bits(sum / l);
-            if (a.lse && dim == 0) a.lse[(size_t)row * Hq + hq] = (s_ml[h][0] + log2f(l)) * kLn2;
+            if (a.lse && dim == 0) a.lse[(size_t)row * Hq + hq] = (m + log2f(l)) * kLn2;
         }
         return;
     }
     const size_t base = ((size_t)row * Hq + g * G) * a.splits;  // slot of (head g*G, split 0)
     for (int e = tid; e < G * kHeadDim; e += 256) {
         const int h = e / kHeadDim, dim = e - h * kHeadDim;
+        float m, l, sum;
+        combine(h, e, m, l, sum);
         const size_t slot = base + (size_t)h * a.splits + split;
-        a.part_o[slot * kHeadDim + dim] = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+        a.part_o[slot * kHeadDim + dim] = sum;
         if (dim == 0) {
-            a.part_ml[slot * 2] = s_ml[h][0];
-            a.part_ml[slot * 2 + 1] = s_ml[h][1];
+            a.part_ml[slot * 2] = m;
+            a.part_ml[slot * 2 + 1] = l;
         }
     }
 }

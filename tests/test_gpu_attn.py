@@ -83,6 +83,19 @@ def test_many_rows_split_by_key_range():
     _case(w, 5, what="520 rows x 8 KV heads, split by key range")
 
 
+@pytest.mark.parametrize("qh,kvh,nq,k,ps", [(16, 4, 1030, 256, 0), (16, 2, 2050, 128, 64),
+                                            (20, 4, 1030, 320, 64)])
+def test_matrix_core_logits_form(qh, kvh, nq, k, ps):
+    """Over 4096 (row, KV head) units the logits run on the matrix cores and each
+    wave keeps its own softmax state: groups of 4, 8 and 5 heads, one split
+    (k = 128) and several, contiguous and paged, ragged counts (0, 1, 37, 63, 65)."""
+    w = inputs.small_workload(batch=1, lens=(4000,), n_q=nq, causal=True, q_pos0=(4000 - nq,),
+                              top_k=k, q_heads=qh, kv_heads=kvh, page_size=ps, n_layers=1,
+                              wid=88)
+    _case(w, 9, nsel_override={(0, 3): 37, (0, 5): 1, (0, 7): 0, (0, 8): 63, (0, 9): 65},
+          what=f"matrix-core form Hq={qh} Hkv={kvh} rows={nq} k={k} page={ps}")
+
+
 def test_paged():
     w = inputs.small_workload(batch=3, lens=(3000, 64, 5000), top_k=512, page_size=64, n_layers=1,
                               wid=85)
