@@ -10,15 +10,22 @@
 //     are each issued as one unconditional batch (positions past the end are
 //     clamped and masked afterwards), so a workgroup waits for memory about
 //     three times instead of once per token;
-//   * the G query heads of the GQA group share those rows: each lane dots its
-//     8 key values with the matching 8 values of every head (v_dot2_f32_bf16),
-//     a transpose-reduction over the 16 lanes leaves one (head, token) logit
-//     per lane, and the logits go to LDS.  With thousands of units (chunked
-//     prefill, where the kernel is bound by its vector instructions) the
-//     logits come from the matrix cores instead (MQK);
-//   * one wave per head takes the chunk maximum and sum (base-2 exponentials),
-//     updates the running max / denominator and rescales its accumulators
-//     (online softmax), so a split of any length needs one pass;
+//   * the G query heads of the GQA group share those rows.  Two forms:
+//     - matrix-core form (MQK; contiguous caches, and chunked prefill with
+//       thousands of units): each wave's 16 K rows go through its own LDS rows
+//       into v_mfma_f32_16x16x32_bf16 against Q^T (heads padded to 16), and
+//       each wave keeps its own online softmax per head (base-2 exponentials;
+//       the four lanes of a head combine with permlane swaps), passes the
+//       weights to the lanes holding the matching V rows through its LDS rows
+//       and keeps its own weighted-V accumulators: no workgroup barrier per
+//       chunk; the four wave states are merged by the log-sum-exp rule at the end;
+//     - vector form (paged decode grids): each lane dots its 8 key values with
+//       the matching 8 values of every head (v_dot2_f32_bf16), a
+//       transpose-reduction over the 16 lanes leaves one (head, token) logit
+//       per lane, the logits go to LDS, and one wave per head takes the chunk
+//       maximum and sum, updates the running max / denominator and rescales
+//       (online softmax, shared by the workgroup);
+//     so a split of any length needs one pass;
 //   * each lane accumulates weight x V for its 8 dimensions and G heads.
 // The accumulators are then reduced over lanes and waves in LDS.  With one
 // split the workgroup writes the bf16 output and lse itself.  Otherwise it
@@ -529,14 +536,13 @@ size_t attn_partial_floats(const Geometry &g, bool dense) {
 template <int G, bool DENSE>
 static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int units,
                                 hipStream_t stream, hipEvent_t split_done) {
-    // Many units (chunked prefill): logits on the matrix cores.  The grids of
-    // decode (few units, latency-bound) keep the vector-unit logits, which were
-    // measured faster there.
-    const bool mqk = grid.x / a.splits >= (unsigned)kManyUnits;
+    // Logits on the matrix cores with per-wave softmax states for contiguous
+    // caches and for many units (chunked prefill); paged decode grids keep the
+    // vector-unit logits and the shared softmax, which measured faster there.
+    const bool mqk = !paged || grid.x / a.splits >= (unsigned)kManyUnits;
     if (paged && mqk) sparse_attn_kernel<G, true, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
     else if (paged) sparse_attn_kernel<G, true, DENSE, false><<<grid, dim3(256), 0, stream>>>(a);
-    else if (mqk) sparse_attn_kernel<G, false, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
-    else sparse_attn_kernel<G, false, DENSE, false><<<grid, dim3(256), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1) return e;
