@@ -44,6 +44,8 @@ namespace clsa {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kHeadDim = 128;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -109,17 +111,19 @@ __device__ __forceinline__ int sel_at(const int32_t *sel, int pos) {
                                               (uint32_t)pos * 4u);
 }
 
-template <int G, bool PAGED, bool DENSE, bool MQK>
+// MQK: matrix-core logits with per-wave softmax states; PVM (with MQK): the
+// weighted V on the matrix cores as well.
+template <int G, bool PAGED, bool DENSE, bool MQK, bool PVM>
 __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
     constexpr int NO = pow2_at_least(8 * G);   // accumulators per lane before the reduction
     __shared__ float zs[G][64];                // logits -> weights of the current chunk
     __shared__ float s_scale[G];               // per-head rescale factor of this chunk
     __shared__ float s_ml[G][2];               // running max (log2 domain) and denominator
-    __shared__ float red[4][G * kHeadDim];     // cross-wave reduction of the accumulators
+    __shared__ __align__(16) float red[4][G * kHeadDim];  // cross-wave reduction of the accumulators
     // MQK: per wave, its 16 gathered K rows (16 x 16 pieces of 16 bytes, padded)
     __shared__ __align__(16) u32x4 s_kt[MQK ? 4 : 1][MQK ? 16 : 1][MQK ? kKtPitch : 1];
-    __shared__ __align__(16) float zw[MQK ? 4 : 1][MQK ? G : 1][16];  // MQK: weights per wave
+    __shared__ __align__(16) float zw[MQK && !PVM ? 4 : 1][MQK && !PVM ? G : 1][16];  // MQK: weights per wave
     __shared__ float s_wml[MQK ? 4 : 1][G][2];  // MQK: each wave's (max, sum) per head
 
     // flattened grid, few (row, KV head) units: (row * kv_heads + g) * splits + split;
@@ -192,6 +196,10 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.0f;
     float m_run = -INFINITY, l_run = 0.0f;  // MQK: head sub's running max / sum (this wave)
+    // PVM: weighted V per 16-dim block blk, lane (qq, sub): heads 4qq + r, dim 8sub + blk
+    f32x4 pacc[PVM ? 8 : 1];
+#pragma unroll
+    for (int i = 0; i < (PVM ? 8 : 1); ++i) pacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int c0 = tok_begin; c0 < tok_end; c0 += 64) {
         int jr[4];
@@ -270,8 +278,10 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             // Logits on the matrix cores: C = K_w (16 tokens x 128) x Q^T (128 x 16
             // head columns).  The wave's 16 K rows (gathered as above: token slot
             // r = 4i + qq is chunk token 16i + 4w + qq) go through this wave's LDS
-            // rows to reach the operand layout: lane (qq, sub) supplies slot sub,
-            // dims 8qq + 32s of step s, and receives slots 4qq + r of head sub.
+            // rows to reach the operand layout: lane (qq, sub) supplies A row sub,
+            // dims 8qq + 32s of step s, and receives C rows 4qq + r of head sub.
+            // A row m holds slot m, or with PVM slot 4(m & 3) + (m >> 2), so that
+            // C row 4qq + r is slot 4r + qq: this lane's own gathered row of round r.
             u32x4 *sk = &s_kt[wave][0][0];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -279,7 +289,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) {
-                const bf16x8 ka = __builtin_bit_cast(bf16x8, sk[sub * kKtPitch + qq + 4 * s4]);
+                const int arow = PVM ? 4 * (sub & 3) + (sub >> 2) : sub;
+                const bf16x8 ka = __builtin_bit_cast(bf16x8, sk[arow * kKtPitch + qq + 4 * s4]);
                 c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[s4], c, 0, 0, 0);
             }
             // Online softmax per wave over its own 16 slots (no workgroup barrier):
@@ -288,7 +299,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             float z[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int tl = qq * 16 + wave * 4 + r;  // slot 4qq + r
+                const int tl = PVM ? r * 16 + wave * 4 + qq    // slot 4r + qq
+                                   : qq * 16 + wave * 4 + r;   // slot 4qq + r
                 z[r] = sub < G && c0 + tl < tok_end ? c[r] * a.scale_log2 : -INFINITY;
             }
             const float mx = rows4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
@@ -300,18 +312,65 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             const float scl = __builtin_amdgcn_exp2f(m_run - base);  // m_run = -inf -> 0
             l_run = l_run * scl + rows4_sum((w[0] + w[1]) + (w[2] + w[3]));
             m_run = m_new;
-            if (sub < G)
-                *reinterpret_cast<float4 *>(&zw[wave][sub][4 * qq]) = make_float4(w[0], w[1], w[2], w[3]);
-            // head h's rescale factor is held by lane h (row 0)
+            if constexpr (PVM) {
+                // Weighted V on the matrix cores with no data movement: contraction
+                // index k = 4qq + j stands for slot 4j + qq, so the A operand (P,
+                // heads x slots) is this lane's own weights w[0..3] (bf16) and the
+                // B operand of 16-dim block blk (slots x dims 8n + blk) is element
+                // blk of this lane's own four V rows.
+                const s16x4 pa = __builtin_bit_cast(
+                    s16x4, u32x2{__builtin_bit_cast(uint32_t, bf16x2{(__bf16)w[0], (__bf16)w[1]}),
+                                 __builtin_bit_cast(uint32_t, bf16x2{(__bf16)w[2], (__bf16)w[3]})});
+                // rescale: C row 4qq + r is head 4qq + r, whose factor every lane
+                // (*, head) holds
+                float f[4];
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float sc = __builtin_bit_cast(
-                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, scl), h));
+                for (int r = 0; r < 4; ++r) {
+                    f[r] = r < G ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                                 __builtin_bit_cast(int, scl), r))
+                                 : 1.0f;
+                    if (4 + r < G)
+                        f[r] = qq == 1 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                                       __builtin_bit_cast(int, scl), 4 + r))
+                                       : f[r];
+                }
 #pragma unroll
-                for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
+                for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) pacc[blk][r] *= f[r];
+                const uint32_t v0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
+                const uint32_t v1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+                const uint32_t v2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
+                const uint32_t v3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
+#pragma unroll
+                for (int c2 = 0; c2 < 4; ++c2) {
+                    // dims 2c2 (low halves) and 2c2 + 1 (high halves) of rounds 0..3
+                    const s16x4 blo = __builtin_bit_cast(
+                        s16x4, u32x2{__builtin_amdgcn_perm(v1[c2], v0[c2], 0x05040100u),
+                                     __builtin_amdgcn_perm(v3[c2], v2[c2], 0x05040100u)});
+                    const s16x4 bhi = __builtin_bit_cast(
+                        s16x4, u32x2{__builtin_amdgcn_perm(v1[c2], v0[c2], 0x07060302u),
+                                     __builtin_amdgcn_perm(v3[c2], v2[c2], 0x07060302u)});
+                    pacc[2 * c2] =
+                        __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, blo, pacc[2 * c2], 0, 0, 0);
+                    pacc[2 * c2 + 1] =
+                        __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, bhi, pacc[2 * c2 + 1], 0, 0, 0);
+                }
+            } else {
+                if (sub < G)
+                    *reinterpret_cast<float4 *>(&zw[wave][sub][4 * qq]) =
+                        make_float4(w[0], w[1], w[2], w[3]);
+                // head h's rescale factor is held by lane h (row 0)
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    const float sc = __builtin_bit_cast(
+                        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, scl), h));
+#pragma unroll
+                    for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
+                }
+                // this lane's tokens 16i + 4w + qq are slots 4i + qq of the wave
+                weighted_v([&](int h, int i) { return zw[wave][h][4 * i + qq]; });
             }
-            // this lane's tokens 16i + 4w + qq are slots 4i + qq of the wave
-            weighted_v([&](int h, int i) { return zw[wave][h][4 * i + qq]; });
         } else {
             // logits: value index i*G + h, transpose-reduced over the 16 lanes of the quarter
             float p[NV];
@@ -365,6 +424,19 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         }
     }
 
+    if constexpr (PVM) {
+        // the wave's weighted V is complete in the C tiles: head 4qq + r, dims 8sub..8sub+7
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            if (4 * qq + r < G) {
+                float *dst = &red[wave][(4 * qq + r) * kHeadDim + sub * 8];
+                *reinterpret_cast<float4 *>(dst) =
+                    make_float4(pacc[0][r], pacc[1][r], pacc[2][r], pacc[3][r]);
+                *reinterpret_cast<float4 *>(dst + 4) =
+                    make_float4(pacc[4][r], pacc[5][r], pacc[6][r], pacc[7][r]);
+            }
+        }
+    } else {
     // ---- reduce the accumulators over the 4 quarters of each wave (lanes ^16, ^32) ----
     float o[NO];
 #pragma unroll
@@ -382,6 +454,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             const int h = orig >> 3, d = orig & 7;
             red[wave][h * kHeadDim + sub * 8 + d] = o[v];
         }
+    }
     }
     if (MQK && qq == 0 && sub < G) {  // this wave's (max, sum) of head sub
         s_wml[wave][sub][0] = m_run;
@@ -503,10 +576,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 }
 
 // Splits per (row, KV head): about 1024 workgroups in all (four per CU), and at
-// least two 64-token chunks per split while that still leaves 256 workgroups,
-// so that a workgroup's second chunk of gathers overlaps its first chunk's
-// arithmetic (measured best on the 128K, 32K and ragged-batch workloads; the
-// 4K single-sequence step prefers one chunk per split).  With many units
+// least four 64-token chunks per split while that still leaves 256 workgroups,
+// so that the per-workgroup prologue and final merge are spread over more
+// chunks (measured best with the matrix-core form on the 128K and 32K
+// workloads, 8 splits of 4 chunks against 16 of 2 and 32 of 1; the ragged
+// batch keeps its 4 splits of 8 chunks and the 4K single-sequence step its one
+// chunk per split).  With many units
 // (chunked prefill: thousands of rows) the grid is far wider than the chip
 // anyway; there each list is cut into kManySplits stretches, issued stretch by
 // stretch over all rows, so that the K/V rows gathered at any time come from
@@ -518,7 +593,7 @@ static void plan_splits(const Geometry &g, int keys, int &splits, int &chunks_pe
     const long units = (long)g.rows * g.kv_heads;
     long want = units > 0 ? (1024 + units - 1) / units : 1;
     if (units >= kManyUnits && want < kManySplits) want = kManySplits;
-    const long cap = units * (chunks / 2) >= 256 ? chunks / 2 : chunks;
+    const long cap = units * (chunks / 4) >= 256 ? chunks / 4 : chunks;
     if (want > cap) want = cap;
     if (want > kMaxSplits) want = kMaxSplits;
     if (want < 1) want = 1;
@@ -539,10 +614,14 @@ static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int un
     // Logits on the matrix cores with per-wave softmax states for contiguous
     // caches and for many units (chunked prefill); paged decode grids keep the
     // vector-unit logits and the shared softmax, which measured faster there.
-    const bool mqk = !paged || grid.x / a.splits >= (unsigned)kManyUnits;
-    if (paged && mqk) sparse_attn_kernel<G, true, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
-    else if (paged) sparse_attn_kernel<G, true, DENSE, false><<<grid, dim3(256), 0, stream>>>(a);
-    else sparse_attn_kernel<G, false, DENSE, true><<<grid, dim3(256), 0, stream>>>(a);
+    const bool many = grid.x / a.splits >= (unsigned)kManyUnits;
+    const bool mqk = !paged || many;
+    // The weighted V goes to the matrix cores as well on decode grids; chunked
+    // prefill (held by its gathers) measured faster with it on bf16 dot2.
+    if (paged && mqk) sparse_attn_kernel<G, true, DENSE, true, false><<<grid, dim3(256), 0, stream>>>(a);
+    else if (paged) sparse_attn_kernel<G, true, DENSE, false, false><<<grid, dim3(256), 0, stream>>>(a);
+    else if (many) sparse_attn_kernel<G, false, DENSE, true, false><<<grid, dim3(256), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false, DENSE, true, true><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1) return e;
