@@ -575,23 +575,28 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     }
 }
 
-// Splits per (row, KV head): about 1024 workgroups in all (four per CU), and at
-// least four 64-token chunks per split while that still leaves 256 workgroups,
-// so that the per-workgroup prologue and final merge are spread over more
-// chunks (measured best with the matrix-core form on the 128K and 32K
-// workloads, 8 splits of 4 chunks against 16 of 2 and 32 of 1; the ragged
-// batch keeps its 4 splits of 8 chunks and the 4K single-sequence step its one
-// chunk per split).  With many units
-// (chunked prefill: thousands of rows) the grid is far wider than the chip
-// anyway; there each list is cut into kManySplits stretches, issued stretch by
-// stretch over all rows, so that the K/V rows gathered at any time come from
-// one key range (the lists are ascending) and stay in the Infinity Cache
-// (8192 rows x 2048 of 131072 keys: 8.8 -> 7.2 ms per layer).  keys: the most
-// keys a row can have (top_k, or max_len for dense attention).
-static void plan_splits(const Geometry &g, int keys, int &splits, int &chunks_per_split) {
+// Splits per (row, KV head).  Sparse attention on contiguous caches (the
+// matrix-core form) aims at about 256 workgroups (one per CU) with at most 8
+// chunks of 64 tokens per split; everything else at about 1024 (four per CU).
+// Either way a split keeps at least four chunks while that still leaves 256
+// workgroups, so that the per-workgroup prologue and final merge are spread
+// over more chunks.  Measured with the matrix-core form: 128K, 8 splits of 4
+// chunks against 16 of 2 and 32 of 1; 32K, 4 splits of 8 chunks against 8 of 4.
+// The paged 32-sequence ragged batch keeps 4 splits of 8 chunks (1 split is
+// far slower there) and the 4K single-sequence step one chunk per split.  With
+// many units (chunked prefill: thousands of rows) the grid is far wider than
+// the chip anyway; there each list is cut into kManySplits stretches, issued
+// stretch by stretch over all rows, so that the K/V rows gathered at any time
+// come from one key range (the lists are ascending) and stay in the Infinity
+// Cache (8192 rows x 2048 of 131072 keys: 8.8 -> 7.2 ms per layer).  keys: the
+// most keys a row can have (top_k, or max_len for dense attention).
+static void plan_splits(const Geometry &g, int keys, bool dense, int &splits,
+                        int &chunks_per_split) {
     const int chunks = div_up(keys, 64);
     const long units = (long)g.rows * g.kv_heads;
-    long want = units > 0 ? (1024 + units - 1) / units : 1;
+    const bool wide = !dense && g.page_shift < 0;  // matrix-core form: fewer, longer workgroups
+    long want = units > 0 ? ((wide ? 256 : 1024) + units - 1) / units : 1;
+    if (wide && want < (chunks + 7) / 8) want = (chunks + 7) / 8;  // at most 8 chunks per split
     if (units >= kManyUnits && want < kManySplits) want = kManySplits;
     const long cap = units * (chunks / 4) >= 256 ? chunks / 4 : chunks;
     if (want > cap) want = cap;
@@ -603,7 +608,7 @@ static void plan_splits(const Geometry &g, int keys, int &splits, int &chunks_pe
 
 size_t attn_partial_floats(const Geometry &g, bool dense) {
     int splits, cps;
-    plan_splits(g, dense ? g.max_len : g.top_k, splits, cps);
+    plan_splits(g, dense ? g.max_len : g.top_k, dense, splits, cps);
     if (splits == 1) return 0;
     return (size_t)g.rows * g.q_heads * splits * (kHeadDim + 2);
 }
@@ -649,7 +654,8 @@ static hipError_t launch_attn(const Geometry &g, const AttnArgs &a, bool paged, 
 
 static AttnArgs attn_args(const Geometry &g, const void *q, const void *k_cache,
                           const void *v_cache, const int32_t *page_table, void *out, float *lse,
-                          float *partials, int keys) {
+                          float *partials, bool dense) {
+    const int keys = dense ? g.max_len : g.top_k;
     AttnArgs a;
     a.q = static_cast<const uint16_t *>(q);
     a.k = static_cast<const uint16_t *>(k_cache);
@@ -669,7 +675,7 @@ static AttnArgs attn_args(const Geometry &g, const void *q, const void *k_cache,
     a.kv_heads = g.kv_heads;
     a.q_heads = g.q_heads;
     a.causal = g.causal;
-    plan_splits(g, keys, a.splits, a.chunks_per_split);
+    plan_splits(g, keys, dense, a.splits, a.chunks_per_split);
     a.scale_log2 = g.softmax_scale * kLog2e;
     const size_t part_o = (size_t)g.rows * g.q_heads * a.splits * kHeadDim;
     a.part_o = a.splits > 1 ? partials : nullptr;
@@ -681,7 +687,7 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
                               float *partials, hipStream_t stream, hipEvent_t split_done) {
-    AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, g.top_k);
+    AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, false);
     a.idx = idx;
     a.n_sel = n_sel;
     if (g.rows == 0) return hipSuccess;
@@ -696,7 +702,7 @@ hipError_t launch_dense_attn(const Geometry &g, const void *q, const void *k_cac
                              const void *v_cache, const int32_t *page_table,
                              const int32_t *seq_lens, const int32_t *q_pos, void *out, float *lse,
                              float *partials, hipStream_t stream) {
-    AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, g.max_len);
+    AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, true);
     a.seq_lens = seq_lens;
     a.q_pos = q_pos;
     if (g.rows == 0) return hipSuccess;
