@@ -15,10 +15,14 @@
 //       thousands of units): each wave's 16 K rows go through its own LDS rows
 //       into v_mfma_f32_16x16x32_bf16 against Q^T (heads padded to 16), and
 //       each wave keeps its own online softmax per head (base-2 exponentials;
-//       the four lanes of a head combine with permlane swaps), passes the
-//       weights to the lanes holding the matching V rows through its LDS rows
-//       and keeps its own weighted-V accumulators: no workgroup barrier per
-//       chunk; the four wave states are merged by the log-sum-exp rule at the end;
+//       the four lanes of a head combine with permlane swaps) and its own
+//       weighted-V accumulators: no workgroup barrier per chunk; the four wave
+//       states are merged by the log-sum-exp rule at the end.  On decode grids
+//       (PVM) the weighted V is a v_mfma_f32_16x16x16_bf16 product whose
+//       operands are the lane's own weights and V rows (the logits tile is
+//       ordered for that); in chunked prefill the weights reach the lanes
+//       holding the matching V rows through the wave's LDS rows and the
+//       weighted V is a bf16 dot2 product;
 //     - vector form (paged decode grids): each lane dots its 8 key values with
 //       the matching 8 values of every head (v_dot2_f32_bf16), a
 //       transpose-reduction over the 16 lanes leaves one (head, token) logit
@@ -26,7 +30,8 @@
 //       maximum and sum, updates the running max / denominator and rescales
 //       (online softmax, shared by the workgroup);
 //     so a split of any length needs one pass;
-//   * each lane accumulates weight x V for its 8 dimensions and G heads.
+//   * in the dot2 forms each lane accumulates weight x V for its 8 dimensions
+//     and G heads.
 // The accumulators are then reduced over lanes and waves in LDS.  With one
 // split the workgroup writes the bf16 output and lse itself.  Otherwise it
 // writes fp32 partials (o, m, l) and attn_merge_kernel combines the splits with
