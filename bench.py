@@ -123,6 +123,32 @@ def roofline(kernel: str, w, alg_bytes: int, ms: float):
             "avg_launch_us": round(ms * 1e3, 2)}
 
 
+def host_cpu():
+    """(threads for the oracle, CPUs this process may run on, CPU model name).
+
+    The oracle uses one thread per CPU available to the process, or
+    OMP_NUM_THREADS when that is set lower (the GPU machines set it to the
+    host-core share of one GPU)."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        avail = os.cpu_count() or 1
+    threads = avail
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        threads = min(threads, int(env))
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return threads, avail, model
+
+
 def cpu_baseline(w, x, budget_s: float):
     """Time the CPU oracle on the same workload, repeating whole steps until
     ``budget_s`` seconds have passed (at least one).  With many query rows per
@@ -139,24 +165,29 @@ def cpu_baseline(w, x, budget_s: float):
                   q_pos=None if x["q_pos"] is None else np.ascontiguousarray(x["q_pos"][:, :16]))
         scale = w.n_q / 16
     sh = orc.shape_of(ws)
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        orc.decode_step(sh, xs["q_idx"], xs["k_idx"], xs["k_cache"], xs["v_cache"],
-                        xs["seq_lens"], xs["q_layers"], xs["q_pos"], xs["page_table"])
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
-            break
+    threads, avail, model = host_cpu()
+    orc.set_threads(threads)
+    try:
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            orc.decode_step(sh, xs["q_idx"], xs["k_idx"], xs["k_cache"], xs["v_cache"],
+                            xs["seq_lens"], xs["q_layers"], xs["q_pos"], xs["page_table"])
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or el / reps * (reps + 1) > 3 * budget_s:
+                break
+    finally:
+        orc.set_threads(1)
     us = el / reps * 1e6 * scale
+    how = f"C oracle on {threads} host thread(s)"
     if scale == 1.0:
-        sample = (f"{reps} full step(s) of {w.name} (B={w.batch}, L={w.n_layers}), "
-                  f"single-threaded C, {el:.1f} s")
+        sample = f"{reps} full step(s) of {w.name} (B={w.batch}, L={w.n_layers}), {how}, {el:.1f} s"
     else:
         sample = (f"{reps} step(s) over the first 16 of {w.n_q} query rows of {w.name} "
-                  f"(L={w.n_layers}), single-threaded C, {el:.1f} s; scaled x{scale:g} "
+                  f"(L={w.n_layers}), {how}, {el:.1f} s; scaled x{scale:g} "
                   f"to all rows (extrapolated)")
-    return {"value": round(us, 1), "unit": "us/step", "cores": 1, "kind": "oracle",
-            "sample": sample}
+    return {"value": round(us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+            "sample": sample, "host_cpus_available": avail, "cpu_model": model}
 
 
 def copy_reference(mib: int, dev) -> None:
@@ -206,18 +237,25 @@ def kd_cpu_baseline(w, x, budget_s: float):
         pairs = int(valid_keys_per_row(ws, {"q_pos": qp}).sum())
         return el, pairs
 
-    el, pairs = run(1)
-    rows = 1
-    more = int(budget_s / max(el, 1e-6))
-    if more >= 2:
-        rows = min(more, w.n_q)
-        el, pairs = run(rows)
+    threads, avail, model = host_cpu()
+    orc.set_threads(threads)
+    try:
+        el, pairs = run(threads)
+        rows = threads
+        more = int(budget_s / max(el, 1e-6)) * threads
+        if more >= 2 * threads:
+            rows = min(more, w.n_q)
+            el, pairs = run(rows)
+    finally:
+        orc.set_threads(1)
     scale = kd_counts(w, x)["pairs"] / pairs
-    return {"value": round(el * scale * 1e3, 1), "unit": "ms/step", "cores": 1, "kind": "oracle",
+    return {"value": round(el * scale * 1e3, 1), "unit": "ms/step", "cores": threads,
+            "kind": "oracle", "host_cpus_available": avail, "cpu_model": model,
             "sample": (f"Eq. 5 target + Eq. 6 loss and gradient of the oracle over the last "
                        f"{rows} of {w.n_q} rows of {w.name} (L={w.n_layers}, {pairs} row-key "
-                       f"pairs), single-threaded C, {el:.1f} s; scaled x{scale:.4g} by row-key "
-                       f"pairs to the whole sequence (extrapolated)")}
+                       f"pairs), C oracle with the target on {threads} host thread(s) (the "
+                       f"loss's sums across rows on one), {el:.1f} s; scaled x{scale:.4g} by "
+                       f"row-key pairs to the whole sequence (extrapolated)")}
 
 
 def run_kd(args, w) -> int:

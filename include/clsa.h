@@ -24,9 +24,16 @@
  *   - Arguments are validated on the host before anything is enqueued; on any
  *     error nothing is enqueued.  No C++ exception crosses this interface.
  *   - Device-side values are trusted within documented ranges: seq_lens[b] is
- *     clamped to [0, max_len]; q_pos (causal) limits row (b,t) to keys
+ *     clamped to [0, max_len] and n_sel[r] (an input of clsa_sparse_attn) to
+ *     [0, top_k], and a value outside its range raises a device error bit that
+ *     clsa_get_device_error() reports; q_pos (causal) limits row (b,t) to keys
  *     j <= q_pos[b,t]; page_table entries for pages that hold valid tokens
  *     must be valid physical page numbers (they are not range-checked).
+ *   - Thread safety: entry points may be called concurrently from several host
+ *     threads (each with its own workspace and outputs).  The library keeps no
+ *     mutable state shared between calls except a per-device cache of one
+ *     device property (filled atomically) and the device error bits; the
+ *     profiling hook (clsa_set_phase_events) is per host thread.
  *
  * Tensor layouts (row-major, R = batch * n_q query rows, row r = b * n_q + t):
  *   q_idx       bf16 [batch, n_q, idx_heads, idx_dim]   index query (Eq. 2)
@@ -85,6 +92,12 @@ typedef enum {
     CLSA_ERR_HIP = -4          /* the HIP runtime reported an error on enqueue   */
 } clsa_status;
 
+/* Bits reported by clsa_get_device_error(). */
+enum {
+    CLSA_DEVERR_SEQ_LEN = 1, /* a seq_lens[b] outside [0, max_len] was clamped        */
+    CLSA_DEVERR_N_SEL = 2    /* an n_sel[r] outside [0, top_k] was clamped            */
+};
+
 typedef enum {
     CLSA_OP_INDEX = 0,  /* clsa_index_scores (needs no workspace) */
     CLSA_OP_TOPK = 1,   /* clsa_topk */
@@ -113,7 +126,8 @@ typedef struct clsa_shape {
 } clsa_shape;
 
 /* Bytes of workspace `op` needs for `shape` (n_layers matters for
- * CLSA_OP_KD_TARGET only; for CLSA_OP_DECODE it never changes the size).
+ * CLSA_OP_KD_TARGET only, whose statistics buffer grows with the layer count;
+ * for CLSA_OP_DECODE it never changes the size: layers reuse the same buffers).
  * Returns 0 for CLSA_OP_INDEX, and also 0 when the shape is invalid or
  * unsupported (the entry point then reports the reason). */
 size_t clsa_workspace_bytes(const clsa_shape *shape, int32_t op, int32_t n_layers);
@@ -249,7 +263,16 @@ clsa_status clsa_kd_loss(const clsa_shape *shape, const float *abar, const void 
 /* Static, human-readable name of a status code. */
 const char *clsa_status_string(clsa_status status);
 
-/* Profiling hook (not thread-safe; set and use from one thread).  With
+/* Debug call for device-side range errors: *bits receives the CLSA_DEVERR_*
+ * bits raised on the current device by any kernel of this library since the
+ * last call (0 if none), and the bits are cleared.  Unlike every other entry
+ * point it synchronises: it waits for the whole device (hipDeviceSynchronize)
+ * before reading.  Calls overlapping on one device may each see a part of the
+ * bits.  bits NULL: CLSA_ERR_INVALID_ARG. */
+clsa_status clsa_get_device_error(uint32_t *bits);
+
+/* Profiling hook, per host thread: it applies only to the calls made from
+ * the thread that set it (a benchmarking facility, not meant for serving).  With
  * n = 4 + 2m (0 <= m <= 64) non-null hipEvent_t handles, the next
  * clsa_decode_step calls record, on the call's stream: events[0] right before
  * the indexer kernel, events[1] after it, events[2] after the top-k and

@@ -26,8 +26,8 @@ _lib = None
 def build() -> str:
     """Compile the oracle (always) and return the path of the shared library."""
     tmp = _LIB + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math", "-Wall", "-Wextra",
-           "-o", tmp, _SRC, "-lm"]
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", "-fno-fast-math", "-Wall",
+           "-Wextra", "-o", tmp, _SRC, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB)
     return _LIB
@@ -70,6 +70,10 @@ def _load():
     lib = ctypes.CDLL(_LIB)
     P = ctypes.c_void_p
     SP = ctypes.POINTER(Shape)
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = None
+    lib.oracle_get_threads.argtypes = []
+    lib.oracle_get_threads.restype = ctypes.c_int
     lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
     lib.oracle_bf16_to_double.restype = ctypes.c_double
     lib.oracle_valid_len.argtypes = [SP, P, P, ctypes.c_int, ctypes.c_int]
@@ -96,6 +100,15 @@ def _c(a, dtype):
     if a is None:
         return None
     return np.ascontiguousarray(a, dtype=dtype)
+
+
+def set_threads(n: int) -> None:
+    """Host threads for the row / head loops (results do not depend on it)."""
+    _load().oracle_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(_load().oracle_get_threads())
 
 
 def bf16_to_double(h: int) -> float:

@@ -33,6 +33,10 @@ typedef struct {
     double softmax_scale;
 } oracle_shape;
 
+/* Host threads used by the index, top-k, attention and distillation-target
+ * loops (default 1).  Results are identical for every thread count. */
+void oracle_set_threads(int n);
+int oracle_get_threads(void);
 double oracle_bf16_to_double(uint16_t h);
 int oracle_valid_len(const oracle_shape *s, const int32_t *seq_lens, const int32_t *q_pos, int b,
                      int t);

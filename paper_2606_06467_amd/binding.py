@@ -88,6 +88,7 @@ def lib() -> ctypes.CDLL:
         "clsa_kd_loss": (i32, [SP, P, P, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_status_string": (ctypes.c_char_p, [i32]),
         "clsa_set_phase_events": (i32, [ctypes.POINTER(P), i32]),
+        "clsa_get_device_error": (i32, [ctypes.POINTER(ctypes.c_uint32)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -216,6 +217,18 @@ def clsa_kd_loss(shape, abar, q_idx, k_idx, page_table, seq_lens, q_pos, loss, d
                               _ptr(seq_lens, "seq_lens"), _ptr(q_pos, "q_pos"),
                               _ptr(loss, "loss"), _ptr(dq_idx, "dq_idx"), _ptr(dk_idx, "dk_idx"),
                               _ptr(ws, "ws"), wsb, _stream(stream)), "clsa_kd_loss")
+
+
+CLSA_DEVERR_SEQ_LEN = 1
+CLSA_DEVERR_N_SEL = 2
+
+
+def clsa_get_device_error() -> int:
+    """Device error bits (CLSA_DEVERR_*) raised since the last call on the
+    current device, cleared by the call.  Synchronises the device."""
+    v = ctypes.c_uint32(0)
+    _check(lib().clsa_get_device_error(ctypes.byref(v)), "clsa_get_device_error")
+    return int(v.value)
 
 
 def clsa_set_phase_events(events: Optional[Sequence[int]]) -> None:

@@ -1,9 +1,12 @@
 // C-ABI entry points of libclsa: host-side validation, workspace carving and
-// kernel dispatch.  Nothing here allocates device memory or synchronises.
+// kernel dispatch.  Nothing here allocates device memory, and only the debug
+// call clsa_get_device_error synchronises.
 #include "clsa.h"
 
 #include <math.h>
 #include <stdint.h>
+
+#include <atomic>
 
 #include "clsa_internal.h"
 
@@ -20,7 +23,10 @@ struct PhaseHook {
     hipEvent_t ev[4 + 2 * kHookLayers];
     int layers = 0;                 // layers bracketed by ev[4 + 2l], ev[5 + 2l]
     bool on = false;
-} g_hook;
+};
+// The profiling hook belongs to the host thread that set it: calls made from
+// other threads never see it, so concurrent callers do not share any state here.
+thread_local PhaseHook t_hook;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -97,20 +103,21 @@ clsa_status check_common(const clsa_shape *s, const int32_t *page_table, const i
     return CLSA_OK;
 }
 
-// Device limit on dynamic LDS per workgroup, cached per device.
+// Device limit on LDS per workgroup, one entry per device (0 = not read yet).
+// Threads that race on an entry store the same value, so relaxed atomics suffice.
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_lds_limit[kMaxDevices];
+
 clsa_status check_topk_lds(const Geometry &g) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return CLSA_ERR_HIP;
-    static int cached_dev = -1, cached_lds = 0;
-    if (cached_dev != dev) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+    int lds = dev >= 0 && dev < kMaxDevices ? g_lds_limit[dev].load(std::memory_order_relaxed) : 0;
+    if (lds == 0) {
+        if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
             return CLSA_ERR_HIP;
-        cached_lds = v;
-        cached_dev = dev;
+        if (dev >= 0 && dev < kMaxDevices) g_lds_limit[dev].store(lds, std::memory_order_relaxed);
     }
-    return clsa::topk_lds_bytes(g) + 1024 <= (size_t)cached_lds ? CLSA_OK
-                                                                        : CLSA_ERR_UNSUPPORTED;
+    return clsa::topk_lds_bytes(g) + 1024 <= (size_t)lds ? CLSA_OK : CLSA_ERR_UNSUPPORTED;
 }
 
 // Carves 256-byte aligned sub-buffers out of a workspace; with base == nullptr
@@ -336,7 +343,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
 
     carve_decode(g, ws, w);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const bool hook = g_hook.on;
+    const bool hook = t_hook.on;
     // Many query rows per sequence (chunked prefill): scores on the matrix cores,
     // without the coarse histogram, which the top-k then makes itself.  The
     // histogram needs clearing unless that top-k is the per-row one.
@@ -353,31 +360,31 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
         const bool first = s == 0;
         if (!mfma || clsa::topk_uses_wide(g))
             CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
-        if (first && hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+        if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
         if (mfma)
             CLSA_TRY(from_hip(clsa::launch_index_prefill(g, qi, ki, page_table, seq_lens, q_pos,
                                                          w.scores, st)));
         else
             CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
                                                         w.scores, w.topk.hist, st)));
-        if (first && hook && hipEventRecord(g_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
+        if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
         CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, is, ns,
                                             st)));
-        if (first && hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
+        if (first && hook && hipEventRecord(t_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
         const int l_end = n_layers < (s + 1) * group ? n_layers : (s + 1) * group;
         for (int l = s * group; l < l_end; ++l) {
             const uint16_t *ql = static_cast<const uint16_t *>(q_layers) + l * q_stride;
             uint16_t *ol = static_cast<uint16_t *>(out_layers) + l * q_stride;
             float *lsel = lse_layers ? lse_layers + l * lse_stride : nullptr;
-            const bool mark = hook && l < g_hook.layers;
-            if (mark && hipEventRecord(g_hook.ev[4 + 2 * l], st) != hipSuccess)
+            const bool mark = hook && l < t_hook.layers;
+            if (mark && hipEventRecord(t_hook.ev[4 + 2 * l], st) != hipSuccess)
                 return CLSA_ERR_HIP;
             CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, is,
                                                        ns, ol, lsel, w.partials, st,
-                                                       mark ? g_hook.ev[5 + 2 * l] : nullptr)));
+                                                       mark ? t_hook.ev[5 + 2 * l] : nullptr)));
         }
     }
-    if (hook && hipEventRecord(g_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
+    if (hook && hipEventRecord(t_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
     return CLSA_OK;
 }
 
@@ -471,13 +478,13 @@ clsa_status clsa_kd_target(const clsa_shape *shape, int32_t n_layers, const void
     const size_t need = align_up(sizeof(float) * clsa::kd_target_ws_floats(g, n_layers));
     if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const bool hook = g_hook.on;
-    if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+    const bool hook = t_hook.on;
+    if (hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
     CLSA_TRY(from_hip(clsa::launch_kd_target(g, n_layers, q_layers, k_cache, page_table,
                                              seq_lens, q_pos, lse_layers, abar,
                                              static_cast<float *>(ws), st,
-                                             hook ? g_hook.ev[1] : nullptr)));
-    if (hook && hipEventRecord(g_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
+                                             hook ? t_hook.ev[1] : nullptr)));
+    if (hook && hipEventRecord(t_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
     return CLSA_OK;
 }
 
@@ -499,13 +506,13 @@ clsa_status clsa_kd_loss(const clsa_shape *shape, const float *abar, const void 
     const size_t need = align_up(sizeof(float) * clsa::kd_loss_ws_floats(g));
     if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return CLSA_ERR_WORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const bool hook = g_hook.on;
-    if (hook && hipEventRecord(g_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+    const bool hook = t_hook.on;
+    if (hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
     CLSA_TRY(from_hip(clsa::launch_kd_loss(g, abar, q_idx, k_idx, page_table, seq_lens, q_pos,
                                            loss, dq_idx, dk_idx, static_cast<float *>(ws), st,
-                                           hook ? g_hook.ev[1] : nullptr,
-                                           hook ? g_hook.ev[2] : nullptr)));
-    if (hook && hipEventRecord(g_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
+                                           hook ? t_hook.ev[1] : nullptr,
+                                           hook ? t_hook.ev[2] : nullptr)));
+    if (hook && hipEventRecord(t_hook.ev[3], st) != hipSuccess) return CLSA_ERR_HIP;
     return CLSA_OK;
 }
 
@@ -520,17 +527,31 @@ const char *clsa_status_string(clsa_status status) {
     return "CLSA_ERR_UNKNOWN";
 }
 
+clsa_status clsa_get_device_error(uint32_t *bits) {
+    if (!bits) return CLSA_ERR_INVALID_ARG;
+    *bits = 0;
+    if (hipDeviceSynchronize() != hipSuccess) return CLSA_ERR_HIP;
+    uint32_t v = 0;
+    CLSA_TRY(from_hip(clsa::take_device_error_index_decode(&v)));
+    CLSA_TRY(from_hip(clsa::take_device_error_index_prefill(&v)));
+    CLSA_TRY(from_hip(clsa::take_device_error_topk(&v)));
+    CLSA_TRY(from_hip(clsa::take_device_error_sparse_attn(&v)));
+    CLSA_TRY(from_hip(clsa::take_device_error_kd(&v)));
+    *bits = v;
+    return CLSA_OK;
+}
+
 clsa_status clsa_set_phase_events(void *const *events, int32_t n) {
     if (n == 0) {
-        g_hook.on = false;
+        t_hook.on = false;
         return CLSA_OK;
     }
     if (n < 4 || n > 4 + 2 * kHookLayers || (n & 1) || !events) return CLSA_ERR_INVALID_ARG;
     for (int i = 0; i < n; ++i)
         if (!events[i]) return CLSA_ERR_INVALID_ARG;
-    for (int i = 0; i < n; ++i) g_hook.ev[i] = static_cast<hipEvent_t>(events[i]);
-    g_hook.layers = (n - 4) / 2;
-    g_hook.on = true;
+    for (int i = 0; i < n; ++i) t_hook.ev[i] = static_cast<hipEvent_t>(events[i]);
+    t_hook.layers = (n - 4) / 2;
+    t_hook.on = true;
     return CLSA_OK;
 }
 

@@ -36,6 +36,15 @@ constexpr int kTopkWideMaxRows = 128;
 
 __host__ __device__ inline int div_up(int a, int b) { return (a + b - 1) / b; }
 
+// Device error bits (CLSA_DEVERR_* of clsa.h) raised by the kernels of each
+// source file on the current device: OR-ed into *bits, then cleared there.
+// Synchronous copies (a debug path).
+hipError_t take_device_error_index_decode(uint32_t *bits);
+hipError_t take_device_error_index_prefill(uint32_t *bits);
+hipError_t take_device_error_topk(uint32_t *bits);
+hipError_t take_device_error_sparse_attn(uint32_t *bits);
+hipError_t take_device_error_kd(uint32_t *bits);
+
 // ---- index_decode.hip ----
 // coarse_hist: [rows, kCoarseBins], zero on entry, or NULL for no histogram.
 hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void *k_idx,

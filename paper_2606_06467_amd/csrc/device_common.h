@@ -152,8 +152,44 @@ __device__ __forceinline__ uint32_t score_key(float s) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Device-side error bits of the kernels of one source file: every kernel
+// source includes this header, so each code object holds its own copy, read and
+// cleared from the host by take_source_device_error().  Raised when a device
+// value the host cannot check lies outside its documented range and is clamped.
+constexpr uint32_t kDevErrSeqLen = 1u;  // seq_lens[b] outside [0, max_len]
+constexpr uint32_t kDevErrNSel = 2u;    // n_sel[r] outside [0, top_k]
+static __device__ uint32_t g_device_error;
+
+// One atomic per wave that meets the condition (called inside the branch that
+// found it; the first active lane reports).
+__device__ __forceinline__ void note_device_error(uint32_t bit) {
+    const uint64_t active = __ballot(1);
+    if ((uint64_t)__lane_id() == (uint64_t)__builtin_ctzll(active)) atomicOr(&g_device_error, bit);
+}
+
+// A sequence length clamped to [0, max_len]; out-of-range lengths are flagged.
 __device__ __forceinline__ int clamp_len(int n, int max_len) {
-    return n < 0 ? 0 : (n > max_len ? max_len : n);
+    if (n < 0 || n > max_len) {
+        note_device_error(kDevErrSeqLen);
+        return n < 0 ? 0 : max_len;
+    }
+    return n;
+}
+
+// Host side: this source file's error bits on the current device, cleared.
+// Synchronous (a debug path).
+static inline hipError_t take_source_device_error(uint32_t *bits) {
+    uint32_t v = 0;
+    hipError_t e = hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_device_error), sizeof v, 0,
+                                       hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return e;
+    if (v) {
+        const uint32_t zero = 0;
+        e = hipMemcpyToSymbol(HIP_SYMBOL(g_device_error), &zero, sizeof zero, 0,
+                              hipMemcpyHostToDevice);
+    }
+    *bits |= v;
+    return e;
 }
 
 // Number of valid keys of query row (b, t).

@@ -135,4 +135,6 @@ hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void 
     return hipGetLastError();
 }
 
+hipError_t take_device_error_index_decode(uint32_t *bits) { return take_source_device_error(bits); }
+
 }  // namespace clsa

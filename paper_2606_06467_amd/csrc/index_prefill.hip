@@ -258,4 +258,6 @@ hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void
     return hipGetLastError();
 }
 
+hipError_t take_device_error_index_prefill(uint32_t *bits) { return take_source_device_error(bits); }
+
 }  // namespace clsa

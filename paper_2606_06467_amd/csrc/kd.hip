@@ -896,4 +896,6 @@ hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_id
     return hipGetLastError();
 }
 
+hipError_t take_device_error_kd(uint32_t *bits) { return take_source_device_error(bits); }
+
 }  // namespace clsa

@@ -92,7 +92,12 @@ __host__ __device__ constexpr int pow2_at_least(int x) {
 template <bool DENSE>
 __device__ __forceinline__ int row_keys(const AttnArgs &a, int row) {
     if (DENSE) return valid_keys(a.seq_lens, a.q_pos, a.causal, row / a.n_q, row, a.max_len);
-    return min(max(a.n_sel[row], 0), a.top_k);
+    const int m = a.n_sel[row];
+    if (m < 0 || m > a.top_k) {
+        note_device_error(kDevErrNSel);
+        return m < 0 ? 0 : a.top_k;
+    }
+    return m;
 }
 
 // Maximum / sum over the four rows (lanes l, l ^ 16, l ^ 32, l ^ 48) of a wave.
@@ -762,5 +767,7 @@ hipError_t launch_dense_attn(const Geometry &g, const void *q, const void *k_cac
     return launch_attn<true>(g, a, g.page_shift >= 0, dim3((unsigned)blocks), units, stream,
                              nullptr);
 }
+
+hipError_t take_device_error_sparse_attn(uint32_t *bits) { return take_source_device_error(bits); }
 
 }  // namespace clsa

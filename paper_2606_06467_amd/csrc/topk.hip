@@ -676,4 +676,6 @@ hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *se
     return hipGetLastError();
 }
 
+hipError_t take_device_error_topk(uint32_t *bits) { return take_source_device_error(bits); }
+
 }  // namespace clsa

@@ -5,11 +5,20 @@ Nothing here feeds a GPU result into the oracle: the oracle only ever sees the
 generator's arrays."""
 from __future__ import annotations
 
+import os
 import sys
 import numpy as np
 
 import oracle as orc
 from paper_2606_06467_amd import inputs
+
+# The oracle's results do not depend on its thread count (tests/test_oracle_threads.py);
+# threads only shorten the full-size parity cases.
+try:
+    _CPUS = len(os.sched_getaffinity(0))
+except (AttributeError, OSError):
+    _CPUS = os.cpu_count() or 1
+orc.set_threads(max(1, min(16, _CPUS)))
 
 # Tolerances for bf16 inputs against the fp64 oracle (attention outputs).
 ATTN_MAX_ABS = 2e-2

@@ -32,7 +32,7 @@ def test_header_declares_the_entry_points():
     for n in ("clsa_index_scores", "clsa_topk", "clsa_sparse_attn", "clsa_decode_step",
               "clsa_decode_step_grouped", "clsa_dense_attn", "clsa_project_append",
               "clsa_kd_target", "clsa_kd_loss", "clsa_workspace_bytes",
-              "clsa_status_string", "clsa_set_phase_events"):
+              "clsa_status_string", "clsa_set_phase_events", "clsa_get_device_error"):
         assert n in names
 
 
@@ -203,6 +203,55 @@ def test_phase_event_hook_arguments(lib):
     assert lib.clsa_set_phase_events(many, 4 + 2 * 64) == 0
     assert lib.clsa_set_phase_events(many, 6) == 0
     assert lib.clsa_set_phase_events(None, 0) == 0
+
+
+def test_get_device_error_rejects_null(lib):
+    assert lib.clsa_get_device_error(None) == -1
+
+
+def _symbols():
+    out = subprocess.run(["readelf", "-sW", LIB], capture_output=True, text=True, check=True).stdout
+    return [line.split() for line in out.splitlines() if len(line.split()) >= 8]
+
+
+def test_phase_hook_is_thread_local():
+    """The profiling hook is per host thread: its storage is a TLS object, so
+    calls from other threads never read or write it."""
+    hooks = [f for f in _symbols() if "hook" in f[7]]
+    assert hooks and all(f[3] == "TLS" for f in hooks), hooks
+
+
+def test_no_function_static_state_in_the_entry_points():
+    """Host-side mutable state of the entry points: no function-local statics
+    (``_ZZ`` symbols), and of the file-scope objects of the host code only the
+    per-device property cache (an array of atomics indexed by device) is a
+    non-TLS object."""
+    syms = _symbols()
+    assert not [f[7] for f in syms if f[7].startswith("_ZZ")]
+    objs = [f[7] for f in syms if f[3] == "OBJECT" and "GLOBAL__N" in f[7]]
+    assert objs and all("lds_limit" in n for n in objs), objs
+
+
+def test_phase_hook_set_from_threads(lib):
+    """Setting and clearing the hook from many threads at once is safe (each
+    thread writes only its own copy) and every call reports the same status."""
+    import threading
+    arr = (ctypes.c_void_p * 6)(A, A, A, A, A, A)
+    res = []
+
+    def work():
+        r = []
+        for i in range(200):
+            r.append(lib.clsa_set_phase_events(arr, 6 if i % 2 == 0 else 4))
+            r.append(lib.clsa_set_phase_events(None, 0))
+        res.append(r)
+
+    th = [threading.Thread(target=work) for _ in range(8)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert len(res) == 8 and all(v == 0 for r in res for v in r)
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -5,6 +5,8 @@ Index sets: rows whose exact k-th / (k+1)-th score gap is at least 1e-5 relative
 must match the oracle exactly; rows inside that tie band must hold a valid top-k
 (counted and printed).  Attention outputs are compared on every row whose set
 matches: max |d| <= 2e-2, mean |d| <= 2e-3 against the fp64 oracle."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -103,7 +105,7 @@ def test_deterministic_bits():
 def test_full_decode_b4_n128k_planted():
     w = inputs.workload("decode_b4_n128k_planted")
     x = inputs.make_inputs(w)
-    gidx, gns, _ = _check_step(w, x, [0, w.n_layers - 1], w.name)
+    gidx, gns, _ = _check_step(w, x, range(w.n_layers), w.name)
     pos = inputs.planted_positions(w)
     frac = np.mean([np.isin(pos[b], gidx[b, 0]).mean() for b in range(w.batch)])
     U.log(f"  planted positions selected: {frac:.3f}")
@@ -140,13 +142,189 @@ def test_tie_band_statistics_128k_planted_many_seeds():
 def test_full_decode_b8_n32k():
     w = inputs.workload("decode_b8_n32k")
     x = inputs.make_inputs(w)
-    _check_step(w, x, [0, w.n_layers - 1], w.name)
+    _check_step(w, x, range(w.n_layers), w.name)
 
 
 def test_full_decode_b32_ragged_paged():
     w = inputs.workload("decode_b32_ragged_paged")
     x = inputs.make_inputs(w)
-    _check_step(w, x, [0, w.n_layers - 1], w.name)
+    _check_step(w, x, range(w.n_layers), w.name)
+
+
+def test_chunked_prefill_many_rows_chain():
+    """More than 128 query rows through the whole step: the matrix-core indexer,
+    the per-row top-k (including rows whose causal prefix holds no more than k
+    keys, which select their whole prefix) and the key-range split attention
+    (at least 4096 (row, KV head) units), every row and layer compared."""
+    w = inputs.small_workload(batch=2, lens=(20000, 20000), n_q=512, causal=True,
+                              q_pos0=(1800, 19488), top_k=2048, n_layers=2, wid=81)
+    x = inputs.make_inputs(w)
+    assert w.batch * w.n_q > 128 and w.batch * w.n_q * w.kv_heads >= 4096
+    n = np.minimum(x["q_pos"] + 1, np.asarray(w.lens)[:, None])
+    assert (n <= w.top_k).sum() > 100 and (n > w.top_k).sum() > 100
+    gidx, gns, _ = _check_step(w, x, range(w.n_layers), "prefill 1024 rows")
+    short = n <= w.top_k
+    np.testing.assert_array_equal(gns[short], n[short])
+
+
+def test_many_single_query_rows():
+    """160 decode rows (more than 128): the per-row top-k fed by the decode
+    indexer's coarse histograms, with empty rows, rows with fewer keys than k,
+    exactly k and k + 1 keys."""
+    g = np.random.default_rng(82)
+    lens = [int(v) for v in g.integers(500, 6000, size=160)]
+    lens[:4] = [0, 1024, 1025, 700]
+    w = inputs.small_workload(batch=160, lens=lens, top_k=1024, n_layers=2, wid=82)
+    x = inputs.make_inputs(w)
+    gidx, gns, _ = _check_step(w, x, range(w.n_layers), "160 single-query rows")
+    assert gns[0, 0] == 0 and gns[1, 0] == 1024 and gns[2, 0] == 1024 and gns[3, 0] == 700
+
+
+def _slice_rows(w, x, rows):
+    """The workload restricted to query rows ``rows`` of its one sequence (same
+    caches and layers; each row keeps its own causal position)."""
+    rows = np.asarray(rows)
+    ws = dataclasses.replace(w, n_q=len(rows), q_pos0=None)
+    xs = dict(x, q_idx=np.ascontiguousarray(x["q_idx"][:, rows]),
+              q_layers=np.ascontiguousarray(x["q_layers"][:, :, rows]),
+              q_pos=np.ascontiguousarray(x["q_pos"][:, rows]))
+    return ws, xs
+
+
+def test_full_prefill_t8k_n128k_sampled_rows():
+    """The whole chunked-prefill step at full size (8192 causal rows over a
+    131072-token cache, 16 layers) through clsa_decode_step; sampled rows (block
+    edges and seeded rows) are compared with the oracle run on those rows alone:
+    index sets bit-exact outside the tie band, every layer's output within the
+    attention tolerances."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    w = inputs.workload("prefill_t8k_n128k")
+    x = inputs.make_inputs(w)
+    g = np.random.default_rng(4004)
+    rows = sorted(set([0, 15, 16, 127, 128, 4095, 4096, 8191] +
+                      [int(v) for v in g.choice(w.n_q, size=16, replace=False)]))
+    d = U.to_dev(x)
+    sh = U.shape_of(w)
+    L = w.n_layers
+    out = torch.full((L, w.batch, w.n_q, w.q_heads, w.head_dim), float("nan"),
+                     dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((L, w.batch, w.n_q, w.q_heads), float("nan"), device="cuda")
+    idx = torch.full((w.batch, w.n_q, w.top_k), -7, dtype=torch.int32, device="cuda")
+    ns = torch.full((w.batch, w.n_q), -7, dtype=torch.int32, device="cuda")
+    ws = B.workspace(sh, B.CLSA_OP_DECODE, L)
+    U.log(f"  prefill_t8k_n128k: full step on the GPU, rows compared {rows}")
+    B.clsa_decode_step(sh, d["q_idx"], d["k_idx"], d["k_cache"], d["v_cache"], d["page_table"],
+                       d["seq_lens"], d["q_pos"], d["q_layers"], out, lse, idx, ns, ws)
+    torch.cuda.synchronize()
+    del ws
+    r = torch.as_tensor(rows, device="cuda")
+    g_out = B.bits_from_bf16(out[:, :, r].contiguous())
+    g_lse = lse[:, :, r].cpu().numpy().astype(np.float64)
+    gidx, gns = idx[:, r].cpu().numpy(), ns[:, r].cpu().numpy()
+    del out, lse, idx, ns, d
+    torch.cuda.empty_cache()
+    assert np.all(gns == w.top_k)
+    ws_, xs = _slice_rows(w, x, rows)
+    osh = orc.shape_of(ws_)
+    scores = orc.index_scores(osh, xs["q_idx"], xs["k_idx"], xs["seq_lens"], xs["q_pos"])
+    oidx, ons = orc.topk(osh, scores.astype(np.float32), xs["seq_lens"], xs["q_pos"])
+    nr, in_band, differ = U.check_index_sets(ws_, osh, scores, gidx, gns, xs["seq_lens"],
+                                             xs["q_pos"], ref=(oidx, ons),
+                                             bound=U.higham_bound(ws_, xs))
+    U.log(f"  prefill sampled rows: {nr} rows, {in_band} in the tie band, {differ} of them "
+          f"differ, 0 differ outside it")
+    same = np.array([[np.array_equal(gidx[0, t], oidx[0, t]) for t in range(len(rows))]])
+    assert same.sum() >= len(rows) - in_band
+    for l in range(L):
+        ro, rl = orc.sparse_attn(osh, xs["q_layers"][l], xs["k_cache"], xs["v_cache"], oidx, ons)
+        U.compare_attn(g_out[l], g_lse[l], ro, rl, mask_rows=same, what=f"prefill layer {l}")
+
+
+def test_device_error_bits_for_out_of_range_lengths():
+    """seq_lens outside [0, max_len] are clamped (the step equals the one with
+    clamped lengths) and raise CLSA_DEVERR_SEQ_LEN; n_sel outside [0, top_k] is
+    clamped by the attention and raises CLSA_DEVERR_N_SEL; reading clears them."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    w = inputs.small_workload(batch=3, lens=(3000, 3000, 0), top_k=512, n_layers=1, wid=83)
+    x = inputs.make_inputs(w)
+    B.clsa_get_device_error()                       # clear what earlier calls may have raised
+    assert B.clsa_get_device_error() == 0
+    ref = _gpu_step(w, x, 1)
+    assert B.clsa_get_device_error() == 0
+    bad = dict(x, seq_lens=np.array([w.max_len + 7, 3000, -5], np.int32))
+    got = _gpu_step(w, bad, 1)
+    assert B.clsa_get_device_error() == B.CLSA_DEVERR_SEQ_LEN
+    assert B.clsa_get_device_error() == 0
+    for u, v in zip(ref, got):
+        np.testing.assert_array_equal(u, v)
+    # n_sel past top_k on a stand-alone attention call
+    d = U.to_dev(x)
+    sh = U.shape_of(w)
+    idx = torch.from_numpy(ref[2]).cuda()
+    ns = torch.from_numpy(ref[3]).cuda()
+    ws = B.workspace(sh, B.CLSA_OP_ATTN)
+    q = d["q_layers"][0].contiguous()
+    o1 = torch.empty_like(q)
+    o2 = torch.empty_like(q)
+    B.clsa_sparse_attn(sh, q, d["k_cache"], d["v_cache"], None, idx, ns, o1, None, ws)
+    ns_bad = ns.clone()
+    ns_bad[0, 0] = w.top_k + 9
+    ns_full = ns.clone()
+    ns_full[0, 0] = w.top_k
+    B.clsa_sparse_attn(sh, q, d["k_cache"], d["v_cache"], None, idx, ns_bad, o2, None, ws)
+    assert B.clsa_get_device_error() == B.CLSA_DEVERR_N_SEL
+    B.clsa_sparse_attn(sh, q, d["k_cache"], d["v_cache"], None, idx, ns_full, o1, None, ws)
+    assert B.clsa_get_device_error() == 0
+    np.testing.assert_array_equal(B.bits_from_bf16(o1), B.bits_from_bf16(o2))
+
+
+def test_concurrent_host_threads():
+    """Four host threads, each with its own stream, workspace and outputs, run
+    the step at the same time; every result equals the serial one bit for bit."""
+    import threading
+    import torch
+    from paper_2606_06467_amd import binding as B
+    ws_ = [inputs.small_workload(batch=2, lens=(6000 + 700 * i, 2500), top_k=1024, n_layers=2,
+                                 page_size=64 if i % 2 else 0, wid=84 + i) for i in range(4)]
+    xs = [inputs.make_inputs(w) for w in ws_]
+    serial = [_gpu_step(w, x, 2) for w, x in zip(ws_, xs)]
+    devs = [U.to_dev(x) for x in xs]
+    results = [None] * 4
+    errors = []
+
+    def run(i):
+        try:
+            w, d = ws_[i], devs[i]
+            sh = U.shape_of(w)
+            st = torch.cuda.Stream()
+            out = torch.empty((2, w.batch, 1, w.q_heads, w.head_dim), dtype=torch.bfloat16,
+                              device="cuda")
+            lse = torch.empty((2, w.batch, 1, w.q_heads), device="cuda")
+            idx = torch.empty((w.batch, 1, w.top_k), dtype=torch.int32, device="cuda")
+            ns = torch.empty((w.batch, 1), dtype=torch.int32, device="cuda")
+            ws = B.workspace(sh, B.CLSA_OP_DECODE, 2)
+            torch.cuda.synchronize()
+            for _ in range(5):
+                B.clsa_decode_step(sh, d["q_idx"], d["k_idx"], d["k_cache"], d["v_cache"],
+                                   d["page_table"], d["seq_lens"], d["q_pos"], d["q_layers"],
+                                   out, lse, idx, ns, ws, st)
+            st.synchronize()
+            results[i] = (B.bits_from_bf16(out), lse.cpu().numpy().astype(np.float64),
+                          idx.cpu().numpy(), ns.cpu().numpy())
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    th = [threading.Thread(target=run, args=(i,)) for i in range(4)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert not errors, errors
+    for a, b in zip(serial, results):
+        for u, v in zip(a, b):
+            np.testing.assert_array_equal(u, v)
 
 
 def _grouped(w, q_idx_sets, k_idx_sets, x, group, stride_q, stride_k):

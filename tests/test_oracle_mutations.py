@@ -54,8 +54,8 @@ MUTANTS = {
     "destination_ignores_page_table": ("(int64_t)token_row(s, page_table, b, p, 1);",
                                        "(int64_t)((size_t)b * (size_t)s->max_len + (size_t)p);"),
     "drop_first_index_component": ("for (int i = 0; i < d_idx; i++)", "for (int i = 1; i < d_idx; i++)"),
-    "index_key_off_by_one_token": ("token_row(s, page_table, b, j, (size_t)d_idx)",
-                                   "token_row(s, page_table, b, (j + 1) % s->max_len, (size_t)d_idx)"),
+    "index_key_off_by_one_token": ("token_row(s, a->page_table, b, j, (size_t)d_idx)",
+                                   "token_row(s, a->page_table, b, (j + 1) % s->max_len, (size_t)d_idx)"),
     "select_lowest_scores": ("if (a->s > b->s) return -1;\n    if (a->s < b->s) return 1;",
                              "if (a->s < b->s) return -1;\n    if (a->s > b->s) return 1;"),
     "ties_to_highest_index": ("return (a->j > b->j) - (a->j < b->j);",
@@ -66,8 +66,8 @@ MUTANTS = {
                          "int lim = q_pos[(size_t)b * s->n_q + t];"),
     "gqa_modulo_mapping": ("const int g = h / group;", "const int g = h % Hkv;"),
     "no_softmax_scale": ("z[i] = s->softmax_scale * acc;", "z[i] = acc;"),
-    "keys_read_from_values": ("const uint16_t *kr = k_cache + token_row(s, page_table, b, S[i]",
-                              "const uint16_t *kr = v_cache + token_row(s, page_table, b, S[i]"),
+    "keys_read_from_values": ("const uint16_t *kr = a->k_cache + token_row(s, a->page_table, b, S[i]",
+                              "const uint16_t *kr = a->v_cache + token_row(s, a->page_table, b, S[i]"),
     "unnormalised_weights": ("const double w = exp(z[i] - zmax) / denom;",
                              "const double w = exp(z[i] - zmax);"),
     "lse_without_max": ("lse[r * Hq + h] = zmax + log(denom);", "lse[r * Hq + h] = log(denom);"),
@@ -83,7 +83,7 @@ def _build_mutant(tmp_path, name, find, repl):
     msrc.write_text(src.replace(find, repl))
     (tmp_path / "clsa_oracle.h").write_text(open(SRC.replace(".c", ".h")).read())
     lib = tmp_path / f"lib{name}.so"
-    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-o", str(lib), str(msrc), "-lm"],
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", "-o", str(lib), str(msrc), "-lm"],
                    check=True)
     return str(lib)
 
