@@ -89,8 +89,13 @@ typedef enum {
     CLSA_ERR_INVALID_ARG = -1, /* null/misaligned pointer, non-positive size, ... */
     CLSA_ERR_UNSUPPORTED = -2, /* a shape outside the compiled set               */
     CLSA_ERR_WORKSPACE = -3,   /* ws NULL or smaller than clsa_workspace_bytes()  */
-    CLSA_ERR_HIP = -4          /* the HIP runtime reported an error on enqueue   */
+    CLSA_ERR_HIP = -4,         /* the HIP runtime reported an error on enqueue   */
+    CLSA_ERR_SCRATCH_LIMIT = -5 /* clsa_decode_step_noalloc: the step needs more  */
+                                /* scratch than CLSA_NOALLOC_SCRATCH_BYTES        */
 } clsa_status;
+
+/* Size of the fixed per-device scratch of clsa_decode_step_noalloc. */
+#define CLSA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
 
 /* Bits reported by clsa_get_device_error(). */
 enum {
@@ -168,6 +173,26 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
                              const int32_t *q_pos, int32_t n_layers, const void *q_layers,
                              void *out_layers, float *lse_layers, int32_t *idx, int32_t *n_sel,
                              void *ws, size_t ws_bytes, void *stream);
+
+/* clsa_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same computation, arguments and results, but no workspace argument.  The
+ * step's scratch is a fixed device array inside the library, one per device,
+ * of CLSA_NOALLOC_SCRATCH_BYTES (32 MiB), held until the process ends; its
+ * address is looked up on the first call on each device.  The call allocates
+ * nothing and calls no allocating routine.  A shape whose step needs more
+ * than that (clsa_workspace_bytes(shape, CLSA_OP_DECODE, n_layers) >
+ * CLSA_NOALLOC_SCRATCH_BYTES, e.g. thousands of query rows) is rejected with
+ * CLSA_ERR_SCRATCH_LIMIT before anything is enqueued.  Every call on one
+ * device uses that device's one array (whatever is left in it from the last
+ * call is cleared or overwritten as the step needs): calls that overlap in
+ * time on one device, from any stream or thread, race and must not be made. */
+clsa_status clsa_decode_step_noalloc(const clsa_shape *shape, const void *q_idx,
+                                     const void *k_idx, const void *k_cache, const void *v_cache,
+                                     const int32_t *page_table, const int32_t *seq_lens,
+                                     const int32_t *q_pos, int32_t n_layers, const void *q_layers,
+                                     void *out_layers, float *lse_layers, int32_t *idx,
+                                     int32_t *n_sel, void *stream);
 
 /* The same step with the routing refreshed every `group` layers, for measuring
  * what the shared routing saves (Section 3.4 and Appendix D compare per-layer

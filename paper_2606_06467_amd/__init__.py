@@ -9,7 +9,7 @@ generator can be used without torch or a GPU.
 
 _BINDING_NAMES = (
     "clsa_index_scores", "clsa_topk", "clsa_sparse_attn", "clsa_decode_step",
-    "clsa_decode_step_grouped", "clsa_dense_attn", "clsa_project_append", "clsa_kd_target",
+    "clsa_decode_step_grouped", "clsa_decode_step_noalloc", "clsa_dense_attn", "clsa_project_append", "clsa_kd_target",
     "clsa_kd_loss", "clsa_workspace_bytes", "clsa_status_string", "clsa_set_phase_events",
     "clsa_get_device_error",
     "ClsaShape", "ClsaError", "make_shape", "workspace", "HipEvents", "lib",

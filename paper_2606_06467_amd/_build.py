@@ -13,7 +13,7 @@ LIB = os.path.join(PKG, "libclsa.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["index_decode.hip", "index_prefill.hip", "topk.hip", "sparse_attn.hip", "project.hip",
-           "kd.hip",
+           "kd.hip", "noalloc.hip",
            "api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -23,6 +23,8 @@ CLSA_ERR_INVALID_ARG = -1
 CLSA_ERR_UNSUPPORTED = -2
 CLSA_ERR_WORKSPACE = -3
 CLSA_ERR_HIP = -4
+CLSA_ERR_SCRATCH_LIMIT = -5
+CLSA_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 CLSA_OP_INDEX = 0
 CLSA_OP_TOPK = 1
@@ -80,6 +82,7 @@ def lib() -> ctypes.CDLL:
         "clsa_topk": (i32, [SP, P, P, P, P, P, P, sz, P]),
         "clsa_sparse_attn": (i32, [SP, P, P, P, P, P, P, P, P, P, sz, P]),
         "clsa_decode_step": (i32, [SP, P, P, P, P, P, P, P, i32, P, P, P, P, P, P, sz, P]),
+        "clsa_decode_step_noalloc": (i32, [SP, P, P, P, P, P, P, P, i32, P, P, P, P, P, P]),
         "clsa_decode_step_grouped": (i32, [SP, P, i64, P, i64, P, P, P, P, P, i32, i32, P, P, P,
                                            P, P, P, sz, P]),
         "clsa_dense_attn": (i32, [SP, P, P, P, P, P, P, P, P, P, sz, P]),
@@ -163,6 +166,18 @@ def clsa_decode_step(shape, q_idx, k_idx, k_cache, v_cache, page_table, seq_lens
                                   _ptr(out_layers, "out_layers"), _ptr(lse_layers, "lse_layers"),
                                   _ptr(idx, "idx"), _ptr(n_sel, "n_sel"), _ptr(ws, "ws"), wsb,
                                   _stream(stream)), "clsa_decode_step")
+
+
+def clsa_decode_step_noalloc(shape, q_idx, k_idx, k_cache, v_cache, page_table, seq_lens, q_pos,
+                             q_layers, out_layers, lse_layers, idx, n_sel, stream=None):
+    """clsa_decode_step on the library's fixed per-device scratch (no workspace)."""
+    n_layers = 0 if q_layers is None else int(q_layers.shape[0])
+    _check(lib().clsa_decode_step_noalloc(
+        ctypes.byref(shape), _ptr(q_idx, "q_idx"), _ptr(k_idx, "k_idx"), _ptr(k_cache, "k_cache"),
+        _ptr(v_cache, "v_cache"), _ptr(page_table, "page_table"), _ptr(seq_lens, "seq_lens"),
+        _ptr(q_pos, "q_pos"), n_layers, _ptr(q_layers, "q_layers"), _ptr(out_layers, "out_layers"),
+        _ptr(lse_layers, "lse_layers"), _ptr(idx, "idx"), _ptr(n_sel, "n_sel"), _stream(stream)),
+        "clsa_decode_step_noalloc")
 
 
 def clsa_decode_step_grouped(shape, q_idx, q_idx_group_stride, k_idx, k_idx_group_stride,

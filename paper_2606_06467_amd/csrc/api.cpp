@@ -105,7 +105,8 @@ clsa_status check_common(const clsa_shape *s, const int32_t *page_table, const i
 
 // Device limit on LDS per workgroup, one entry per device (0 = not read yet).
 // Threads that race on an entry store the same value, so relaxed atomics suffice.
-constexpr int kMaxDevices = 64;
+using clsa::kMaxDevices;
+static_assert(CLSA_NOALLOC_SCRATCH_BYTES == clsa::kNoallocScratchBytes, "one scratch size");
 std::atomic<int> g_lds_limit[kMaxDevices];
 
 clsa_status check_topk_lds(const Geometry &g) {
@@ -404,6 +405,24 @@ clsa_status clsa_decode_step(const clsa_shape *shape, const void *q_idx, const v
                             ws, ws_bytes, stream);
 }
 
+clsa_status clsa_decode_step_noalloc(const clsa_shape *shape, const void *q_idx,
+                                     const void *k_idx, const void *k_cache, const void *v_cache,
+                                     const int32_t *page_table, const int32_t *seq_lens,
+                                     const int32_t *q_pos, int32_t n_layers, const void *q_layers,
+                                     void *out_layers, float *lse_layers, int32_t *idx,
+                                     int32_t *n_sel, void *stream) {
+    Geometry g;
+    CLSA_TRY(check_shape(shape, kIndex | kTopk | kAttn, &g));
+    DecodeWs w;
+    if (carve_decode(g, nullptr, w) > clsa::kNoallocScratchBytes) return CLSA_ERR_SCRATCH_LIMIT;
+    void *scratch = nullptr;
+    CLSA_TRY(from_hip(clsa::noalloc_scratch(&scratch)));
+    const int32_t group = n_layers > 0 ? n_layers : 1;
+    return decode_step_impl(shape, q_idx, 0, k_idx, 0, k_cache, v_cache, page_table, seq_lens,
+                            q_pos, n_layers, group, q_layers, out_layers, lse_layers, idx, n_sel,
+                            scratch, clsa::kNoallocScratchBytes, stream);
+}
+
 clsa_status clsa_decode_step_grouped(const clsa_shape *shape, const void *q_idx,
                                      int64_t q_idx_group_stride, const void *k_idx,
                                      int64_t k_idx_group_stride, const void *k_cache,
@@ -523,6 +542,7 @@ const char *clsa_status_string(clsa_status status) {
         case CLSA_ERR_UNSUPPORTED: return "CLSA_ERR_UNSUPPORTED";
         case CLSA_ERR_WORKSPACE: return "CLSA_ERR_WORKSPACE";
         case CLSA_ERR_HIP: return "CLSA_ERR_HIP";
+        case CLSA_ERR_SCRATCH_LIMIT: return "CLSA_ERR_SCRATCH_LIMIT";
     }
     return "CLSA_ERR_UNKNOWN";
 }

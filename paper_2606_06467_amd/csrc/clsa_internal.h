@@ -36,6 +36,17 @@ constexpr int kTopkWideMaxRows = 128;
 
 __host__ __device__ inline int div_up(int a, int b) { return (a + b - 1) / b; }
 
+// Devices for which host-side per-device tables have an entry.
+constexpr int kMaxDevices = 64;
+
+// ---- noalloc.hip ----
+// Size of the fixed per-device scratch of clsa_decode_step_noalloc (covers the
+// decode steps of up to 32 sequences of 65536 tokens, or 4 of 131072).
+constexpr size_t kNoallocScratchBytes = (size_t)32 << 20;
+// Device address of the current device's copy of that scratch (looked up once
+// per device with that device current).
+hipError_t noalloc_scratch(void **ptr);
+
 // Device error bits (CLSA_DEVERR_* of clsa.h) raised by the kernels of each
 // source file on the current device: OR-ed into *bits, then cleared there.
 // Synchronous copies (a debug path).
