@@ -66,8 +66,12 @@ def algorithmic_bytes(w, x):
     # one sparse-attention launch: the selected K/V rows of every row, its query
     # and its index list (the output leaves through the split merge)
     attn = kv_rows + w.batch * w.n_q * (w.q_heads * w.head_dim * 2 + w.top_k * 4)
+    # matrix FLOPs of one attention launch: q.k and the weighted V, 2 x 2 x head_dim
+    # per (row, query head, selected token)
+    attn_flops = sel * w.q_heads * w.head_dim * 4
     return dict(index=index_keys + scores, step=index_keys + scores + kv_rows + qo + idx,
-                kv_rows=kv_rows, attn=attn, index_flops=2 * w.idx_heads * w.idx_dim * int(n.sum()))
+                kv_rows=kv_rows, attn=attn, attn_flops=attn_flops,
+                index_flops=2 * w.idx_heads * w.idx_dim * int(n.sum()))
 
 
 KERNEL_SOURCES = {
@@ -188,6 +192,42 @@ def cpu_baseline(w, x, budget_s: float):
                   f"to all rows (extrapolated)")
     return {"value": round(us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
             "sample": sample, "host_cpus_available": avail, "cpu_model": model}
+
+
+def cold_read_reference(dev, stream, n_bytes: int, reps: int = 7):
+    """What one launch reading ``n_bytes`` from HBM cold achieves on this GPU:
+    the library's decode indexer (a coalesced 16-byte streaming read of index
+    keys, 1 FLOP per byte) over a key set of ``n_bytes``, timed with events
+    around the launch exactly as the attention layers are, each time after a
+    2 GiB read that evicts the 256 MB Infinity Cache.  Median of ``reps``."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    batch = 4
+    n = max(64, n_bytes // (batch * 512))
+    sh = B.make_shape(batch=batch, n_q=1, max_len=n, top_k=64)
+    q = torch.zeros((batch, 1, 4, 64), dtype=torch.bfloat16, device=dev)
+    k = torch.ones((batch, n, 4, 64), dtype=torch.bfloat16, device=dev)
+    lens = torch.full((batch,), n, dtype=torch.int32, device=dev)
+    scores = torch.empty((batch, 1, n), dtype=torch.float32, device=dev)
+    flush = torch.ones(2 << 30, dtype=torch.uint8, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t = []
+    for r in range(reps + 1):
+        flush.sum(dtype=torch.int32)
+        e0.record(stream)
+        B.clsa_index_scores(sh, q, k, None, lens, None, scores, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if r:
+            t.append(e0.elapsed_time(e1))
+    us = float(np.median(t)) * 1e3
+    read = batch * n * 512
+    del q, k, lens, scores, flush
+    return {"kernel": "index_decode_kernel", "bytes": read, "us": round(us, 2),
+            "achieved_GBps": round(read / (us * 1e-6) / 1e9, 1),
+            "frac_of_hbm_peak": round(read / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "note": "one launch streaming this many bytes cold (Infinity Cache evicted), "
+                    "timed between events like the attention layers"}
 
 
 def copy_reference(mib: int, dev) -> None:
@@ -597,6 +637,9 @@ def main() -> int:
         del g
     attn_ms = float(attn.mean())
     attn_first_ms = float(attn[:, 0].mean())
+    attn_warm_ms = float(attn[:, 1:].mean()) if L > 1 else attn_first_ms
+    prefill = w.n_q >= PREFILL_MIN_ROWS
+    cold_ref = None if prefill else cold_read_reference(dev, stream, algorithmic_bytes(w, x)["attn"])
 
     if args.copy_mib > 0:
         copy_reference(args.copy_mib, dev)
@@ -630,12 +673,24 @@ def main() -> int:
                       "attn_kernel": round(attn_ms * 1e3, 2),
                       "attn_kernel_first_layer": round(attn_first_ms * 1e3, 2)},
         # the kernel with the largest share of the step: the sparse-attention
-        # kernel, launched once per layer
-        "roofline": roofline("sparse_attn_kernel", w, ab["attn"], attn_ms),
+        # kernel, launched once per layer.  Decode: bound by reading its rows
+        # (HBM for the first layer after the top-k, the caches after); chunked
+        # prefill: most of its 68.7 GB of logical gathers per layer are served by
+        # the caches, so it is priced by its matrix FLOPs
+        "roofline": (roofline_mfma("sparse_attn_kernel", w, ab["attn_flops"], attn_ms)
+                     if prefill else roofline("sparse_attn_kernel", w, ab["attn"], attn_ms)),
         "roofline_index": (roofline_mfma("index_prefill_kernel", w, ab["index_flops"], index_ms)
                            if w.n_q >= PREFILL_MIN_ROWS else
                            roofline("index_decode_kernel", w, ab["index"], index_ms)),
     }
+    if prefill:
+        res["roofline"]["logical_gather_bytes_per_launch"] = ab["attn"]
+    else:
+        cold = roofline("sparse_attn_kernel", w, ab["attn"], attn_first_ms)
+        cold["frac_of_cold_read_reference"] = round(cold_ref["us"] / (attn_first_ms * 1e3), 4)
+        res["roofline_cold_layer"] = cold
+        res["roofline_warm_layers"] = roofline("sparse_attn_kernel", w, ab["attn"], attn_warm_ms)
+        res["cold_read_reference"] = cold_ref
     if graph_us is not None:
         res["graph_us_per_step"] = round(graph_us, 2)
     if args.cpu_budget > 0:

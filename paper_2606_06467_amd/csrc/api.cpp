@@ -167,6 +167,11 @@ struct DecodeWs {
     size_t zero_count = 0;
     clsa::TopkBuffers topk{};
     float *partials = nullptr;
+    // two-pass chunked-prefill top-k
+    float *samples = nullptr;      // [rows, sample columns]
+    uint32_t *thresh = nullptr;    // [rows]
+    uint32_t *cand_count = nullptr;  // [rows, key blocks]
+    uint32_t *cands = nullptr;     // [rows, key blocks, kTopkBlockSlots, 2]
 };
 
 // Every layer gathers its K/V rows from the cache through the shared index set.
@@ -186,6 +191,13 @@ size_t carve_decode(const Geometry &g, void *base, DecodeWs &w) {
         w.topk.counts = c.take<uint32_t>(L.count_u32);
     }
     w.partials = c.take<float>(clsa::attn_partial_floats(g));
+    if (clsa::topk_uses_two_pass(g)) {
+        w.samples = c.take<float>((size_t)g.rows * clsa::topk_sample_cols(g));
+        w.thresh = c.take<uint32_t>(g.rows);
+        const size_t blocks = (size_t)g.rows * clsa::topk_key_blocks(g);
+        w.cand_count = c.take<uint32_t>(blocks);
+        w.cands = c.take<uint32_t>(blocks * clsa::kTopkBlockSlots * 2);
+    }
     return c.off;
 }
 
@@ -349,6 +361,10 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
     // without the coarse histogram, which the top-k then makes itself.  The
     // histogram needs clearing unless that top-k is the per-row one.
     const bool mfma = clsa::index_uses_mfma(g);
+    // Many causal rows with a moderate k: the scores are never written; a
+    // sampled pass sets each row's candidate threshold and a second pass
+    // emits the candidates (see topk.hip).
+    const bool two_pass = clsa::topk_uses_two_pass(g);
     const size_t q_stride = (size_t)g.rows * g.q_heads * 128;  // bf16 elements per layer
     const size_t lse_stride = (size_t)g.rows * g.q_heads;
     const size_t set_stride = (size_t)g.rows * g.top_k;         // index entries per set
@@ -359,18 +375,32 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
         int32_t *is = idx + (size_t)s * set_stride;
         int32_t *ns = n_sel + (size_t)s * g.rows;
         const bool first = s == 0;
-        if (!mfma || clsa::topk_uses_wide(g))
-            CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
-        if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
-        if (mfma)
-            CLSA_TRY(from_hip(clsa::launch_index_prefill(g, qi, ki, page_table, seq_lens, q_pos,
-                                                         w.scores, st)));
-        else
-            CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
-                                                        w.scores, w.topk.hist, st)));
-        if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
-        CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, is, ns,
-                                            st)));
+        if (two_pass) {
+            if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+            CLSA_TRY(from_hip(clsa::launch_index_prefill_sample(g, qi, ki, page_table, seq_lens,
+                                                                q_pos, w.samples, st)));
+            CLSA_TRY(from_hip(clsa::launch_topk_sample_thresh(g, w.samples, seq_lens, q_pos,
+                                                              w.thresh, st)));
+            CLSA_TRY(from_hip(clsa::launch_index_prefill_emit(g, qi, ki, page_table, seq_lens,
+                                                              q_pos, w.thresh, w.cand_count,
+                                                              w.cands, st)));
+            if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
+            CLSA_TRY(from_hip(clsa::launch_topk_cands(g, w.cand_count, w.cands, seq_lens, q_pos,
+                                                      qi, ki, page_table, w.scores, is, ns, st)));
+        } else {
+            if (!mfma || clsa::topk_uses_wide(g))
+                CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
+            if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
+            if (mfma)
+                CLSA_TRY(from_hip(clsa::launch_index_prefill(g, qi, ki, page_table, seq_lens,
+                                                             q_pos, w.scores, st)));
+            else
+                CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
+                                                            w.scores, w.topk.hist, st)));
+            if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
+            CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, is,
+                                                ns, st)));
+        }
         if (first && hook && hipEventRecord(t_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;
         const int l_end = n_layers < (s + 1) * group ? n_layers : (s + 1) * group;
         for (int l = s * group; l < l_end; ++l) {

@@ -72,6 +72,44 @@ hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void
                                 const int32_t *page_table, const int32_t *seq_lens,
                                 const int32_t *q_pos, float *scores, hipStream_t stream);
 
+// ---- two-pass chunked-prefill top-k (index_prefill.hip, topk.hip) ----
+// Every kTopkSampleStride-th key of each row is scored first; the threshold of
+// the candidate pass is the rank-th largest sampled score, rank =
+// topk_sample_rank(g).  Used for many causal rows with top_k <= kTopkTwoPassMaxK.
+constexpr int kTopkSampleStride = 32;
+constexpr int kTopkTwoPassMaxK = 2048;
+// Candidate slots per (row, block of kTopkKeyBlock keys) of the second pass.
+// The path is chosen only where a full-length row expects at most
+// kTopkBlockMean candidates per block (Poisson tail past 48: ~1e-14).
+constexpr int kTopkKeyBlock = 256;
+constexpr int kTopkBlockSlots = 48;
+constexpr int kTopkBlockMean = 12;
+inline int topk_sample_cols(const Geometry &g) { return div_up(g.max_len, kTopkSampleStride); }
+inline int topk_key_blocks(const Geometry &g) { return div_up(g.max_len, kTopkKeyBlock); }
+bool topk_uses_two_pass(const Geometry &g);
+int topk_sample_rank(const Geometry &g);
+// Pass 1: sampled scores [rows, topk_sample_cols(g)].
+hipError_t launch_index_prefill_sample(const Geometry &g, const void *q_idx, const void *k_idx,
+                                       const int32_t *page_table, const int32_t *seq_lens,
+                                       const int32_t *q_pos, float *samples, hipStream_t stream);
+// Per-row thresholds (order-preserving keys) from the samples.
+hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
+                                     const int32_t *seq_lens, const int32_t *q_pos,
+                                     uint32_t *thresh, hipStream_t stream);
+// Pass 2: cand_count [rows, topk_key_blocks(g)] and cands [rows,
+// topk_key_blocks(g), kTopkBlockSlots] of (key, position) pairs (every block a
+// row sees gets its count written; no clearing needed).
+hipError_t launch_index_prefill_emit(const Geometry &g, const void *q_idx, const void *k_idx,
+                                     const int32_t *page_table, const int32_t *seq_lens,
+                                     const int32_t *q_pos, const uint32_t *thresh,
+                                     uint32_t *cand_count, uint32_t *cands, hipStream_t stream);
+// Exact selection from the candidates; rows whose candidates do not decide
+// the set recompute their scores into scores [rows, max_len].
+hipError_t launch_topk_cands(const Geometry &g, const uint32_t *cand_count, const uint32_t *cands,
+                             const int32_t *seq_lens, const int32_t *q_pos, const void *q_idx,
+                             const void *k_idx, const int32_t *page_table, float *scores,
+                             int32_t *idx, int32_t *n_sel, hipStream_t stream);
+
 // ---- topk.hip ----
 struct TopkWideLayout {
     int words_max, regions;  // per row: bitmap words, 1024-key candidate regions

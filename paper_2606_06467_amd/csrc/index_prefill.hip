@@ -31,6 +31,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kPfWaveKeys = 64;                // keys per wave (four 16-row tiles)
 constexpr int kPfKeys = 4 * kPfWaveKeys;        // keys per workgroup
 constexpr int kIdxDim = 256;
+static_assert(kPfKeys == kTopkKeyBlock, "a workgroup's keys are one candidate block");
 
 struct PrefillArgs {
     const uint16_t *q_idx;
@@ -38,10 +39,16 @@ struct PrefillArgs {
     const int32_t *page_table;
     const int32_t *seq_lens;
     const int32_t *q_pos;
-    float *scores;
+    float *scores;            // scores: [rows, row_stride]
+    const uint32_t *thresh;   // EMIT: [rows] candidate threshold (order-preserving key)
+    uint32_t *cand_count;     // EMIT: [rows, kblocks] candidates per key block (may exceed the slots)
+    uint2 *cands;             // EMIT: [rows, kblocks, kTopkBlockSlots] (key, position)
     int n_q, max_len, page_shift, max_pages, causal;
-    int kblocks;      // key blocks per sequence
-    int vec_store;    // max_len % 4 == 0: rows are 16-byte aligned
+    int kblocks;      // key blocks per sequence (of sampled keys when key_stride > 1)
+    int vec_store;    // row_stride % 4 == 0: rows are 16-byte aligned
+    int key_stride;   // 1, or S: a block's keys are positions 0, S, 2S, ... (the sample pass)
+    int row_stride;   // floats per score row
+    int qsplit;       // query-tile ranges per sequence (workgroups per key block)
 };
 
 __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t *p) {
@@ -60,6 +67,12 @@ template <bool CAUSAL>
 __device__ __forceinline__ int key_limit(int pos, int len, int n_q, int t) {
     const int n = CAUSAL ? min(len, max(pos + 1, 0)) : len;
     return t < n_q ? n : 0;
+}
+
+// Keys of the workgroup are key indices m (positions m * key_stride); a row
+// that sees the first n positions sees the first ceil(n / key_stride) of them.
+__device__ __forceinline__ int strided_limit(int n, int stride) {
+    return stride == 1 ? n : (n + stride - 1) / stride;
 }
 
 // LDS staging of one query tile's scores: 16 rows x the workgroup's 256 keys
@@ -123,7 +136,7 @@ __device__ __forceinline__ void store_tile(const PrefillArgs &a, const float (*t
         const int nr = __builtin_amdgcn_readlane(n, rr);
         if (j0 >= nr) continue;
         const f32x4 v = *reinterpret_cast<const f32x4 *>(&tile[rr][4 * lane]);
-        float *dst = a.scores + ((size_t)b * a.n_q + qt * 16 + rr) * a.max_len + j0;
+        float *dst = a.scores + ((size_t)b * a.n_q + qt * 16 + rr) * a.row_stride + j0;
         if (a.vec_store && j0 + 4 <= nr) {
             __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
         } else {
@@ -132,6 +145,19 @@ __device__ __forceinline__ void store_tile(const PrefillArgs &a, const float (*t
                 if (j0 + r < nr) dst[r] = v[r];
         }
     }
+}
+
+// Scores of one query tile against the wave's 64 keys, left in registers:
+// c[kt][r] is key jw + 16 kt + 4 grp + r of query col.
+__device__ __forceinline__ void score_regs(const bf16x8 (&kv)[4][8], const bf16x8 (&qv)[8],
+                                           f32x4 (&c)[4]) {
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) c[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb)
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+            c[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv[kt][kb], qv[kb], c[kt], 0, 0, 0);
 }
 
 // Workgroup: 256 keys of one sequence against all of its query tiles.  Per
@@ -144,24 +170,35 @@ __device__ __forceinline__ void store_tile(const PrefillArgs &a, const float (*t
 // before it; issuing a tile's stores only after the next tile's queries have
 // arrived keeps the stores' completion out of the wait.  Tiles whose rows all
 // end before the workgroup's first key (causal) compute and store nothing.
-template <bool PAGED, bool CAUSAL>
+// EMIT (the second pass of the chunked-prefill top-k): instead of storing the
+// scores, append each row's candidates (scores at or above its threshold) to
+// its list.  With key_stride S > 1 (the first pass) the block's keys are every
+// S-th position and the scores go to a [rows, row_stride] sample matrix.
+// Workgroups of one key block split the query tiles into qsplit ranges.
+template <bool PAGED, bool CAUSAL, bool EMIT>
 __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
-    const int b = blockIdx.x / a.kblocks;
-    const int kblk = blockIdx.x - b * a.kblocks;
+    const int per_seq = a.kblocks * a.qsplit;
+    const int b = blockIdx.x / per_seq;
+    const int kblk = (blockIdx.x - b * per_seq) / a.qsplit;
+    const int qs = blockIdx.x - b * per_seq - kblk * a.qsplit;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int col = lane & 15, grp = lane >> 4;
-    const int len = clamp_len(a.seq_lens[b], a.max_len);
+    const int stride = a.key_stride;
+    const int len_pos = clamp_len(a.seq_lens[b], a.max_len);  // positions
+    const int len = strided_limit(len_pos, stride);           // keys (of this pass)
     const int jg = kblk * kPfKeys;                       // first key of this workgroup
     const int jw = jg + wave * kPfWaveKeys;              // first key of this wave
     if (jg >= len) return;                               // uniform over the workgroup
-    __shared__ float tile[2][16][kTileStride];
+    __shared__ float tile[EMIT ? 1 : 2][16][kTileStride];
     __shared__ __align__(16) uint16_t s_q[2][16][kQStride];  // query tiles (bf16)
+    // EMIT: candidates per (query, wave, lane group) of a tile, two tiles in turn
+    __shared__ __align__(16) uint32_t s_cnt[EMIT ? 2 : 1][16][16];
 
     // the wave's 64 keys as A operands: key tile kt, row col = key jw + 16*kt + col
     bf16x8 kv[4][8];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-        const int j = min(jw + 16 * kt + col, len - 1);  // clamped keys are never stored
+        const int j = min(jw + 16 * kt + col, len - 1) * stride;  // clamped keys are never stored
         size_t off;
         if (PAGED) {
             const int page = a.page_table[(size_t)b * a.max_pages + (j >> a.page_shift)];
@@ -173,43 +210,110 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
         for (int kb = 0; kb < 8; ++kb) kv[kt][kb] = load_bf16x8(a.k_idx + off + grp * 8 + kb * 32);
     }
 
-    const int ntiles = div_up(a.n_q, 16);
+    const int ntiles_all = div_up(a.n_q, 16);
+    const int tpw = div_up(ntiles_all, a.qsplit);        // query tiles of each range
+    const int qt0 = qs * tpw;
+    const int qt_end = min(ntiles_all, qt0 + tpw);
+    if (qt0 >= qt_end) return;                           // uniform
     const int32_t *qpos = CAUSAL ? a.q_pos + (size_t)b * a.n_q : nullptr;
     // Query tiles go through LDS, each loaded once per workgroup: wave w loads
     // queries 4w .. 4w+3 of a tile (lane: 32 bytes of query 4w + (lane >> 4)),
     // a tile ahead, and writes them to s_q after the next wait.
     const int sq_row = wave * 4 + (lane >> 4), sq_col = (lane & 15) * 16;
-    u32x4 qs[2];
+    u32x4 qs_v[2];
     auto load_quarter = [&](int qt) {
         const int t = min(qt * 16 + sq_row, a.n_q - 1);  // rows past n_q: never stored
         const uint16_t *p = a.q_idx + ((size_t)b * a.n_q + t) * kIdxDim + sq_col;
-        qs[0] = *reinterpret_cast<const u32x4 *>(p);
-        qs[1] = *reinterpret_cast<const u32x4 *>(p + 8);
+        qs_v[0] = *reinterpret_cast<const u32x4 *>(p);
+        qs_v[1] = *reinterpret_cast<const u32x4 *>(p + 8);
     };
     auto stage_quarter = [&](int buf) {
-        *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col]) = qs[0];
-        *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col + 8]) = qs[1];
+        *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col]) = qs_v[0];
+        *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col + 8]) = qs_v[1];
     };
-    int p_cur = key_pos<CAUSAL>(qpos, a.n_q, col);  // raw positions, a tile ahead
-    load_quarter(0);
+    // row thresholds (EMIT), a tile ahead like the key limits
+    auto load_thresh = [&](int qt) -> uint32_t {
+        return EMIT ? a.thresh[(size_t)b * a.n_q + min(qt * 16 + col, a.n_q - 1)] : 0u;
+    };
+    int p_cur = key_pos<CAUSAL>(qpos, a.n_q, qt0 * 16 + col);  // raw positions, a tile ahead
+    uint32_t th_cur = load_thresh(qt0);
+    load_quarter(qt0);
     __builtin_amdgcn_s_waitcnt(kPfWaitVm0);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    stage_quarter(0);
-    if (ntiles > 1) load_quarter(1);
+    stage_quarter(qt0 & 1);
+    if (qt0 + 1 < qt_end) load_quarter(qt0 + 1);
     pf_lds_barrier();
     int n_prev = 0;       // key limits of the tile staged in LDS, not yet stored
+    uint32_t th_prev = 0;
     bool staged = false;
-    for (int qt = 0; qt < ntiles; ++qt) {
+    // EMIT (the second pass of the chunked-prefill top-k): a key is a candidate
+    // when it is valid for its query and its order-preserving score key is at
+    // least the query's threshold.  The tile's scores stay in registers; each
+    // lane counts its candidates into s_cnt, and after the tile's barrier (in
+    // the next iteration, after its wait, so that no wait covers these stores)
+    // it takes its slots of the (query, key block) list: those of the lanes
+    // before it in (wave, lane group) order.  Each (query, key block) list is
+    // written by this workgroup alone, so no atomics are needed; its count is
+    // written in full (a count past the slots sends the row to the exact
+    // fallback of the top-k).
+    f32x4 e_c[4];
+    uint32_t e_mask = 0u;
+    int e_qt = -1;
+    auto emit_store = [&]() {
+        if (!EMIT || e_qt < 0) return;
+        const uint32_t *cs = &s_cnt[e_qt & 1][col][0];
+        const u32x4 c0 = *reinterpret_cast<const u32x4 *>(cs);
+        const u32x4 c1 = *reinterpret_cast<const u32x4 *>(cs + 4);
+        const u32x4 c2 = *reinterpret_cast<const u32x4 *>(cs + 8);
+        const u32x4 c3 = *reinterpret_cast<const u32x4 *>(cs + 12);
+        const uint32_t cnt[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
+                                  c2.x, c2.y, c2.z, c2.w, c3.x, c3.y, c3.z, c3.w};
+        const int me = wave * 4 + grp;
+        uint32_t before = 0, total = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            before += i < me ? cnt[i] : 0u;
+            total += cnt[i];
+        }
+        const int t = e_qt * 16 + col;
+        if (t < a.n_q) {
+            const size_t blk = (size_t)(b * a.n_q + t) * a.kblocks + kblk;
+            uint2 *dst = a.cands + blk * kTopkBlockSlots;
+            uint32_t slot = before;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if ((e_mask >> (4 * kt + r)) & 1u) {
+                        if (slot < (uint32_t)kTopkBlockSlots)
+                            dst[slot] = make_uint2(score_key(e_c[kt][r]),
+                                                   (uint32_t)(jw + 16 * kt + 4 * grp + r));
+                        ++slot;
+                    }
+                }
+            if (me == 0) a.cand_count[blk] = total;
+        }
+        e_qt = -1;
+    };
+    for (int qt = qt0; qt < qt_end; ++qt) {
         int p_next = 0;
+        uint32_t th_next = 0;
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_waitcnt(kPfWaitVm0);                         // (a)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_sched_barrier(0);
-        const int n_cur = key_limit<CAUSAL>(p_cur, len, a.n_q, qt * 16 + col);
-        if (qt + 1 < ntiles) stage_quarter((qt + 1) & 1);               // tile qt+1's queries
-        if (staged) store_tile(a, tile[(qt - 1) & 1], n_prev, b, qt - 1, jg, wave, lane);  // (b)
-        if (qt + 1 < ntiles) p_next = key_pos<CAUSAL>(qpos, a.n_q, (qt + 1) * 16 + col);  // (c)
-        if (qt + 2 < ntiles) load_quarter(qt + 2);
+        const int n_cur = strided_limit(key_limit<CAUSAL>(p_cur, len_pos, a.n_q, qt * 16 + col), stride);
+        if (qt + 1 < qt_end) stage_quarter((qt + 1) & 1);               // tile qt+1's queries
+        if (EMIT) {                                                     // (b)
+            emit_store();
+        } else if (staged) {
+            store_tile(a, tile[(qt - 1) & 1], n_prev, b, qt - 1, jg, wave, lane);
+        }
+        if (qt + 1 < qt_end) {                                          // (c)
+            p_next = key_pos<CAUSAL>(qpos, a.n_q, (qt + 1) * 16 + col);
+            th_next = load_thresh(qt + 1);
+        }
+        if (qt + 2 < qt_end) load_quarter(qt + 2);
         __builtin_amdgcn_sched_barrier(0);
         staged = tile_limit(n_cur) > jg;                                // uniform
         if (staged) {                                                   // (d)
@@ -218,44 +322,113 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
             for (int kb = 0; kb < 8; ++kb)
                 qv[kb] = __builtin_bit_cast(
                     bf16x8, *reinterpret_cast<const u32x4 *>(&s_q[qt & 1][col][kb * 32 + grp * 8]));
-            score_tile(kv, qv, wave, lane, tile[qt & 1]);
+            if (EMIT) {
+                score_regs(kv, qv, e_c);
+                e_mask = 0u;
+#pragma unroll
+                for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const bool cand = jw + 16 * kt + 4 * grp + r < n_cur &&
+                                          score_key(e_c[kt][r]) >= th_cur;
+                        e_mask |= (cand ? 1u : 0u) << (4 * kt + r);
+                    }
+                s_cnt[qt & 1][col][wave * 4 + grp] = (uint32_t)__popc(e_mask);
+                e_qt = qt;
+            } else {
+                score_tile(kv, qv, wave, lane, tile[qt & 1]);
+            }
         }
         n_prev = n_cur;
+        th_prev = th_cur;
         p_cur = p_next;
+        th_cur = th_next;
         pf_lds_barrier();                                               // (e)
     }
-    if (staged) store_tile(a, tile[(ntiles - 1) & 1], n_prev, b, ntiles - 1, jg, wave, lane);
+    if (EMIT) emit_store();
+    else if (staged) store_tile(a, tile[(qt_end - 1) & 1], n_prev, b, qt_end - 1, jg, wave, lane);
 }
 
 bool index_uses_mfma(const Geometry &g) { return g.n_q >= kPrefillMinRows; }
 
-hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void *k_idx,
+static PrefillArgs prefill_args(const Geometry &g, const void *q_idx, const void *k_idx,
                                 const int32_t *page_table, const int32_t *seq_lens,
-                                const int32_t *q_pos, float *scores, hipStream_t stream) {
-    PrefillArgs a;
+                                const int32_t *q_pos) {
+    PrefillArgs a{};
     a.q_idx = static_cast<const uint16_t *>(q_idx);
     a.k_idx = static_cast<const uint16_t *>(k_idx);
     a.page_table = page_table;
     a.seq_lens = seq_lens;
     a.q_pos = q_pos;
-    a.scores = scores;
     a.n_q = g.n_q;
     a.max_len = g.max_len;
     a.page_shift = g.page_shift;
     a.max_pages = g.max_pages;
     a.causal = g.causal;
-    a.kblocks = div_up(g.max_len, kPfKeys);
-    a.vec_store = (g.max_len % 4) == 0;
-    const size_t blocks = (size_t)g.batch * a.kblocks;
+    a.key_stride = 1;
+    a.qsplit = 1;
+    return a;
+}
+
+template <bool EMIT>
+static hipError_t launch_prefill(const Geometry &g, const PrefillArgs &a, hipStream_t stream) {
+    const size_t blocks = (size_t)g.batch * a.kblocks * a.qsplit;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)blocks), block(256);
     const bool paged = g.page_shift >= 0;
-    if (paged && g.causal) index_prefill_kernel<true, true><<<grid, block, 0, stream>>>(a);
-    else if (paged) index_prefill_kernel<true, false><<<grid, block, 0, stream>>>(a);
-    else if (g.causal) index_prefill_kernel<false, true><<<grid, block, 0, stream>>>(a);
-    else index_prefill_kernel<false, false><<<grid, block, 0, stream>>>(a);
+    if (paged && g.causal) index_prefill_kernel<true, true, EMIT><<<grid, block, 0, stream>>>(a);
+    else if (paged) index_prefill_kernel<true, false, EMIT><<<grid, block, 0, stream>>>(a);
+    else if (g.causal) index_prefill_kernel<false, true, EMIT><<<grid, block, 0, stream>>>(a);
+    else index_prefill_kernel<false, false, EMIT><<<grid, block, 0, stream>>>(a);
     return hipGetLastError();
+}
+
+hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void *k_idx,
+                                const int32_t *page_table, const int32_t *seq_lens,
+                                const int32_t *q_pos, float *scores, hipStream_t stream) {
+    PrefillArgs a = prefill_args(g, q_idx, k_idx, page_table, seq_lens, q_pos);
+    a.scores = scores;
+    a.row_stride = g.max_len;
+    a.kblocks = div_up(g.max_len, kPfKeys);
+    a.vec_store = (g.max_len % 4) == 0;
+    return launch_prefill<false>(g, a, stream);
+}
+
+// Enough workgroups for the chip when a pass has few key blocks: split the
+// query tiles of each key block over ranges.
+static int prefill_qsplit(const Geometry &g, int kblocks) {
+    const int ntiles = div_up(g.n_q, 16);
+    int qsplit = 1;
+    while ((long)g.batch * kblocks * qsplit < 1024 && qsplit * 4 <= ntiles) qsplit *= 2;
+    return qsplit;
+}
+
+hipError_t launch_index_prefill_sample(const Geometry &g, const void *q_idx, const void *k_idx,
+                                       const int32_t *page_table, const int32_t *seq_lens,
+                                       const int32_t *q_pos, float *samples, hipStream_t stream) {
+    PrefillArgs a = prefill_args(g, q_idx, k_idx, page_table, seq_lens, q_pos);
+    a.scores = samples;
+    a.key_stride = kTopkSampleStride;
+    a.row_stride = topk_sample_cols(g);
+    a.kblocks = div_up(a.row_stride, kPfKeys);
+    a.vec_store = (a.row_stride % 4) == 0;
+    a.qsplit = prefill_qsplit(g, a.kblocks);
+    return launch_prefill<false>(g, a, stream);
+}
+
+hipError_t launch_index_prefill_emit(const Geometry &g, const void *q_idx, const void *k_idx,
+                                     const int32_t *page_table, const int32_t *seq_lens,
+                                     const int32_t *q_pos, const uint32_t *thresh,
+                                     uint32_t *cand_count, uint32_t *cands, hipStream_t stream) {
+    PrefillArgs a = prefill_args(g, q_idx, k_idx, page_table, seq_lens, q_pos);
+    a.thresh = thresh;
+    a.cand_count = cand_count;
+    a.cands = reinterpret_cast<uint2 *>(cands);
+    a.row_stride = g.max_len;
+    a.kblocks = div_up(g.max_len, kPfKeys);
+    a.qsplit = prefill_qsplit(g, a.kblocks);
+    return launch_prefill<true>(g, a, stream);
 }
 
 hipError_t take_device_error_index_prefill(uint32_t *bits) { return take_source_device_error(bits); }

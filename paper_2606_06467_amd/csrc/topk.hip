@@ -291,39 +291,27 @@ struct TopkRowArgs {
     int cand_cap;
 };
 
-template <bool HAVE_HIST>
-__global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
+// Steps 1-5 for one row of scores srow[0 .. n-1] (n > k) by one workgroup of
+// kRowThreads, writing k ascending positions to out.  ghist: the row's coarse
+// histogram from the indexer, or null (made here from the scores).  lds:
+// dynamic LDS of row_kernel_lds() bytes.
+__device__ void row_topk(const float *srow, const uint32_t *ghist, int n, int k, int words_max,
+                         int cand_cap, int32_t *out, uint32_t *lds, uint32_t *s_wave,
+                         uint32_t *s_res, uint32_t *s_cand_count) {
     constexpr int NW = kRowThreads / 64;
-    extern __shared__ __align__(16) uint32_t lds[];
-    __shared__ uint32_t s_wave[2 * NW];
-    __shared__ uint32_t s_res[2];
-    __shared__ uint32_t s_cand_count;
-
-    const int row = blockIdx.x;
-    const int b = row / a.n_q;
-    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
-    const int k = a.top_k;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int32_t *out = a.idx + (size_t)row * k;
-    if (n <= k) {  // every valid key is selected
-        for (int i = tid; i < k; i += kRowThreads) out[i] = i < n ? i : -1;
-        if (tid == 0) a.n_sel[row] = n;
-        return;
-    }
-    const float *srow = a.scores + (size_t)row * a.max_len;
     uint32_t *hist = lds;                // kHistWords
     uint32_t *low = hist + kHistWords;   // kLowBins
     uint32_t *sure = low + kLowBins;     // words_max
-    uint32_t *tie = sure + a.words_max;  // words_max
-    uint32_t *ckey = tie + a.words_max;  // cand_cap
-    uint32_t *cidx = ckey + a.cand_cap;  // cand_cap
+    uint32_t *tie = sure + words_max;    // words_max
+    uint32_t *ckey = tie + words_max;    // cand_cap
+    uint32_t *cidx = ckey + cand_cap;    // cand_cap
     const int nchunks = div_up(n, 1024);
 
-    for (int x = tid; x < kCoarseBins; x += kRowThreads)
-        hist[x] = HAVE_HIST ? a.hist[(size_t)row * kCoarseBins + x] : 0u;
-    if (tid == 0) s_cand_count = 0u;
+    for (int x = tid; x < kCoarseBins; x += kRowThreads) hist[x] = ghist ? ghist[x] : 0u;
+    if (tid == 0) *s_cand_count = 0u;
     __syncthreads();
-    if (!HAVE_HIST) {
+    if (!ghist) {
         for (int c = wave; c < nchunks; c += NW) {
             uint32_t key[16];
 #pragma unroll
@@ -339,7 +327,7 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
     const uint32_t b1 = s_res[0];
     const uint32_t need1 = (uint32_t)k - s_res[1];
 
-    const uint32_t cap = (uint32_t)a.cand_cap;
+    const uint32_t cap = (uint32_t)cand_cap;
     for (int c = wave; c < nchunks; c += NW) {
         uint32_t key[16];
         filter_load_1024(srow, c * 1024, n - 1, key);
@@ -347,7 +335,7 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
         const uint32_t cnt =
             filter_classify_1024(key, c * 1024, n, b1, sure + c * 32, tie + c * 32, cmask);
         uint32_t slot = 0;
-        if (lane == 0 && cnt) slot = atomicAdd(&s_cand_count, cnt);
+        if (lane == 0 && cnt) slot = atomicAdd(s_cand_count, cnt);
         filter_append_1024(key, c * 1024, cmask, __shfl(slot, 0),
                            [&](uint32_t at, uint32_t kv, uint32_t j) {
                                if (at < cap) {
@@ -357,7 +345,7 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
                            });
     }
     __syncthreads();
-    const uint32_t ncand = s_cand_count;
+    const uint32_t ncand = *s_cand_count;
     auto visit = [&](auto &&fn) {
         if (ncand <= cap) {
             for (uint32_t i = tid; i < ncand; i += kRowThreads) fn(ckey[i], cidx[i]);
@@ -372,6 +360,234 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
     refine_and_mark<kRowThreads>(visit, b1, need1, hist, low, s_res, sure, tie, r_ties);
     __syncthreads();
     compact_bitmaps<kRowThreads>(sure, tie, nchunks * 32, r_ties, k, out, s_wave);
+}
+
+template <bool HAVE_HIST>
+__global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
+    constexpr int NW = kRowThreads / 64;
+    extern __shared__ __align__(16) uint32_t lds[];
+    __shared__ uint32_t s_wave[2 * NW];
+    __shared__ uint32_t s_res[2];
+    __shared__ uint32_t s_cand_count;
+
+    const int row = blockIdx.x;
+    const int b = row / a.n_q;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+    const int k = a.top_k;
+    const int tid = threadIdx.x;
+    int32_t *out = a.idx + (size_t)row * k;
+    if (n <= k) {  // every valid key is selected
+        for (int i = tid; i < k; i += kRowThreads) out[i] = i < n ? i : -1;
+        if (tid == 0) a.n_sel[row] = n;
+        return;
+    }
+    row_topk(a.scores + (size_t)row * a.max_len,
+             HAVE_HIST ? a.hist + (size_t)row * kCoarseBins : nullptr, n, k, a.words_max,
+             a.cand_cap, out, lds, s_wave, s_res, &s_cand_count);
+    if (tid == 0) a.n_sel[row] = k;
+}
+
+// ------------------------------------------------------------------------------------
+// Chunked prefill without the score block (many causal rows, k <= 2048).
+//
+//   pass 1: the indexer scores every kTopkSampleStride-th key of every row;
+//           topk_sample_thresh_kernel takes, per row, the order-preserving key
+//           tau' of the R-th largest sampled score (topk_sample_rank);
+//   pass 2: the indexer recomputes every score with the same arithmetic and
+//           writes the keys at or above tau' (key, position) to the row's
+//           slots of each 256-key block (kTopkBlockSlots kept, all counted);
+//   finish: topk_cand_kernel selects exactly from the candidates.
+// If a row has at least k candidates, every key at or above its k-th largest
+// score is among them (that score is >= tau'), so the selection, ties
+// included, is the one the full row would give.  A row with fewer than k
+// candidates, or more than the list holds (very flat rows), is finished by its
+// workgroup the slow way: it recomputes the row's scores on the vector units
+// and runs the per-row selection on them.
+
+struct SampleArgs {
+    const float *samples;    // [rows, cols] sampled scores
+    const int32_t *seq_lens;
+    const int32_t *q_pos;
+    uint32_t *thresh;        // [rows]
+    int n_q, max_len, causal, top_k, cols, rank;
+};
+
+constexpr int kSampleThreads = 256;
+constexpr int kSamplePerThread = kMaxLen / kTopkSampleStride / kSampleThreads;  // 32
+
+// One workgroup per row: the rank-th largest of the row's valid sampled keys,
+// by three radix levels (11, 11 and 10 bits) over keys held in registers.
+// Rows with no more than k valid keys select them all and get the largest
+// threshold (no candidates); rows with no more than `rank` valid samples get 0
+// (every key a candidate).
+__global__ __launch_bounds__(kSampleThreads) void topk_sample_thresh_kernel(SampleArgs a) {
+    __shared__ __align__(16) uint32_t hist[kHistWords];
+    __shared__ uint32_t s_res[2];
+    const int row = blockIdx.x, b = row / a.n_q, tid = threadIdx.x;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+    const int m = div_up(n, kTopkSampleStride);  // valid samples
+    if (n <= a.top_k || m <= a.rank) {
+        if (tid == 0) a.thresh[row] = n <= a.top_k ? 0xffffffffu : 0u;
+        return;
+    }
+    const float *srow = a.samples + (size_t)row * a.cols;
+    uint32_t key[kSamplePerThread];
+#pragma unroll
+    for (int u = 0; u < kSamplePerThread; ++u) {
+        const int i = u * kSampleThreads + tid;
+        key[u] = i < m ? score_key(srow[i]) : 0u;
+    }
+    uint32_t need = (uint32_t)a.rank, prefix = 0u;
+    // level: bits [lo, hi) of keys whose bits above hi equal prefix
+    auto level = [&](int hi, int lo, int nbins) {
+        for (int x = tid; x < nbins; x += kSampleThreads) hist[x] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kSamplePerThread; ++u) {
+            const int i = u * kSampleThreads + tid;
+            if (i < m && (hi == 32 || (key[u] >> hi) == prefix))
+                atomicAdd(&hist[(key[u] >> lo) & (uint32_t)(nbins - 1)], 1u);
+        }
+        __syncthreads();
+    };
+    level(32, kCoarseShift, kCoarseBins);
+    find_threshold_bin<kCoarseBins>(hist, need, s_res);
+    prefix = s_res[0];
+    need -= s_res[1];
+    __syncthreads();
+    level(kCoarseShift, kMidShift, kMidBins);
+    find_threshold_bin<kMidBins>(hist, need, s_res);
+    prefix = (prefix << (kCoarseShift - kMidShift)) | s_res[0];
+    need -= s_res[1];
+    __syncthreads();
+    level(kMidShift, 0, kLowBins);
+    find_threshold_bin<kLowBins>(hist, need, s_res);
+    if (tid == 0) a.thresh[row] = (prefix << kMidShift) | s_res[0];
+}
+
+struct CandArgs {
+    const uint32_t *cand_count;  // [rows, kblocks]
+    const uint2 *cands;          // [rows, kblocks, kTopkBlockSlots]
+    const int32_t *seq_lens;
+    const int32_t *q_pos;
+    int32_t *idx;
+    int32_t *n_sel;
+    float *scores;               // [rows, max_len]: rows finished the slow way
+    const uint16_t *q_idx;
+    const uint16_t *k_idx;
+    const int32_t *page_table;
+    int n_q, max_len, causal, top_k, words_max, cand_cap, page_shift, max_pages, kblocks;
+};
+
+static_assert(kMaxLen / kTopkKeyBlock <= kRowThreads, "one key block per thread");
+
+__global__ __launch_bounds__(kRowThreads) void topk_cand_kernel(CandArgs a) {
+    constexpr int NW = kRowThreads / 64;
+    extern __shared__ __align__(16) uint32_t lds[];
+    __shared__ uint32_t s_wave[2 * NW];
+    __shared__ uint32_t s_res[2];
+    __shared__ uint32_t s_cand_count;
+    __shared__ __align__(16) uint32_t s_q[128];  // the row's index query (slow way)
+
+    const int row = blockIdx.x, b = row / a.n_q, tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+    const int k = a.top_k;
+    int32_t *out = a.idx + (size_t)row * k;
+    if (n <= k) {  // every valid key is selected
+        for (int i = tid; i < k; i += kRowThreads) out[i] = i < n ? i : -1;
+        if (tid == 0) a.n_sel[row] = n;
+        return;
+    }
+    uint32_t *hist = lds;                     // kHistWords
+    uint32_t *low = hist + kHistWords;        // kLowBins
+    uint32_t *sure = low + kLowBins;          // words_max
+    uint32_t *tie = sure + a.words_max;       // words_max
+    uint32_t *ckey = tie + a.words_max;       // cand_cap
+    uint32_t *cidx = ckey + a.cand_cap;       // cand_cap
+    // the row's candidates: block kb's count and its first slots; a block count
+    // past the slots means some candidates were not kept
+    const int nblk = div_up(n, kTopkKeyBlock);
+    const uint32_t cb = tid < nblk ? a.cand_count[(size_t)row * a.kblocks + tid] : 0u;
+    const uint32_t kept = min(cb, (uint32_t)kTopkBlockSlots);
+    uint32_t before, dummy0, cnt, lost;
+    block_excl_scan2<kRowThreads>(kept, cb - kept, s_wave, before, dummy0, cnt, lost);
+    if (lost == 0 && cnt >= (uint32_t)k && cnt <= (uint32_t)a.cand_cap) {
+        const int words = div_up(n, 1024) * 32;
+        if (tid < nblk) {  // blocks' first slots and counts, for the copy below
+            low[tid] = before;
+            hist[tid] = kept;
+        }
+        __syncthreads();
+        // slot s of the row's lists: block s / slots, entry s % slots; every
+        // thread loads all of its kept entries before storing any
+        const uint2 *src = a.cands + (size_t)row * a.kblocks * kTopkBlockSlots;
+        constexpr int kSlotsPerThread = kMaxLen / kTopkKeyBlock * kTopkBlockSlots / kRowThreads;
+        constexpr int kBatch = kSlotsPerThread / 2;  // loads in flight per thread
+        const int slots = nblk * kTopkBlockSlots;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint2 e[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int sl = (h * kBatch + u) * kRowThreads + tid;
+                const int kb = sl / kTopkBlockSlots, q = sl % kTopkBlockSlots;
+                if (sl < slots && (uint32_t)q < hist[kb]) e[u] = src[sl];
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int sl = (h * kBatch + u) * kRowThreads + tid;
+                const int kb = sl / kTopkBlockSlots, q = sl % kTopkBlockSlots;
+                if (sl < slots && (uint32_t)q < hist[kb]) {
+                    ckey[low[kb] + q] = e[u].x;
+                    cidx[low[kb] + q] = e[u].y;
+                }
+            }
+        }
+        __syncthreads();
+        for (int x = tid; x < kCoarseBins; x += kRowThreads) hist[x] = 0u;
+        for (int w = tid; w < words; w += kRowThreads) {
+            sure[w] = 0u;
+            tie[w] = 0u;
+        }
+        __syncthreads();
+        for (uint32_t i = tid; i < cnt; i += kRowThreads) atomicAdd(&hist[ckey[i] >> kCoarseShift], 1u);
+        __syncthreads();
+        find_threshold_bin<kCoarseBins>(hist, (uint32_t)k, s_res);
+        const uint32_t b1 = s_res[0];
+        const uint32_t need1 = (uint32_t)k - s_res[1];
+        for (uint32_t i = tid; i < cnt; i += kRowThreads)
+            if ((ckey[i] >> kCoarseShift) > b1) atomicOr(&sure[cidx[i] >> 5], 1u << (cidx[i] & 31));
+        auto visit = [&](auto &&fn) {
+            for (uint32_t i = tid; i < cnt; i += kRowThreads)
+                if ((ckey[i] >> kCoarseShift) == b1) fn(ckey[i], cidx[i]);
+        };
+        uint32_t r_ties;
+        refine_and_mark<kRowThreads>(visit, b1, need1, hist, low, s_res, sure, tie, r_ties);
+        __syncthreads();
+        compact_bitmaps<kRowThreads>(sure, tie, words, r_ties, k, out, s_wave);
+        if (tid == 0) a.n_sel[row] = k;
+        return;
+    }
+    // The slow way: the row's scores on the vector units, then the per-row path.
+    if (tid < 128) s_q[tid] = reinterpret_cast<const uint32_t *>(a.q_idx + (size_t)row * 256)[tid];
+    __syncthreads();
+    float *srow = a.scores + (size_t)row * a.max_len;
+    for (int j = tid; j < n; j += kRowThreads) {
+        const uint16_t *kr = a.k_idx + token_offset(a.page_table, a.page_shift, a.max_pages,
+                                                    a.max_len, b, j, 256);
+        float acc = 0.0f;
+#pragma unroll 8
+        for (int p = 0; p < 32; ++p) {
+            const uint4 kv = *reinterpret_cast<const uint4 *>(kr + 8 * p);
+            const uint4 qv = *reinterpret_cast<const uint4 *>(&s_q[4 * p]);
+            acc = dot8_bf16(kv, qv, acc);
+        }
+        srow[j] = acc;
+    }
+    __syncthreads();
+    row_topk(srow, nullptr, n, k, a.words_max, a.cand_cap, out, lds, s_wave, s_res,
+             &s_cand_count);
     if (tid == 0) a.n_sel[row] = k;
 }
 
@@ -603,6 +819,75 @@ TopkWideLayout topk_wide_layout(const Geometry &g) {
     L.cand_u32 = rows * L.regions * 1024;
     L.count_u32 = rows * L.regions;
     return L;
+}
+
+// R = c + max(c, 16), c = ceil(k / stride): a full row has about stride * R
+// keys at or above the R-th largest sample, against the k it needs; the
+// sampled keys among a row's top k number about c (at most about c + 4 sqrt(c)
+// in practice), so fewer than k candidates is a many-sigma event.
+int topk_sample_rank(const Geometry &g) {
+    const int c = div_up(g.top_k, kTopkSampleStride);
+    return c + (c > 16 ? c : 16);
+}
+
+// Many causal rows, k <= 2048, and rows long enough that the candidates
+// (about stride * R per row) leave at most kTopkBlockMean per key block.
+bool topk_uses_two_pass(const Geometry &g) {
+    return index_uses_mfma(g) && !topk_uses_wide(g) && g.top_k <= kTopkTwoPassMaxK &&
+           (int64_t)kTopkKeyBlock * kTopkSampleStride * topk_sample_rank(g) <=
+               (int64_t)kTopkBlockMean * g.max_len;
+}
+
+hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
+                                     const int32_t *seq_lens, const int32_t *q_pos,
+                                     uint32_t *thresh, hipStream_t stream) {
+    if (g.rows == 0) return hipSuccess;
+    SampleArgs a;
+    a.samples = samples;
+    a.seq_lens = seq_lens;
+    a.q_pos = q_pos;
+    a.thresh = thresh;
+    a.n_q = g.n_q;
+    a.max_len = g.max_len;
+    a.causal = g.causal;
+    a.top_k = g.top_k;
+    a.cols = topk_sample_cols(g);
+    a.rank = topk_sample_rank(g);
+    topk_sample_thresh_kernel<<<dim3(g.rows), dim3(kSampleThreads), 0, stream>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_cands(const Geometry &g, const uint32_t *cand_count, const uint32_t *cands,
+                             const int32_t *seq_lens, const int32_t *q_pos, const void *q_idx,
+                             const void *k_idx, const int32_t *page_table, float *scores,
+                             int32_t *idx, int32_t *n_sel, hipStream_t stream) {
+    if (g.rows == 0) return hipSuccess;
+    CandArgs a;
+    a.cand_count = cand_count;
+    a.cands = reinterpret_cast<const uint2 *>(cands);
+    a.seq_lens = seq_lens;
+    a.q_pos = q_pos;
+    a.idx = idx;
+    a.n_sel = n_sel;
+    a.scores = scores;
+    a.q_idx = static_cast<const uint16_t *>(q_idx);
+    a.k_idx = static_cast<const uint16_t *>(k_idx);
+    a.page_table = page_table;
+    a.n_q = g.n_q;
+    a.max_len = g.max_len;
+    a.causal = g.causal;
+    a.top_k = g.top_k;
+    a.words_max = row_words(g.max_len);
+    a.cand_cap = kTopkCandCap;
+    a.page_shift = g.page_shift;
+    a.max_pages = g.max_pages;
+    a.kblocks = topk_key_blocks(g);
+    const size_t lds = row_kernel_lds(g.max_len);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&topk_cand_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    topk_cand_kernel<<<dim3(g.rows), dim3(kRowThreads), lds, stream>>>(a);
+    return hipGetLastError();
 }
 
 hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *seq_lens,

@@ -167,6 +167,42 @@ def test_chunked_prefill_many_rows_chain():
     np.testing.assert_array_equal(gns[short], n[short])
 
 
+@pytest.mark.parametrize("page_size,top_k,length", [(64, 256, 20000), (0, 40, 20000),
+                                                    (0, 256, 20000), (0, 4096, 9000)])
+def test_chunked_prefill_many_rows_shapes(page_size, top_k, length):
+    """More than 128 causal rows: the two-pass top-k (long rows next to short
+    ones, whose dense candidates send them to the exact fallback) with paged
+    and contiguous caches and small k, and a k above 2048 (the top-k over full
+    score rows); every row and layer compared."""
+    w = inputs.small_workload(batch=2, lens=(length, length - 2000), n_q=96, causal=True,
+                              q_pos0=(length - 96, 1500), top_k=top_k, n_layers=1,
+                              page_size=page_size, wid=86)
+    x = inputs.make_inputs(w)
+    _check_step(w, x, range(1), f"prefill rows page {page_size} k {top_k}")
+
+
+def test_chunked_prefill_candidate_fallback_rows():
+    """The two-pass chunked-prefill top-k on rows whose candidates cannot decide
+    the set, which their workgroups finish from recomputed scores: rows with a
+    zero index query (every score 0: more candidates than the list holds; ties
+    go to the lowest positions) and rows whose index keys at every 32nd
+    position are aligned with their query (the sampled threshold is high, so
+    fewer than k keys reach it), next to ordinary rows."""
+    w = inputs.small_workload(batch=2, lens=(20000, 20000), n_q=160, causal=True,
+                              q_pos0=(19840, 19840), top_k=256, n_layers=1, wid=85)
+    x = inputs.make_inputs(w)
+    q = x["q_idx"]
+    q[0, :40] = 0                               # all-equal rows
+    shared = q[1, 0].copy()                     # rows 40..79 of sequence 1 share one query
+    q[1, 40:80] = shared
+    qf = inputs.f32_from_bf16_bits(shared).astype(np.float64).reshape(-1)
+    qhat = (qf / np.sqrt((qf * qf).sum())).reshape(4, 64)
+    k1 = inputs.f32_from_bf16_bits(x["k_idx"][1, 0:20000:32]).astype(np.float64)
+    x["k_idx"][1, 0:20000:32] = inputs.bf16_bits_from_f32((k1 + 4.0 * qhat / 8.0).astype(np.float32))
+    gidx, gns, _ = _check_step(w, x, range(1), "prefill fallback rows")
+    np.testing.assert_array_equal(gidx[0, :40], np.broadcast_to(np.arange(256), (40, 256)))
+
+
 def test_many_single_query_rows():
     """160 decode rows (more than 128): the per-row top-k fed by the decode
     indexer's coarse histograms, with empty rows, rows with fewer keys than k,
