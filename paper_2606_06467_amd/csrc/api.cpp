@@ -388,7 +388,10 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
             CLSA_TRY(from_hip(clsa::launch_topk_cands(g, w.cand_count, w.cands, seq_lens, q_pos,
                                                       qi, ki, page_table, w.scores, is, ns, st)));
         } else {
-            if (!mfma || clsa::topk_uses_wide(g))
+            // the decode indexer makes the coarse histogram except for short rows,
+            // whose per-row top-k makes its own in LDS
+            const bool idx_hist = !mfma && !clsa::topk_small_rows(g);
+            if (idx_hist || clsa::topk_uses_wide(g))
                 CLSA_TRY(from_hip(clsa::launch_zero_u32(w.zero, w.zero_count, st)));
             if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
             if (mfma)
@@ -396,9 +399,10 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
                                                              q_pos, w.scores, st)));
             else
                 CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
-                                                            w.scores, w.topk.hist, st)));
+                                                            w.scores, idx_hist ? w.topk.hist : nullptr,
+                                                            st)));
             if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
-            CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, !mfma, is,
+            CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, idx_hist, is,
                                                 ns, st)));
         }
         if (first && hook && hipEventRecord(t_hook.ev[2], st) != hipSuccess) return CLSA_ERR_HIP;

@@ -31,8 +31,10 @@ constexpr int kCoarseShift = 21;  // top 11 key bits: sign, exponent, 2 mantissa
 constexpr int kCoarseBins = 1 << (32 - kCoarseShift);
 // Candidate list capacity of the per-row top-k kernel (LDS entries of 8 bytes).
 constexpr int kTopkCandCap = 8192;
-// Rows up to which the top-k splits each row over many workgroups.
+// Rows up to which the top-k splits each row over many workgroups, when the
+// rows are longer than kTopkRowMaxLen keys.
 constexpr int kTopkWideMaxRows = 128;
+constexpr int kTopkRowMaxLen = 16384;
 
 __host__ __device__ inline int div_up(int a, int b) { return (a + b - 1) / b; }
 
@@ -122,6 +124,7 @@ struct TopkBuffers {
     uint32_t *counts;    // count_u32: candidates per region (wide path)
 };
 bool topk_uses_wide(const Geometry &g);
+bool topk_small_rows(const Geometry &g);
 TopkWideLayout topk_wide_layout(const Geometry &g);
 size_t topk_lds_bytes(const Geometry &g);  // LDS per workgroup of the largest top-k kernel
 // hist_ready: buf.hist already holds the coarse histogram of these scores.

@@ -796,7 +796,11 @@ hipError_t launch_zero_u32(uint32_t *p, size_t n, hipStream_t stream) {
 static int row_words(int max_len) { return div_up(max_len, 1024) * 32; }
 static int wide_words(int max_len) { return div_up(max_len, kWideChunk) * (kWideChunk / 32); }
 
-bool topk_uses_wide(const Geometry &g) { return g.rows <= kTopkWideMaxRows; }
+// Rows of up to kTopkRowMaxLen keys are short enough for one workgroup each
+// (one launch, the histogram made in LDS); the few long rows of decode are
+// spread over many workgroups.
+bool topk_small_rows(const Geometry &g) { return g.max_len <= kTopkRowMaxLen; }
+bool topk_uses_wide(const Geometry &g) { return g.rows <= kTopkWideMaxRows && !topk_small_rows(g); }
 
 static size_t row_kernel_lds(int max_len) {
     return sizeof(uint32_t) * ((size_t)kHistWords + kLowBins + 2 * (size_t)row_words(max_len) +
@@ -833,7 +837,7 @@ int topk_sample_rank(const Geometry &g) {
 // Many causal rows, k <= 2048, and rows long enough that the candidates
 // (about stride * R per row) leave at most kTopkBlockMean per key block.
 bool topk_uses_two_pass(const Geometry &g) {
-    return index_uses_mfma(g) && !topk_uses_wide(g) && g.top_k <= kTopkTwoPassMaxK &&
+    return index_uses_mfma(g) && g.rows > kTopkWideMaxRows && g.top_k <= kTopkTwoPassMaxK &&
            (int64_t)kTopkKeyBlock * kTopkSampleStride * topk_sample_rank(g) <=
                (int64_t)kTopkBlockMean * g.max_len;
 }

@@ -204,11 +204,11 @@ def test_chunked_prefill_candidate_fallback_rows():
 
 
 def test_many_single_query_rows():
-    """160 decode rows (more than 128): the per-row top-k fed by the decode
-    indexer's coarse histograms, with empty rows, rows with fewer keys than k,
-    exactly k and k + 1 keys."""
+    """160 decode rows (more than 128, some longer than 16384 keys): the
+    per-row top-k fed by the decode indexer's coarse histograms, with empty
+    rows, rows with fewer keys than k, exactly k and k + 1 keys."""
     g = np.random.default_rng(82)
-    lens = [int(v) for v in g.integers(500, 6000, size=160)]
+    lens = [int(v) for v in g.integers(500, 20000, size=160)]
     lens[:4] = [0, 1024, 1025, 700]
     w = inputs.small_workload(batch=160, lens=lens, top_k=1024, n_layers=2, wid=82)
     x = inputs.make_inputs(w)
