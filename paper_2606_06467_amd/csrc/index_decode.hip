@@ -3,8 +3,8 @@
 //
 // The pass is bound by HBM: every token contributes one 512-byte index key and
 // 256 multiply-adds.  Layout of the work:
-//   * one workgroup = 4 waves = kIndexTilesPerGroup consecutive 128-token tiles
-//     of one query row (each wave takes 32 tokens of a tile);
+//   * one workgroup = 4 waves = up to kIndexTilesPerGroup consecutive 128-token
+//     tiles of one query row (each wave takes 32 tokens of a tile);
 //   * a half-wave (32 lanes x 16 bytes) reads one token's 512-byte key, so each
 //     load instruction of a wave moves 1 KiB of contiguous HBM; a wave issues
 //     all 16 loads of its 32 tokens (16 KiB) before it waits;
@@ -30,11 +30,14 @@ struct IndexArgs {
     const int32_t *q_pos;
     float *scores;
     uint32_t *hist;
-    int n_q, max_len, page_shift, max_pages, causal, groups_per_row;
+    int n_q, max_len, page_shift, max_pages, causal, groups_per_row, tiles_per_group;
 };
 
 constexpr int kIdxWidth = 256;  // d_idx in bf16 elements (512 bytes per token)
+// Tiles per workgroup, fewer when the grid would otherwise leave CUs idle
+// (one short sequence): each tile is one dependent memory round trip.
 constexpr int kIndexTilesPerGroup = 4;
+constexpr int kIndexMinGroups = 256;
 
 // Scores of the 32 tokens tok0 .. tok0+31 of one wave.
 template <bool HIST, bool PAGED>
@@ -83,7 +86,7 @@ __global__ __launch_bounds__(256) void index_decode_kernel(IndexArgs a) {
     const int grp = blockIdx.x - row * a.groups_per_row;
     const int b = row / a.n_q;
     const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
-    const int tile_first = grp * kIndexTilesPerGroup;
+    const int tile_first = grp * a.tiles_per_group;
     if (tile_first * kIndexTile >= n) return;  // uniform over the workgroup
 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -93,7 +96,7 @@ __global__ __launch_bounds__(256) void index_decode_kernel(IndexArgs a) {
         __syncthreads();
     }
     const uint4 qv = *reinterpret_cast<const uint4 *>(a.q_idx + (size_t)row * kIdxWidth + sub * 8);
-    const int tile_end = min(tile_first + kIndexTilesPerGroup, div_up(n, kIndexTile));
+    const int tile_end = min(tile_first + a.tiles_per_group, div_up(n, kIndexTile));
     for (int tile = tile_first; tile < tile_end; ++tile)
         index_tile<HIST, PAGED>(a, row, b, n, tile * kIndexTile + wave * 32, half, sub, qv, hist_s);
     if (HIST) {
@@ -122,7 +125,11 @@ hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void 
     a.page_shift = g.page_shift;
     a.max_pages = g.max_pages;
     a.causal = g.causal;
-    a.groups_per_row = div_up(div_up(g.max_len, kIndexTile), kIndexTilesPerGroup);
+    const int tiles = div_up(g.max_len, kIndexTile);
+    a.tiles_per_group = kIndexTilesPerGroup;
+    while (a.tiles_per_group > 1 && (size_t)g.rows * div_up(tiles, a.tiles_per_group) < kIndexMinGroups)
+        a.tiles_per_group /= 2;
+    a.groups_per_row = div_up(tiles, a.tiles_per_group);
     const size_t blocks = (size_t)g.rows * a.groups_per_row;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;

@@ -18,7 +18,7 @@
 //
 // Two shapes of the same algorithm:
 //   * topk_row_kernel: one 1024-thread workgroup per row, bitmaps and the
-//     candidate list in LDS -- for many rows (chunked prefill);
+//     candidate list in LDS -- for many long rows (chunked prefill);
 //   * for the few, long rows of decode, step 2 is spread over many 256-thread
 //     workgroups (topk_filter_kernel, 4096 keys each, writing a global bitmap
 //     and, per wave, its candidates into a region of its own) and a second
@@ -30,6 +30,8 @@
 // If the per-row kernel's candidate list overflows (very flat score rows),
 // steps 3-4 re-read the row instead: slower, same result.  The regions of the
 // wide path hold every key of their wave, so they never overflow.
+// Rows of at most kTopkRowMaxLen keys take a third form (topk_short_kernel):
+// the row in registers, tau fixed 4 bits at a time by counting, no bitmaps.
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -384,6 +386,213 @@ __global__ __launch_bounds__(kRowThreads) void topk_row_kernel(TopkRowArgs a) {
     row_topk(a.scores + (size_t)row * a.max_len,
              HAVE_HIST ? a.hist + (size_t)row * kCoarseBins : nullptr, n, k, a.words_max,
              a.cand_cap, out, lds, s_wave, s_res, &s_cand_count);
+    if (tid == 0) a.n_sel[row] = k;
+}
+
+// ------------------------------------------------------------------------------------
+// Short rows (up to kTopkRowMaxLen keys): one workgroup per row holds the whole
+// row in registers, kShortKeys consecutive positions per thread, read once.
+// tau is fixed four bits at a time from the top (up to 8 rounds): every thread
+// counts the digits of its keys that still match the digits fixed so far in 16
+// nibble counters (a 64-bit word per 8 keys); the counters are widened to 16
+// bits, summed over the wave by a transpose-reduction and over the waves
+// through LDS (one barrier per round, the buffer alternating between rounds),
+// and every wave takes the same digit from the totals.  Each round is a chain
+// of dependent latencies (about half a microsecond), so once at most
+// kShortFinish keys still match, they are packed into one wave, which ranks
+// them against each other directly and so fixes tau in one step.  There are no
+// LDS atomics (the scores crowd into a few bins of the leading digits, where
+// same-address atomics serialise) and no second pass over memory.  The
+// ordered output is one workgroup prefix of each thread's counts of keys above
+// tau and equal to tau; of the latter the first r in position order are kept.
+constexpr int kShortKeys = 16;
+static_assert(1024 * kShortKeys >= kTopkRowMaxLen, "one 1024-thread workgroup holds a short row");
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xf, 0xf, false);
+}
+
+// Each of 8 values summed over the 64 lanes; lane L ends with the total of
+// value L >> 3.  Halving exchanges across the row pairs (permlane32 / 16
+// swaps) and inside rows (row mirror), then plain sums with the half mirror
+// and the quad permutes (lanes reached: every lane of the wave exactly once).
+__device__ __forceinline__ uint32_t wave_reduce8(const uint32_t (&w)[8], int lane) {
+    uint32_t p[4], q[2];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {  // lanes 0-31 keep values 0-3, lanes 32-63 values 4-7
+        const auto r = __builtin_amdgcn_permlane32_swap(w[v], w[v + 4], false, false);
+        p[v] = r[0] + r[1];
+    }
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {  // then by lane bit 4
+        const auto r = __builtin_amdgcn_permlane16_swap(p[v], p[v + 2], false, false);
+        q[v] = r[0] + r[1];
+    }
+    const bool up = (lane & 8) != 0;  // then by lane bit 3, with the row-mirror partner
+    uint32_t x = (up ? q[1] : q[0]) + dpp_u32<0x140>(up ? q[0] : q[1]);
+    x += dpp_u32<0x141>(x);
+    x += dpp_u32<0x4E>(x);
+    return x + dpp_u32<0xB1>(x);
+}
+
+// The 16 digit counts of the keys of this wave selected by `sel` (keys past
+// `cnt` are not counted), 16-bit halves two to a word, summed over the wave;
+// lanes with (lane & 7) == 0 write word lane >> 3 to out.
+template <int CNT>
+__device__ __forceinline__ void wave_digit_counts(const uint32_t (&key)[CNT], uint32_t sel,
+                                                  int shift, uint32_t prefix, uint32_t pmask,
+                                                  int lane, uint32_t *out) {
+    uint64_t acc[2] = {0ull, 0ull};  // nibble d of acc[h]: keys 8h .. 8h+7 with digit d
+#pragma unroll
+    for (int j = 0; j < CNT; ++j) {
+        const uint32_t d = (key[j] >> shift) & 15u;
+        const uint32_t m = ((key[j] ^ prefix) & pmask) == 0u ? (sel >> j) & 1u : 0u;
+        acc[j >> 3] += (uint64_t)m << (4 * d);
+    }
+    // bytes of ev: digits 0, 2, .., 14; of od: 1, 3, .., 15 (each at most 16)
+    constexpr uint64_t kLowNibbles = 0x0F0F0F0F0F0F0F0Full;
+    const uint64_t ev = (acc[0] & kLowNibbles) + (acc[1] & kLowNibbles);
+    const uint64_t od = ((acc[0] >> 4) & kLowNibbles) + ((acc[1] >> 4) & kLowNibbles);
+    // 16-bit halves, two digits per word (the lookup is in topk_short_kernel)
+    const uint32_t w[8] = {(uint32_t)ev & 0x00FF00FFu,          (uint32_t)(ev >> 8) & 0x00FF00FFu,
+                           (uint32_t)(ev >> 32) & 0x00FF00FFu,  (uint32_t)(ev >> 40) & 0x00FF00FFu,
+                           (uint32_t)od & 0x00FF00FFu,          (uint32_t)(od >> 8) & 0x00FF00FFu,
+                           (uint32_t)(od >> 32) & 0x00FF00FFu,  (uint32_t)(od >> 40) & 0x00FF00FFu};
+    const uint32_t t = wave_reduce8(w, lane);  // at most 64 * 16 per half
+    if ((lane & 7) == 0) out[lane >> 3] = t;
+}
+
+// Inclusive prefix sum over the 16 lanes of each row (DPP row shifts).
+__device__ __forceinline__ uint32_t row16_incl_scan(uint32_t v) {
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    return v + (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);
+}
+
+constexpr int kShortFinish = 64;  // candidates left when one wave ranks them directly
+
+template <int NT>  // NT * kShortKeys >= max_len
+__global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
+    constexpr int NW = NT / 64;
+    __shared__ uint32_t s_cnt[2][NW][8];  // per round: each wave's 16 digit counts, two per word
+    __shared__ uint32_t s_wave[2 * NW];
+    __shared__ uint32_t s_pack[kShortFinish];
+    __shared__ uint32_t s_tau[2];
+
+    const int row = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float *srow = a.scores + (size_t)row * a.max_len;
+    const int p0 = tid * kShortKeys;
+    // loads issued before the row's length is known (clamped to its capacity)
+    uint32_t key[kShortKeys];
+#pragma unroll
+    for (int j = 0; j < kShortKeys; ++j) key[j] = score_key(srow[min(p0 + j, a.max_len - 1)]);
+    const int b = row / a.n_q;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+    const int k = a.top_k;
+    int32_t *out = a.idx + (size_t)row * k;
+    if (n <= k) {  // every valid key is selected
+        for (int i = tid; i < k; i += NT) out[i] = i < n ? i : -1;
+        if (tid == 0) a.n_sel[row] = n;
+        return;
+    }
+    const int nv = min(max(n - p0, 0), kShortKeys);  // this thread's valid keys: key[0 .. nv)
+    const uint32_t vmask = (1u << nv) - 1u;              // as a bit mask (nv <= 16)
+
+    // Lane l < 16 follows digit d = 15 - l (an inclusive prefix over lanes is
+    // then a suffix over digits); digit d is half (d >> 2) & 1 of word
+    // 4 (d & 1) + 2 (d >> 3) + ((d >> 1) & 1) of the counts.
+    const int dg = 15 - (lane & 15);
+    const int dword = 4 * (dg & 1) + 2 * (dg >> 3) + ((dg >> 1) & 1);
+    const int dhalf = 16 * ((dg >> 2) & 1);
+
+    // prefix: the digits of tau fixed so far; need: keys matching it still to be taken
+    uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)k;
+    uint32_t tau = 0u, r = 0u;
+#pragma unroll 1
+    for (int round = 0; round < 8; ++round) {
+        const int shift = 28 - 4 * round;
+        uint32_t(*buf)[8] = s_cnt[round & 1];
+        wave_digit_counts<kShortKeys>(key, vmask, shift, prefix, pmask, lane, buf[wave]);
+        __syncthreads();
+        uint32_t c = 0u;  // lanes 0..15: keys of digit dg summed over the waves
+        if (lane < 16) {
+#pragma unroll
+            for (int x = 0; x < NW; ++x) c += (buf[x][dword] >> dhalf) & 0xFFFFu;
+        }
+        const uint32_t incl = row16_incl_scan(c);  // lanes 0..15: keys with digit >= dg
+        const uint64_t reach = __ballot(lane < 16 && incl >= need);
+        const int ls = reach ? __builtin_ctzll(reach) : 15;  // consistent counts always reach
+        const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)(incl - c), ls);
+        const uint32_t left = (uint32_t)__builtin_amdgcn_readlane((int)c, ls);  // keys still matching
+        need -= above;
+        prefix |= (15u - (uint32_t)ls) << shift;
+        pmask |= 15u << shift;
+        if (round == 7) {
+            tau = prefix;
+            r = need;
+        } else if (left <= (uint32_t)kShortFinish) {
+            // Few keys still match: pack them (in position order) into one wave,
+            // which ranks them directly.  tau is the need-th largest of them.
+            uint32_t mb = 0u;
+#pragma unroll
+            for (int j = 0; j < kShortKeys; ++j)
+                mb |= (((key[j] ^ prefix) & pmask) == 0u ? 1u : 0u) << j;
+            mb &= vmask;
+            uint32_t before, unused0, total, unused1;
+            block_excl_scan2<NT>((uint32_t)__popc(mb), 0u, s_wave, before, unused0, total, unused1);
+#pragma unroll
+            for (int j = 0; j < kShortKeys; ++j)
+                if ((mb >> j) & 1u) s_pack[before++] = key[j];
+            __syncthreads();
+            if (wave == 0) {
+                const uint32_t cv = lane < (int)left ? s_pack[lane] : 0u;
+                uint32_t gt = 0u, eq = 0u;
+                for (uint32_t i = 0; i < left; ++i) {
+                    const uint32_t ci = (uint32_t)__builtin_amdgcn_readlane((int)cv, (int)i);
+                    gt += ci > cv ? 1u : 0u;
+                    eq += ci == cv ? 1u : 0u;
+                }
+                const uint64_t hit = __ballot(lane < (int)left && gt < need && need <= gt + eq);
+                if (lane == (hit ? __builtin_ctzll(hit) : 0)) {
+                    s_tau[0] = cv;
+                    s_tau[1] = need - gt;
+                }
+            }
+            __syncthreads();
+            tau = s_tau[0];
+            r = s_tau[1];
+            break;
+        }
+    }
+
+    // this thread's keys above tau and equal to tau, as bit masks over j
+    uint32_t sbits = 0u, tbits = 0u;
+#pragma unroll
+    for (int j = 0; j < kShortKeys; ++j) {
+        sbits |= (key[j] > tau ? 1u : 0u) << j;
+        tbits |= (key[j] == tau ? 1u : 0u) << j;
+    }
+    sbits &= vmask;
+    tbits &= vmask;
+    uint32_t sure_before, tie_before, sure_total, tie_total;
+    block_excl_scan2<NT>((uint32_t)__popc(sbits), (uint32_t)__popc(tbits), s_wave, sure_before,
+                         tie_before, sure_total, tie_total);
+    uint32_t take = tie_before < r ? r - tie_before : 0u;  // ties this thread may still keep
+    uint32_t keep = sbits;
+    for (; take && tbits; --take) {  // the first `take` ties in position order
+        keep |= tbits & (0u - tbits);
+        tbits &= tbits - 1u;
+    }
+    uint32_t pos = sure_before + min(tie_before, r);
+    while (keep) {
+        const int j = __builtin_ctz(keep);
+        keep &= keep - 1u;
+        if (pos < (uint32_t)k) out[pos] = p0 + j;
+        ++pos;
+    }
     if (tid == 0) a.n_sel[row] = k;
 }
 
@@ -796,9 +1005,9 @@ hipError_t launch_zero_u32(uint32_t *p, size_t n, hipStream_t stream) {
 static int row_words(int max_len) { return div_up(max_len, 1024) * 32; }
 static int wide_words(int max_len) { return div_up(max_len, kWideChunk) * (kWideChunk / 32); }
 
-// Rows of up to kTopkRowMaxLen keys are short enough for one workgroup each
-// (one launch, the histogram made in LDS); the few long rows of decode are
-// spread over many workgroups.
+// Rows of up to kTopkRowMaxLen keys are short enough for one workgroup each,
+// which holds the row in registers (one launch, no histogram); the few long
+// rows of decode are spread over many workgroups.
 bool topk_small_rows(const Geometry &g) { return g.max_len <= kTopkRowMaxLen; }
 bool topk_uses_wide(const Geometry &g) { return g.rows <= kTopkWideMaxRows && !topk_small_rows(g); }
 
@@ -808,6 +1017,8 @@ static size_t row_kernel_lds(int max_len) {
 }
 
 size_t topk_lds_bytes(const Geometry &g) {
+    if (topk_small_rows(g))  // short-row kernel: static LDS only
+        return sizeof(uint32_t) * (2 * 16 * 8 + 2 * 16);
     if (topk_uses_wide(g))  // finish kernel: static histograms + two bitmaps
         return sizeof(uint32_t) * ((size_t)kHistWords + kLowBins + 2 * (size_t)wide_words(g.max_len));
     return row_kernel_lds(g.max_len);
@@ -949,6 +1160,15 @@ hipError_t launch_topk(const Geometry &g, const float *scores, const int32_t *se
     a.top_k = g.top_k;
     a.words_max = row_words(g.max_len);
     a.cand_cap = kTopkCandCap;
+    if (topk_small_rows(g)) {  // the whole row in registers (a histogram is not needed)
+        if (g.max_len <= 256 * kShortKeys)
+            topk_short_kernel<256><<<dim3(g.rows), dim3(256), 0, stream>>>(a);
+        else if (g.max_len <= 512 * kShortKeys)
+            topk_short_kernel<512><<<dim3(g.rows), dim3(512), 0, stream>>>(a);
+        else
+            topk_short_kernel<1024><<<dim3(g.rows), dim3(1024), 0, stream>>>(a);
+        return hipGetLastError();
+    }
     const size_t lds = row_kernel_lds(g.max_len);
     hipError_t e;
     if (hist_ready) {

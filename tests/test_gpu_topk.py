@@ -110,13 +110,55 @@ def test_many_rows_prefill_like():
 
 
 def test_all_equal_many_rows_per_row_kernel():
-    """Many rows (the one-workgroup-per-row kernel): all-equal rows overflow its
-    LDS candidate list, so it re-reads the row; ordinary rows in the same launch."""
-    s = inputs.random_scores(81, 160, 12000)[None]
+    """Many rows longer than 16384 keys (the one-workgroup-per-row kernel with
+    bitmaps): all-equal rows overflow its LDS candidate list, so it re-reads the
+    row; ordinary rows in the same launch."""
+    n = 20000
+    s = inputs.random_scores(81, 160, n)[None]
     s[0, ::3] = 0.75
     s[0, 1::7] = -0.0
-    q_pos = (12000 - 160 + np.arange(160, dtype=np.int32))[None]
-    _check(s, 2048, [12000], q_pos=q_pos, what="160 rows, every third all-equal")
+    q_pos = (n - 160 + np.arange(160, dtype=np.int32))[None]
+    _check(s, 2048, [n], q_pos=q_pos, what="160 rows, every third all-equal")
+
+
+# Short rows (at most 16384 keys): one workgroup per row with the row in
+# registers, 256 / 512 / 1024 threads for up to 4096 / 8192 / 16384 keys.
+@pytest.mark.parametrize("n", [100, 1023, 1024, 4095, 4096, 4097, 8192, 8193, 16383, 16384])
+def test_short_rows_each_width(n):
+    s = inputs.random_scores(90 + n % 97, 4, n)[:, None, :]
+    ks = sorted({1, max(1, n // 8), min(n - 1, 8192)})
+    for k in ks:
+        lens = [n, n - 1, max(k + 1, n // 3), min(k, n)]
+        _check(s, k, lens, what=f"short n={n} k={k}")
+
+
+def test_short_rows_ties_and_specials():
+    """Short rows where every key of a thread shares each digit (all equal,
+    signed zeros), a few distinct levels, and the extremes of the key order."""
+    n = 4096
+    s = np.empty((5, 1, n), np.float32)
+    s[0, 0] = 0.375
+    s[1, 0] = 0.0
+    s[1, 0, 1::2] = -0.0
+    s[2, 0] = inputs.random_scores(91, 1, n, levels=5)[0]
+    s[3, 0] = inputs.random_scores(92, 1, n)[0]
+    s[3, 0, :64] = np.inf
+    s[3, 0, 64:128] = -np.inf
+    s[3, 0, 128:192] = 3.4e38
+    s[3, 0, 192:256] = 1e-45
+    s[4, 0] = inputs.random_scores(93, 1, n)[0]
+    s[4, 0, 4000:] = s[4, 0, 3999]          # a tied run at the end of the row
+    for k in (1, 64, 512, 4095):
+        _check(s, k, [n] * 5, what=f"short ties/specials k={k}")
+
+
+def test_short_rows_many_causal():
+    """Many causal rows of one short sequence: rows that see fewer keys than k
+    select all of theirs; the rest select through the short-row kernel."""
+    T, n = 300, 6000
+    s = inputs.random_scores(94, T, n)[None]
+    q_pos = (np.linspace(0, n - 1, T).astype(np.int32))[None]
+    _check(s, 512, [n], q_pos=q_pos, what="300 causal short rows")
 
 
 def test_candidate_regions_at_register_boundary():
