@@ -16,6 +16,7 @@ the same workload.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -513,6 +514,9 @@ def main() -> int:
                     help="instead of the decode step, time the training-side distillation step "
                          "(Eq. 5 target, Eq. 6 loss and indexer gradient) on the 32K-token "
                          "sequence workload (one JSON line)")
+    ap.add_argument("--top-k", type=int, default=0,
+                    help="run the workload with this top_k instead of its own (the workload "
+                         "name gets a _k<K> suffix); e.g. index sets whose rows fit the L2")
     ap.add_argument("--schedules", action="store_true",
                     help="instead of the step benchmark, compare routing schedules on the "
                          "workload: one shared index set, a fresh set every 4 layers, a fresh "
@@ -532,6 +536,8 @@ def main() -> int:
         wl = args.workload if args.workload in inputs.KD_WORKLOADS else inputs.KD_WORKLOADS[0]
         return run_kd(args, inputs.workload(wl))
     w = inputs.workload(args.workload)
+    if args.top_k > 0:
+        w = dataclasses.replace(w, name=f"{w.name}_k{args.top_k}", top_k=args.top_k)
     if args.schedules:
         return run_schedules(args, w)
     if w.n_q != 1:
