@@ -172,6 +172,7 @@ struct DecodeWs {
     uint32_t *thresh = nullptr;    // [rows]
     uint32_t *cand_count = nullptr;  // [rows, key blocks]
     uint32_t *cands = nullptr;     // [rows, key blocks, kTopkBlockSlots, 2]
+    uint32_t *slow = nullptr;      // [1 + rows]: rows selected the slow way
 };
 
 // Every layer gathers its K/V rows from the cache through the shared index set.
@@ -197,6 +198,7 @@ size_t carve_decode(const Geometry &g, void *base, DecodeWs &w) {
         const size_t blocks = (size_t)g.rows * clsa::topk_key_blocks(g);
         w.cand_count = c.take<uint32_t>(blocks);
         w.cands = c.take<uint32_t>(blocks * clsa::kTopkBlockSlots * 2);
+        w.slow = c.take<uint32_t>((size_t)g.rows + 1);
     }
     return c.off;
 }
@@ -380,13 +382,14 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
             CLSA_TRY(from_hip(clsa::launch_index_prefill_sample(g, qi, ki, page_table, seq_lens,
                                                                 q_pos, w.samples, st)));
             CLSA_TRY(from_hip(clsa::launch_topk_sample_thresh(g, w.samples, seq_lens, q_pos,
-                                                              w.thresh, st)));
+                                                              w.thresh, w.slow, st)));
             CLSA_TRY(from_hip(clsa::launch_index_prefill_emit(g, qi, ki, page_table, seq_lens,
                                                               q_pos, w.thresh, w.cand_count,
                                                               w.cands, st)));
             if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
             CLSA_TRY(from_hip(clsa::launch_topk_cands(g, w.cand_count, w.cands, seq_lens, q_pos,
-                                                      qi, ki, page_table, w.scores, is, ns, st)));
+                                                      qi, ki, page_table, w.scores, w.slow, is, ns,
+                                                      st)));
         } else {
             // the decode indexer makes the coarse histogram except for short rows,
             // whose per-row top-k makes its own in LDS

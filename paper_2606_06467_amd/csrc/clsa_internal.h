@@ -94,10 +94,11 @@ int topk_sample_rank(const Geometry &g);
 hipError_t launch_index_prefill_sample(const Geometry &g, const void *q_idx, const void *k_idx,
                                        const int32_t *page_table, const int32_t *seq_lens,
                                        const int32_t *q_pos, float *samples, hipStream_t stream);
-// Per-row thresholds (order-preserving keys) from the samples.
+// Per-row thresholds (order-preserving keys) from the samples; also clears the
+// count of the slow list (slow: [1 + rows]) that the selection fills.
 hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
                                      const int32_t *seq_lens, const int32_t *q_pos,
-                                     uint32_t *thresh, hipStream_t stream);
+                                     uint32_t *thresh, uint32_t *slow, hipStream_t stream);
 // Pass 2: cand_count [rows, topk_key_blocks(g)] and cands [rows,
 // topk_key_blocks(g), kTopkBlockSlots] of (key, position) pairs (every block a
 // row sees gets its count written; no clearing needed).
@@ -106,11 +107,12 @@ hipError_t launch_index_prefill_emit(const Geometry &g, const void *q_idx, const
                                      const int32_t *q_pos, const uint32_t *thresh,
                                      uint32_t *cand_count, uint32_t *cands, hipStream_t stream);
 // Exact selection from the candidates; rows whose candidates do not decide
-// the set recompute their scores into scores [rows, max_len].
+// the set go to the slow list and recompute their scores into scores
+// [rows, max_len].
 hipError_t launch_topk_cands(const Geometry &g, const uint32_t *cand_count, const uint32_t *cands,
                              const int32_t *seq_lens, const int32_t *q_pos, const void *q_idx,
                              const void *k_idx, const int32_t *page_table, float *scores,
-                             int32_t *idx, int32_t *n_sel, hipStream_t stream);
+                             uint32_t *slow, int32_t *idx, int32_t *n_sel, hipStream_t stream);
 
 // ---- topk.hip ----
 struct TopkWideLayout {

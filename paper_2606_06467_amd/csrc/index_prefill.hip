@@ -97,12 +97,27 @@ __device__ __forceinline__ void pf_lds_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// Largest key limit over the 16 queries of a tile (every lane gets it; the same
-// in every wave of the workgroup, which holds the same queries).
+// Largest / smallest key limit over the 16 queries of a tile (every lane gets
+// it; the same in every wave of the workgroup, which holds the same queries).
 __device__ __forceinline__ int tile_limit(int n) {
 #pragma unroll
     for (int m = 8; m >= 1; m >>= 1) n = max(n, __shfl_xor(n, m));
     return n;
+}
+__device__ __forceinline__ int tile_limit_min(int n) {
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) n = min(n, __shfl_xor(n, m));
+    return n;
+}
+
+// The fp32 threshold equivalent to an order-preserving key threshold th:
+// score_key(s) >= th exactly when s >= thresh_float(th), for every non-NaN s
+// (the inverse of score_key; keys below that of -inf give -inf, keys above
+// that of +inf give NaN, which no score reaches).  Denormal flushing can only
+// turn a strict comparison into an equality, i.e. admit more candidates.
+__device__ __forceinline__ float thresh_float(uint32_t th) {
+    if (th < 0x007FFFFFu) return -INFINITY;
+    return __uint_as_float((th & 0x80000000u) ? (th & 0x7FFFFFFFu) : ~th);
 }
 
 // Scores of one query tile against the workgroup's 256 keys into the LDS tile:
@@ -189,10 +204,13 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int jg = kblk * kPfKeys;                       // first key of this workgroup
     const int jw = jg + wave * kPfWaveKeys;              // first key of this wave
     if (jg >= len) return;                               // uniform over the workgroup
-    __shared__ float tile[EMIT ? 1 : 2][16][kTileStride];
+    __shared__ float tile[EMIT ? 1 : 2][EMIT ? 1 : 16][kTileStride];
     __shared__ __align__(16) uint16_t s_q[2][16][kQStride];  // query tiles (bf16)
     // EMIT: candidates per (query, wave, lane group) of a tile, two tiles in turn
     __shared__ __align__(16) uint32_t s_cnt[EMIT ? 2 : 1][16][16];
+    // EMIT: each lane's 16 scores of the last tile (fp32 bits), [wave][key slot]
+    // [lane] (a lane reads back only its own, at any slot: no bank conflicts)
+    __shared__ uint32_t s_ek[EMIT ? 4 : 1][EMIT ? 16 : 1][64];
 
     // the wave's 64 keys as A operands: key tile kt, row col = key jw + 16*kt + col
     bf16x8 kv[4][8];
@@ -279,18 +297,18 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
         if (t < a.n_q) {
             const size_t blk = (size_t)(b * a.n_q + t) * a.kblocks + kblk;
             uint2 *dst = a.cands + blk * kTopkBlockSlots;
-            uint32_t slot = before;
-#pragma unroll
-            for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    if ((e_mask >> (4 * kt + r)) & 1u) {
-                        if (slot < (uint32_t)kTopkBlockSlots)
-                            dst[slot] = make_uint2(score_key(e_c[kt][r]),
-                                                   (uint32_t)(jw + 16 * kt + 4 * grp + r));
-                        ++slot;
-                    }
-                }
+            // one store per candidate of the lane, in slot order: the wave
+            // issues as many stores as its busiest lane has candidates (about
+            // one), not one per key slot
+            uint32_t slot = before, m = e_mask;
+            while (m) {
+                const int j = __builtin_ctz(m);
+                m &= m - 1u;
+                if (slot < (uint32_t)kTopkBlockSlots)
+                    dst[slot] = make_uint2(score_key(__uint_as_float(s_ek[wave][j][lane])),
+                                           (uint32_t)(jw + 16 * (j >> 2) + 4 * grp + (j & 3)));
+                ++slot;
+            }
             if (me == 0) a.cand_count[blk] = total;
         }
         e_qt = -1;
@@ -324,15 +342,29 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
                     bf16x8, *reinterpret_cast<const u32x4 *>(&s_q[qt & 1][col][kb * 32 + grp * 8]));
             if (EMIT) {
                 score_regs(kv, qv, e_c);
+                // candidates decided in fp32 against the row's threshold; the
+                // per-key causal test only on tiles where some query of the
+                // tile does not see all of this wave's keys (uniform)
+                const float thf = thresh_float(th_cur);
                 e_mask = 0u;
+                if (tile_limit_min(n_cur) >= jw + kPfWaveKeys) {
 #pragma unroll
-                for (int kt = 0; kt < 4; ++kt)
+                    for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const bool cand = jw + 16 * kt + 4 * grp + r < n_cur &&
-                                          score_key(e_c[kt][r]) >= th_cur;
-                        e_mask |= (cand ? 1u : 0u) << (4 * kt + r);
-                    }
+                        for (int r = 0; r < 4; ++r) {
+                            e_mask |= (e_c[kt][r] >= thf ? 1u : 0u) << (4 * kt + r);
+                            s_ek[wave][4 * kt + r][lane] = __float_as_uint(e_c[kt][r]);
+                        }
+                } else {
+#pragma unroll
+                    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const bool cand = jw + 16 * kt + 4 * grp + r < n_cur && e_c[kt][r] >= thf;
+                            e_mask |= (cand ? 1u : 0u) << (4 * kt + r);
+                            s_ek[wave][4 * kt + r][lane] = __float_as_uint(e_c[kt][r]);
+                        }
+                }
                 s_cnt[qt & 1][col][wave * 4 + grp] = (uint32_t)__popc(e_mask);
                 e_qt = qt;
             } else {

@@ -473,34 +473,27 @@ __device__ __forceinline__ uint32_t row16_incl_scan(uint32_t v) {
 
 constexpr int kShortFinish = 64;  // candidates left when one wave ranks them directly
 
-template <int NT>  // NT * kShortKeys >= max_len
-__global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
+// LDS of short_select<NT>.
+template <int NT>
+struct ShortSelectLds {
+    uint32_t cnt[2][NT / 64][8];  // per round: each wave's 16 digit counts, two per word
+    uint32_t wave[2 * (NT / 64)];
+    uint32_t pack[kShortFinish];
+    uint32_t tau[2];
+};
+
+// tau, the k-th largest of the keys key[j] (j with bit j of vmask set) held by
+// the NT threads of the workgroup (k at most their number), and r, the number
+// of keys equal to tau among the k largest.  Every thread calls it; every
+// thread gets the same tau and r.  first_round > 0: every valid key shares the
+// digits of prefix0 above bit 32 - 4 first_round (the caller found them), and
+// those rounds are skipped.
+template <int NT>
+__device__ void short_select(const uint32_t (&key)[kShortKeys], uint32_t vmask, uint32_t k,
+                             ShortSelectLds<NT> &sm, uint32_t &tau, uint32_t &r,
+                             int first_round = 0, uint32_t prefix0 = 0u) {
     constexpr int NW = NT / 64;
-    __shared__ uint32_t s_cnt[2][NW][8];  // per round: each wave's 16 digit counts, two per word
-    __shared__ uint32_t s_wave[2 * NW];
-    __shared__ uint32_t s_pack[kShortFinish];
-    __shared__ uint32_t s_tau[2];
-
-    const int row = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const float *srow = a.scores + (size_t)row * a.max_len;
-    const int p0 = tid * kShortKeys;
-    // loads issued before the row's length is known (clamped to its capacity)
-    uint32_t key[kShortKeys];
-#pragma unroll
-    for (int j = 0; j < kShortKeys; ++j) key[j] = score_key(srow[min(p0 + j, a.max_len - 1)]);
-    const int b = row / a.n_q;
-    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
-    const int k = a.top_k;
-    int32_t *out = a.idx + (size_t)row * k;
-    if (n <= k) {  // every valid key is selected
-        for (int i = tid; i < k; i += NT) out[i] = i < n ? i : -1;
-        if (tid == 0) a.n_sel[row] = n;
-        return;
-    }
-    const int nv = min(max(n - p0, 0), kShortKeys);  // this thread's valid keys: key[0 .. nv)
-    const uint32_t vmask = (1u << nv) - 1u;              // as a bit mask (nv <= 16)
-
     // Lane l < 16 follows digit d = 15 - l (an inclusive prefix over lanes is
     // then a suffix over digits); digit d is half (d >> 2) & 1 of word
     // 4 (d & 1) + 2 (d >> 3) + ((d >> 1) & 1) of the counts.
@@ -509,12 +502,14 @@ __global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
     const int dhalf = 16 * ((dg >> 2) & 1);
 
     // prefix: the digits of tau fixed so far; need: keys matching it still to be taken
-    uint32_t prefix = 0u, pmask = 0u, need = (uint32_t)k;
-    uint32_t tau = 0u, r = 0u;
+    uint32_t pmask = first_round ? ~0u << (32 - 4 * first_round) : 0u;
+    uint32_t prefix = prefix0 & pmask, need = k;
+    tau = prefix;
+    r = need;
 #pragma unroll 1
-    for (int round = 0; round < 8; ++round) {
+    for (int round = first_round; round < 8; ++round) {
         const int shift = 28 - 4 * round;
-        uint32_t(*buf)[8] = s_cnt[round & 1];
+        uint32_t(*buf)[8] = sm.cnt[round & 1];
         wave_digit_counts<kShortKeys>(key, vmask, shift, prefix, pmask, lane, buf[wave]);
         __syncthreads();
         uint32_t c = 0u;  // lanes 0..15: keys of digit dg summed over the waves
@@ -534,7 +529,7 @@ __global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
             tau = prefix;
             r = need;
         } else if (left <= (uint32_t)kShortFinish) {
-            // Few keys still match: pack them (in position order) into one wave,
+            // Few keys still match: pack them (in thread order) into one wave,
             // which ranks them directly.  tau is the need-th largest of them.
             uint32_t mb = 0u;
 #pragma unroll
@@ -542,13 +537,13 @@ __global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
                 mb |= (((key[j] ^ prefix) & pmask) == 0u ? 1u : 0u) << j;
             mb &= vmask;
             uint32_t before, unused0, total, unused1;
-            block_excl_scan2<NT>((uint32_t)__popc(mb), 0u, s_wave, before, unused0, total, unused1);
+            block_excl_scan2<NT>((uint32_t)__popc(mb), 0u, sm.wave, before, unused0, total, unused1);
 #pragma unroll
             for (int j = 0; j < kShortKeys; ++j)
-                if ((mb >> j) & 1u) s_pack[before++] = key[j];
+                if ((mb >> j) & 1u) sm.pack[before++] = key[j];
             __syncthreads();
             if (wave == 0) {
-                const uint32_t cv = lane < (int)left ? s_pack[lane] : 0u;
+                const uint32_t cv = lane < (int)left ? sm.pack[lane] : 0u;
                 uint32_t gt = 0u, eq = 0u;
                 for (uint32_t i = 0; i < left; ++i) {
                     const uint32_t ci = (uint32_t)__builtin_amdgcn_readlane((int)cv, (int)i);
@@ -557,16 +552,43 @@ __global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
                 }
                 const uint64_t hit = __ballot(lane < (int)left && gt < need && need <= gt + eq);
                 if (lane == (hit ? __builtin_ctzll(hit) : 0)) {
-                    s_tau[0] = cv;
-                    s_tau[1] = need - gt;
+                    sm.tau[0] = cv;
+                    sm.tau[1] = need - gt;
                 }
             }
             __syncthreads();
-            tau = s_tau[0];
-            r = s_tau[1];
+            tau = sm.tau[0];
+            r = sm.tau[1];
             break;
         }
     }
+}
+
+template <int NT>  // NT * kShortKeys >= max_len
+__global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
+    __shared__ ShortSelectLds<NT> sm;
+
+    const int row = blockIdx.x;
+    const int tid = threadIdx.x;
+    const float *srow = a.scores + (size_t)row * a.max_len;
+    const int p0 = tid * kShortKeys;
+    // loads issued before the row's length is known (clamped to its capacity)
+    uint32_t key[kShortKeys];
+#pragma unroll
+    for (int j = 0; j < kShortKeys; ++j) key[j] = score_key(srow[min(p0 + j, a.max_len - 1)]);
+    const int b = row / a.n_q;
+    const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+    const int k = a.top_k;
+    int32_t *out = a.idx + (size_t)row * k;
+    if (n <= k) {  // every valid key is selected
+        for (int i = tid; i < k; i += NT) out[i] = i < n ? i : -1;
+        if (tid == 0) a.n_sel[row] = n;
+        return;
+    }
+    const int nv = min(max(n - p0, 0), kShortKeys);  // this thread's valid keys: key[0 .. nv)
+    const uint32_t vmask = (1u << nv) - 1u;              // as a bit mask (nv <= 16)
+    uint32_t tau, r;
+    short_select<NT>(key, vmask, (uint32_t)k, sm, tau, r);
 
     // this thread's keys above tau and equal to tau, as bit masks over j
     uint32_t sbits = 0u, tbits = 0u;
@@ -578,7 +600,7 @@ __global__ __launch_bounds__(NT) void topk_short_kernel(TopkRowArgs a) {
     sbits &= vmask;
     tbits &= vmask;
     uint32_t sure_before, tie_before, sure_total, tie_total;
-    block_excl_scan2<NT>((uint32_t)__popc(sbits), (uint32_t)__popc(tbits), s_wave, sure_before,
+    block_excl_scan2<NT>((uint32_t)__popc(sbits), (uint32_t)__popc(tbits), sm.wave, sure_before,
                          tie_before, sure_total, tie_total);
     uint32_t take = tie_before < r ? r - tie_before : 0u;  // ties this thread may still keep
     uint32_t keep = sbits;
@@ -618,6 +640,7 @@ struct SampleArgs {
     const int32_t *seq_lens;
     const int32_t *q_pos;
     uint32_t *thresh;        // [rows]
+    uint32_t *slow;          // [1 + rows]: its count is cleared here for the selection pass
     int n_q, max_len, causal, top_k, cols, rank;
 };
 
@@ -633,6 +656,7 @@ __global__ __launch_bounds__(kSampleThreads) void topk_sample_thresh_kernel(Samp
     __shared__ __align__(16) uint32_t hist[kHistWords];
     __shared__ uint32_t s_res[2];
     const int row = blockIdx.x, b = row / a.n_q, tid = threadIdx.x;
+    if (row == 0 && tid == 0) a.slow[0] = 0u;
     const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
     const int m = div_up(n, kTopkSampleStride);  // valid samples
     if (n <= a.top_k || m <= a.rank) {
@@ -685,18 +709,36 @@ struct CandArgs {
     const uint16_t *q_idx;
     const uint16_t *k_idx;
     const int32_t *page_table;
+    uint32_t *slow;              // [1 + rows]: count, then the rows left for the slow way
     int n_q, max_len, causal, top_k, words_max, cand_cap, page_shift, max_pages, kblocks;
 };
 
-static_assert(kMaxLen / kTopkKeyBlock <= kRowThreads, "one key block per thread");
+// Selection from the candidates, one 512-thread workgroup per row: the row's
+// kept candidates are copied to LDS in key-block order (thread t copies those
+// of its BPT consecutive blocks, at its offset from a workgroup prefix of the
+// block counts), each thread takes 16 consecutive ones into registers and
+// short_select fixes tau and the number r of ties to keep; then each thread
+// turns its own blocks' candidates into bitmap words of the keys above tau and
+// of those equal to tau over the blocks' positions (8 words per 256-key block),
+// so that one more workgroup prefix orders the output by position (the slots
+// of a block are not in position order).  A row whose candidates do not decide
+// its set (a block with more than the slots, fewer than k, more than kCandCap)
+// is appended to the slow list for topk_cand_slow_kernel.
+constexpr int kCandThreads = 512;
+constexpr int kCandCap = kCandThreads * kShortKeys;  // candidates held in registers
+static_assert(kMaxLen / kTopkKeyBlock <= 2 * kCandThreads, "at most two key blocks per thread");
+static_assert(kTopkKeyBlock == 8 * 32, "a block's positions are 8 bitmap words");
 
-__global__ __launch_bounds__(kRowThreads) void topk_cand_kernel(CandArgs a) {
-    constexpr int NW = kRowThreads / 64;
-    extern __shared__ __align__(16) uint32_t lds[];
-    __shared__ uint32_t s_wave[2 * NW];
-    __shared__ uint32_t s_res[2];
-    __shared__ uint32_t s_cand_count;
-    __shared__ __align__(16) uint32_t s_q[128];  // the row's index query (slow way)
+template <int BPT>  // key blocks per thread
+__global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a) {
+    constexpr int NT = kCandThreads;
+    constexpr int NW = NT / 64;
+    constexpr int NWD = 8 * BPT;  // bitmap words per thread
+    constexpr int kFirst = 24;    // entries of a block loaded in the first batch (about 8 expected)
+    extern __shared__ __align__(16) uint32_t lds[];  // [kCandCap] keys, then [kCandCap] positions
+    __shared__ ShortSelectLds<NT> sm;
+    __shared__ uint32_t s_andor[2][NW];
+    uint32_t *s_key = lds, *s_pos = lds + kCandCap;
 
     const int row = blockIdx.x, b = row / a.n_q, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -704,100 +746,189 @@ __global__ __launch_bounds__(kRowThreads) void topk_cand_kernel(CandArgs a) {
     const int k = a.top_k;
     int32_t *out = a.idx + (size_t)row * k;
     if (n <= k) {  // every valid key is selected
-        for (int i = tid; i < k; i += kRowThreads) out[i] = i < n ? i : -1;
+        for (int i = tid; i < k; i += NT) out[i] = i < n ? i : -1;
         if (tid == 0) a.n_sel[row] = n;
         return;
     }
-    uint32_t *hist = lds;                     // kHistWords
-    uint32_t *low = hist + kHistWords;        // kLowBins
-    uint32_t *sure = low + kLowBins;          // words_max
-    uint32_t *tie = sure + a.words_max;       // words_max
-    uint32_t *ckey = tie + a.words_max;       // cand_cap
-    uint32_t *cidx = ckey + a.cand_cap;       // cand_cap
-    // the row's candidates: block kb's count and its first slots; a block count
-    // past the slots means some candidates were not kept
     const int nblk = div_up(n, kTopkKeyBlock);
-    const uint32_t cb = tid < nblk ? a.cand_count[(size_t)row * a.kblocks + tid] : 0u;
-    const uint32_t kept = min(cb, (uint32_t)kTopkBlockSlots);
-    uint32_t before, dummy0, cnt, lost;
-    block_excl_scan2<kRowThreads>(kept, cb - kept, s_wave, before, dummy0, cnt, lost);
-    if (lost == 0 && cnt >= (uint32_t)k && cnt <= (uint32_t)a.cand_cap) {
-        const int words = div_up(n, 1024) * 32;
-        if (tid < nblk) {  // blocks' first slots and counts, for the copy below
-            low[tid] = before;
-            hist[tid] = kept;
-        }
-        __syncthreads();
-        // slot s of the row's lists: block s / slots, entry s % slots; every
-        // thread loads all of its kept entries before storing any
-        const uint2 *src = a.cands + (size_t)row * a.kblocks * kTopkBlockSlots;
-        constexpr int kSlotsPerThread = kMaxLen / kTopkKeyBlock * kTopkBlockSlots / kRowThreads;
-        constexpr int kBatch = kSlotsPerThread / 2;  // loads in flight per thread
-        const int slots = nblk * kTopkBlockSlots;
+    // block counts, then at once the first kFirst entries of each of this
+    // thread's blocks (before the workgroup prefix that places them)
+    uint32_t kept[BPT], mine = 0u, lost_mine = 0u;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            uint2 e[kBatch];
+    for (int u = 0; u < BPT; ++u) {
+        const int kb = BPT * tid + u;
+        const uint32_t cb = kb < nblk ? a.cand_count[(size_t)row * a.kblocks + kb] : 0u;
+        kept[u] = min(cb, (uint32_t)kTopkBlockSlots);
+        mine += kept[u];
+        lost_mine += cb - kept[u];
+    }
+    uint2 e[BPT][kFirst];
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                const int sl = (h * kBatch + u) * kRowThreads + tid;
-                const int kb = sl / kTopkBlockSlots, q = sl % kTopkBlockSlots;
-                if (sl < slots && (uint32_t)q < hist[kb]) e[u] = src[sl];
-            }
+    for (int u = 0; u < BPT; ++u) {
+        const uint2 *src = a.cands + ((size_t)row * a.kblocks + BPT * tid + u) * kTopkBlockSlots;
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                const int sl = (h * kBatch + u) * kRowThreads + tid;
-                const int kb = sl / kTopkBlockSlots, q = sl % kTopkBlockSlots;
-                if (sl < slots && (uint32_t)q < hist[kb]) {
-                    ckey[low[kb] + q] = e[u].x;
-                    cidx[low[kb] + q] = e[u].y;
-                }
-            }
-        }
-        __syncthreads();
-        for (int x = tid; x < kCoarseBins; x += kRowThreads) hist[x] = 0u;
-        for (int w = tid; w < words; w += kRowThreads) {
-            sure[w] = 0u;
-            tie[w] = 0u;
-        }
-        __syncthreads();
-        for (uint32_t i = tid; i < cnt; i += kRowThreads) atomicAdd(&hist[ckey[i] >> kCoarseShift], 1u);
-        __syncthreads();
-        find_threshold_bin<kCoarseBins>(hist, (uint32_t)k, s_res);
-        const uint32_t b1 = s_res[0];
-        const uint32_t need1 = (uint32_t)k - s_res[1];
-        for (uint32_t i = tid; i < cnt; i += kRowThreads)
-            if ((ckey[i] >> kCoarseShift) > b1) atomicOr(&sure[cidx[i] >> 5], 1u << (cidx[i] & 31));
-        auto visit = [&](auto &&fn) {
-            for (uint32_t i = tid; i < cnt; i += kRowThreads)
-                if ((ckey[i] >> kCoarseShift) == b1) fn(ckey[i], cidx[i]);
-        };
-        uint32_t r_ties;
-        refine_and_mark<kRowThreads>(visit, b1, need1, hist, low, s_res, sure, tie, r_ties);
-        __syncthreads();
-        compact_bitmaps<kRowThreads>(sure, tie, words, r_ties, k, out, s_wave);
-        if (tid == 0) a.n_sel[row] = k;
+        for (int v = 0; v < kFirst; ++v)
+            if ((uint32_t)v < kept[u]) e[u][v] = src[v];
+    }
+    uint32_t before, unused0, cnt, lost;
+    block_excl_scan2<NT>(mine, lost_mine, sm.wave, before, unused0, cnt, lost);
+    if (lost != 0 || cnt < (uint32_t)k || cnt > (uint32_t)kCandCap) {  // uniform
+        if (tid == 0) a.slow[1 + atomicAdd(&a.slow[0], 1u)] = (uint32_t)row;
         return;
     }
-    // The slow way: the row's scores on the vector units, then the per-row path.
-    if (tid < 128) s_q[tid] = reinterpret_cast<const uint32_t *>(a.q_idx + (size_t)row * 256)[tid];
-    __syncthreads();
-    float *srow = a.scores + (size_t)row * a.max_len;
-    for (int j = tid; j < n; j += kRowThreads) {
-        const uint16_t *kr = a.k_idx + token_offset(a.page_table, a.page_shift, a.max_pages,
-                                                    a.max_len, b, j, 256);
-        float acc = 0.0f;
-#pragma unroll 8
-        for (int p = 0; p < 32; ++p) {
-            const uint4 kv = *reinterpret_cast<const uint4 *>(kr + 8 * p);
-            const uint4 qv = *reinterpret_cast<const uint4 *>(&s_q[4 * p]);
-            acc = dot8_bf16(kv, qv, acc);
+    {
+        uint32_t at = before;
+#pragma unroll
+        for (int u = 0; u < BPT; ++u) {
+#pragma unroll
+            for (int v = 0; v < kFirst; ++v)
+                if ((uint32_t)v < kept[u]) {
+                    s_key[at + v] = e[u][v].x;
+                    s_pos[at + v] = e[u][v].y;
+                }
+            const uint2 *src = a.cands + ((size_t)row * a.kblocks + BPT * tid + u) * kTopkBlockSlots;
+            for (uint32_t q0 = kFirst; q0 < kept[u]; q0 += 8) {  // rare: more than kFirst candidates
+                uint2 x[8];
+#pragma unroll
+                for (int v = 0; v < 8; ++v)
+                    if (q0 + v < kept[u]) x[v] = src[q0 + v];
+#pragma unroll
+                for (int v = 0; v < 8; ++v)
+                    if (q0 + v < kept[u]) {
+                        s_key[at + q0 + v] = x[v].x;
+                        s_pos[at + q0 + v] = x[v].y;
+                    }
+            }
+            at += kept[u];
         }
-        srow[j] = acc;
     }
     __syncthreads();
-    row_topk(srow, nullptr, n, k, a.words_max, a.cand_cap, out, lds, s_wave, s_res,
-             &s_cand_count);
+    uint32_t key[kShortKeys];
+#pragma unroll
+    for (int j = 0; j < kShortKeys; ++j) key[j] = s_key[tid * kShortKeys + j];
+    const int nv = min(max((int)cnt - tid * kShortKeys, 0), kShortKeys);
+    const uint32_t vmask = (1u << nv) - 1u;
+    // The candidates crowd above the row's threshold, so their keys share their
+    // leading digits: AND and OR of every valid key fix those digits at once.
+    uint32_t kand = ~0u, kor = 0u;
+#pragma unroll
+    for (int j = 0; j < kShortKeys; ++j)
+        if ((vmask >> j) & 1u) {
+            kand &= key[j];
+            kor |= key[j];
+        }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        kand &= (uint32_t)__shfl_xor((int)kand, m);
+        kor |= (uint32_t)__shfl_xor((int)kor, m);
+    }
+    if (lane == 0) {
+        s_andor[0][wave] = kand;
+        s_andor[1][wave] = kor;
+    }
+    __syncthreads();
+    kand = ~0u;
+    kor = 0u;
+#pragma unroll
+    for (int x = 0; x < NW; ++x) {
+        kand &= s_andor[0][x];
+        kor |= s_andor[1][x];
+    }
+    const uint32_t differ = kand ^ kor;  // bits in which some valid keys differ
+    const int first_round = differ ? __builtin_clz(differ) / 4 : 8;
+    uint32_t tau, r;
+    if (first_round == 8) {  // every candidate equal: the first k of them
+        tau = kand;
+        r = (uint32_t)k;
+    } else {
+        short_select<NT>(key, vmask, (uint32_t)k, sm, tau, r, first_round, kand);
+    }
+
+    // this thread's blocks (positions 256 BPT tid ..): keys above / equal to tau
+    const uint32_t p_first = (uint32_t)tid * BPT * kTopkKeyBlock;
+    uint32_t sw[NWD], tw[NWD];
+#pragma unroll
+    for (int i = 0; i < NWD; ++i) sw[i] = tw[i] = 0u;
+    for (uint32_t q = 0; q < mine; ++q) {
+        const uint32_t kk = s_key[before + q];
+        const uint32_t p = s_pos[before + q] - p_first;  // 0 .. 256 BPT - 1
+        const uint32_t bit = 1u << (p & 31u), wi = p >> 5;
+        const uint32_t sb = kk > tau ? bit : 0u, tb = kk == tau ? bit : 0u;
+#pragma unroll
+        for (int i = 0; i < NWD; ++i) {
+            sw[i] |= wi == (uint32_t)i ? sb : 0u;
+            tw[i] |= wi == (uint32_t)i ? tb : 0u;
+        }
+    }
+    uint32_t cs = 0u, ct = 0u;
+#pragma unroll
+    for (int i = 0; i < NWD; ++i) {
+        cs += (uint32_t)__popc(sw[i]);
+        ct += (uint32_t)__popc(tw[i]);
+    }
+    uint32_t sure_before, tie_before, sure_total, tie_total;
+    block_excl_scan2<NT>(cs, ct, sm.wave, sure_before, tie_before, sure_total, tie_total);
+    uint32_t take = tie_before < r ? r - tie_before : 0u;  // ties this thread may still keep
+#pragma unroll
+    for (int i = 0; i < NWD; ++i) {
+        for (; take && tw[i]; --take) {  // the first `take` ties in position order
+            sw[i] |= tw[i] & (0u - tw[i]);
+            tw[i] &= tw[i] - 1u;
+        }
+    }
+    uint32_t pos = sure_before + min(tie_before, r);
+#pragma unroll
+    for (int i = 0; i < NWD; ++i) {
+        uint32_t m = sw[i];
+        while (m) {
+            const int j = __builtin_ctz(m);
+            m &= m - 1u;
+            if (pos < (uint32_t)k) out[pos] = (int32_t)(p_first + 32 * i + j);
+            ++pos;
+        }
+    }
     if (tid == 0) a.n_sel[row] = k;
+}
+
+// Rows whose candidates do not decide the set (the slow list), the slow way:
+// the row's scores recomputed on the vector units into the score buffer, then
+// the per-row selection over them.  Each workgroup takes list entries
+// blockIdx.x, blockIdx.x + gridDim.x, ...
+__global__ __launch_bounds__(kRowThreads) void topk_cand_slow_kernel(CandArgs a) {
+    constexpr int NW = kRowThreads / 64;
+    extern __shared__ __align__(16) uint32_t lds[];
+    __shared__ uint32_t s_wave[2 * NW];
+    __shared__ uint32_t s_res[2];
+    __shared__ uint32_t s_cand_count;
+    __shared__ __align__(16) uint32_t s_q[128];  // the row's index query
+    const int tid = threadIdx.x;
+    const uint32_t count = a.slow[0];
+    for (uint32_t li = blockIdx.x; li < count; li += gridDim.x) {
+        const int row = (int)a.slow[1 + li], b = row / a.n_q;
+        const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
+        const int k = a.top_k;
+        int32_t *out = a.idx + (size_t)row * k;
+        if (tid < 128) s_q[tid] = reinterpret_cast<const uint32_t *>(a.q_idx + (size_t)row * 256)[tid];
+        __syncthreads();
+        float *srow = a.scores + (size_t)row * a.max_len;
+        for (int j = tid; j < n; j += kRowThreads) {
+            const uint16_t *kr = a.k_idx + token_offset(a.page_table, a.page_shift, a.max_pages,
+                                                        a.max_len, b, j, 256);
+            float acc = 0.0f;
+#pragma unroll 8
+            for (int p = 0; p < 32; ++p) {
+                const uint4 kv = *reinterpret_cast<const uint4 *>(kr + 8 * p);
+                const uint4 qv = *reinterpret_cast<const uint4 *>(&s_q[4 * p]);
+                acc = dot8_bf16(kv, qv, acc);
+            }
+            srow[j] = acc;
+        }
+        __syncthreads();
+        row_topk(srow, nullptr, n, k, a.words_max, a.cand_cap, out, lds, s_wave, s_res,
+                 &s_cand_count);
+        if (tid == 0) a.n_sel[row] = k;
+        __syncthreads();  // LDS reused by the next row
+    }
 }
 
 // ------------------------------------------------------------------------------------
@@ -1055,13 +1186,14 @@ bool topk_uses_two_pass(const Geometry &g) {
 
 hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
                                      const int32_t *seq_lens, const int32_t *q_pos,
-                                     uint32_t *thresh, hipStream_t stream) {
+                                     uint32_t *thresh, uint32_t *slow, hipStream_t stream) {
     if (g.rows == 0) return hipSuccess;
     SampleArgs a;
     a.samples = samples;
     a.seq_lens = seq_lens;
     a.q_pos = q_pos;
     a.thresh = thresh;
+    a.slow = slow;
     a.n_q = g.n_q;
     a.max_len = g.max_len;
     a.causal = g.causal;
@@ -1075,7 +1207,7 @@ hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
 hipError_t launch_topk_cands(const Geometry &g, const uint32_t *cand_count, const uint32_t *cands,
                              const int32_t *seq_lens, const int32_t *q_pos, const void *q_idx,
                              const void *k_idx, const int32_t *page_table, float *scores,
-                             int32_t *idx, int32_t *n_sel, hipStream_t stream) {
+                             uint32_t *slow, int32_t *idx, int32_t *n_sel, hipStream_t stream) {
     if (g.rows == 0) return hipSuccess;
     CandArgs a;
     a.cand_count = cand_count;
@@ -1097,11 +1229,23 @@ hipError_t launch_topk_cands(const Geometry &g, const uint32_t *cand_count, cons
     a.page_shift = g.page_shift;
     a.max_pages = g.max_pages;
     a.kblocks = topk_key_blocks(g);
-    const size_t lds = row_kernel_lds(g.max_len);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&topk_cand_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    a.slow = slow;
+    const size_t fast_lds = sizeof(uint32_t) * 2 * (size_t)kCandCap;
+    const bool two = a.kblocks > kCandThreads;  // more key blocks than threads
+    const void *fast = two ? reinterpret_cast<const void *>(&topk_cand_fast_kernel<2>)
+                           : reinterpret_cast<const void *>(&topk_cand_fast_kernel<1>);
+    hipError_t e = hipFuncSetAttribute(fast, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)fast_lds);
     if (e != hipSuccess) return e;
-    topk_cand_kernel<<<dim3(g.rows), dim3(kRowThreads), lds, stream>>>(a);
+    if (two) topk_cand_fast_kernel<2><<<dim3(g.rows), dim3(kCandThreads), fast_lds, stream>>>(a);
+    else topk_cand_fast_kernel<1><<<dim3(g.rows), dim3(kCandThreads), fast_lds, stream>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t lds = row_kernel_lds(g.max_len);
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&topk_cand_slow_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    topk_cand_slow_kernel<<<dim3(g.rows < 1024 ? g.rows : 1024), dim3(kRowThreads), lds, stream>>>(a);
     return hipGetLastError();
 }
 
