@@ -496,6 +496,52 @@ def run_schedules(args, w) -> int:
     return 0
 
 
+def run_project(args) -> int:
+    """Eq. 2 for a chunk of new tokens (the projections of the index query and key
+    and the shared K / V, written into the caches): 8192 rows of d_model 2560 on a
+    131072-token cache, 32 query / 8 KV heads (2560 output features), synthetic
+    bf16 activations and weights."""
+    import torch
+    from paper_2606_06467_amd import binding as B
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    rows, d_model, max_len, kv_heads = 8192, 2560, 131072, 8
+    n_feat = 512 + 2 * kv_heads * 128
+    g = torch.Generator(device=dev)
+    g.manual_seed(2606)
+    h = torch.randn((rows, d_model), generator=g, device=dev).to(torch.bfloat16)
+    wt = (torch.randn((n_feat, d_model), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+    pos = (max_len - rows + torch.arange(rows, device=dev)).to(torch.int32)
+    q_idx = torch.empty((rows, 256), dtype=torch.bfloat16, device=dev)
+    k_idx = torch.zeros((1, max_len, 256), dtype=torch.bfloat16, device=dev)
+    kc = torch.zeros((1, max_len, kv_heads * 128), dtype=torch.bfloat16, device=dev)
+    vc = torch.zeros_like(kc)
+    sh = B.make_shape(batch=1, n_q=rows, max_len=max_len, top_k=2048, q_heads=32,
+                      kv_heads=kv_heads, causal=True)
+
+    def call():
+        B.clsa_project_append(sh, d_model, h, wt, pos, None, q_idx, k_idx, kc, vc)
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    flops = 2 * rows * n_feat * d_model
+    tf = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({"metric": "Eq. 2 projection + cache append, 8192 new tokens", "value": round(ms * 1e3, 2),
+                      "unit": "us/call", "steps": args.steps, "warmup": args.warmup,
+                      "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+                      "config": {"rows": rows, "d_model": d_model, "features": n_feat, "context": max_len},
+                      "roofline": {"bound": "mfma", "kernel": "project_gemm_kernel", "achieved": round(tf, 1),
+                                   "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                                   "algorithmic_flops_per_launch": flops}}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -514,6 +560,10 @@ def main() -> int:
                     help="instead of the decode step, time the training-side distillation step "
                          "(Eq. 5 target, Eq. 6 loss and indexer gradient) on the 32K-token "
                          "sequence workload (one JSON line)")
+    ap.add_argument("--project", action="store_true",
+                    help="instead of the decode step, time the Eq. 2 projection with its cache "
+                         "writes (clsa_project_append) for a chunk of 8192 new tokens at "
+                         "d_model 2560 (one JSON line)")
     ap.add_argument("--top-k", type=int, default=0,
                     help="run the workload with this top_k instead of its own (the workload "
                          "name gets a _k<K> suffix); e.g. index sets whose rows fit the L2")
@@ -535,6 +585,8 @@ def main() -> int:
     if args.kd:
         wl = args.workload if args.workload in inputs.KD_WORKLOADS else inputs.KD_WORKLOADS[0]
         return run_kd(args, inputs.workload(wl))
+    if args.project:
+        return run_project(args)
     w = inputs.workload(args.workload)
     if args.top_k > 0:
         w = dataclasses.replace(w, name=f"{w.name}_k{args.top_k}", top_k=args.top_k)

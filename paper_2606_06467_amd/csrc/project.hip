@@ -17,9 +17,12 @@
 //     its first product, and the eight partial tiles are added in LDS: the
 //     weights (13 MB at d_model 2560, the bytes that bound this case) are then
 //     read by 160 workgroups at once;
-//   * many rows (prefill): four waves per workgroup on four row tiles of the
-//     same 64 features (their weight loads meet in L1), each over all of
-//     d_model with the next step's loads issued before the current products.
+//   * many rows (prefill): a tiled product, 128 rows x 128 features per
+//     workgroup of 4 waves (64 x 64 each, 4 x 4 tiles of 16 x 16), d_model in
+//     steps of 64 staged through LDS (double-buffered: the next step's global
+//     loads are in flight during the current products); the 128-feature tile
+//     lies in one destination (index query, index key, K or V), so the bf16
+//     results go back through LDS and leave as whole 256-byte rows.
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -28,7 +31,6 @@ namespace clsa {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kProjFeat = 64;      // output features per wave tile
 constexpr int kSplitWaves = 8;     // d_model split of the few-rows kernel
 constexpr int kSplitMaxD = 3072;   // largest d_model of the few-rows kernel (register budget)
 
@@ -41,6 +43,7 @@ struct ProjArgs {
     uint16_t *k_idx;           // index-key cache
     uint16_t *k_cache, *v_cache;
     int rows, d, n_q, max_len, page_shift, max_pages, kvw;  // kvw = kv_heads * 128
+    int rtiles, ftiles, band;  // tiled kernel: 128-row and 128-feature tiles, row tiles per band
 };
 
 __device__ __forceinline__ bf16x8 ld8(const uint16_t *p) {
@@ -105,43 +108,144 @@ __global__ __launch_bounds__(512) void project_splitk_kernel(ProjArgs a) {
     }
 }
 
-// Many rows: four waves on four 16-row tiles of the same 64 features.
+// Many rows: the tiled product.
+constexpr int kGemmM = 128, kGemmN = 128, kGemmK = 64;
+constexpr int kGemmPitch = kGemmK + 8;       // bf16 per staged row (16 bytes of padding)
+constexpr int kGemmOutPitch = kGemmN + 8;    // bf16 per staged output row
+constexpr size_t kGemmLds = sizeof(uint16_t) * 2 * 2 * kGemmM * kGemmPitch;
+
 template <bool PAGED>
-__global__ __launch_bounds__(256) void project_rows_kernel(ProjArgs a) {
-    const int ft = blockIdx.x;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+__global__ __launch_bounds__(256, 2) void project_gemm_kernel(ProjArgs a) {
+    // two stages of A (rows of h) and B (features of w), 128 x 64 bf16 each
+    // (dynamic LDS, kGemmLds bytes); the output tile (128 x 128 bf16) reuses it
+    extern __shared__ __align__(16) uint16_t s_lds[];
+    uint16_t(*s_ab)[2][kGemmM][kGemmPitch] =
+        reinterpret_cast<uint16_t(*)[2][kGemmM][kGemmPitch]>(s_lds);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 15, grp = lane >> 4;
-    const int r0 = (blockIdx.y * 4 + wave) * 16;
-    if (r0 >= a.rows) return;  // uniform per wave; no barriers
-    const uint16_t *hp = a.h + (size_t)min(r0 + col, a.rows - 1) * a.d + grp * 8;
-    const uint16_t *wp = a.w + (size_t)(ft * kProjFeat + col) * a.d + grp * 8;
-    const size_t wct = (size_t)16 * a.d;  // next feature tile
-    f32x4 c[4];
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct) c[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bf16x8 a0, a1, b0[4], b1[4];
-    auto load = [&](int kb, bf16x8 &av, bf16x8 (&bv)[4]) {
-        av = ld8(hp + kb);
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) bv[ct] = ld8(wp + ct * wct + kb);
-    };
-    auto mma = [&](const bf16x8 &av, const bf16x8 (&bv)[4]) {
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
-            c[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv[ct], c[ct], 0, 0, 0);
-    };
-    load(0, a0, b0);
-    for (int kb = 0; kb < a.d; kb += 64) {  // d is a multiple of 512
-        load(kb + 32, a1, b1);
-        mma(a0, b0);
-        if (kb + 64 < a.d) load(kb + 64, a0, b0);
-        mma(a1, b1);
+    const int wm = wave >> 1, wn = wave & 1;  // the wave's 64 x 64 quadrant
+    // Tile order: workgroups are dealt to the 8 XCDs in turn (L mod 8); XCD x
+    // takes bands of `band` row tiles (8, fewer when there are few rows) and
+    // walks, for each band, the feature tiles with the band's row tiles next to
+    // each other, so that the workgroups in flight on an XCD share a few row
+    // tiles and feature tiles per 64-wide step of d_model (their slices meet in
+    // its L2).
+    int rt, ft;
+    {
+        const int L = blockIdx.x, x = L & 7, q = L >> 3;
+        const int per_band = a.band * a.ftiles;          // workgroups of one band
+        const int band = 8 * (q / per_band) + x;         // bands dealt to the XCDs in turn
+        const int qi = q % per_band;
+        rt = a.band * band + qi % a.band;
+        ft = qi / a.band;
     }
+    if (rt >= a.rtiles) return;  // uniform: padding workgroups of the last bands
+    const int f0 = ft * kGemmN, r0 = rt * kGemmM;
+    // staging: thread t moves 16-byte pieces t + 256 i (i < 4) of each 128 x 64
+    // tile: row (t >> 3) + 32 i, columns 8 (t & 7) .. + 8
+    const int lrow = tid >> 3, lcol = (tid & 7) * 8;
+    const uint16_t *hp[4], *wp[4];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int i = 0; i < 4; ++i) {
+        hp[i] = a.h + (size_t)min(r0 + lrow + 32 * i, a.rows - 1) * a.d + lcol;  // tail rows: never stored
+        wp[i] = a.w + (size_t)(f0 + lrow + 32 * i) * a.d + lcol;
+    }
+    // two register sets: the loads for step k + 2 are issued while step k is
+    // computed, and step k + 1 (loaded a step earlier) goes to LDS after it;
+    // every step issues its loads (the last two reload a valid step that is
+    // never stored), so that the compiler's wait before each LDS store leaves
+    // the newest 8 loads in flight
+    u32x4 ra[2][4], rb[2][4];
+    auto gload = [&](int set, int k0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-            store_feature<PAGED>(a, r0 + 4 * grp + r, ft * kProjFeat + ct * 16 + col, c[ct][r]);
+        for (int i = 0; i < 4; ++i) {
+            ra[set][i] = *reinterpret_cast<const u32x4 *>(hp[i] + k0);
+            rb[set][i] = *reinterpret_cast<const u32x4 *>(wp[i] + k0);
+        }
+    };
+    auto lstore = [&](int set, int st) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            *reinterpret_cast<u32x4 *>(&s_ab[st][0][lrow + 32 * i][lcol]) = ra[set][i];
+            *reinterpret_cast<u32x4 *>(&s_ab[st][1][lrow + 32 * i][lcol]) = rb[set][i];
+        }
+    };
+    f32x4 c[4][4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) c[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nk = a.d / kGemmK;  // even (d_model is a multiple of 512)
+    gload(0, 0);
+    gload(1, kGemmK);
+    lstore(0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      for (int h = 0; h < 2; ++h) {   // unrolled by two so that register sets are static
+        const int k = kt + h;
+        const int st = h;
+        gload(h, min(k + 2, nk - 1) * kGemmK);  // unconditional (the last steps reload a valid step, never stored): a static load count
+#pragma unroll
+        for (int ks = 0; ks < kGemmK / 32; ++ks) {
+            bf16x8 av[4], bv[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                av[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(
+                                                       &s_ab[st][0][wm * 64 + t * 16 + col][ks * 32 + grp * 8]));
+                bv[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(
+                                                       &s_ab[st][1][wn * 64 + t * 16 + col][ks * 32 + grp * 8]));
+            }
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+                    c[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[mt], bv[nt], c[mt][nt], 0, 0, 0);
+        }
+        if (k + 1 < nk) lstore(h ^ 1, h ^ 1);
+        __syncthreads();
+      }
+    }
+    // bf16 results into LDS: C tile (mt, nt) row 4 grp + r, column col
+    uint16_t(*s_out)[kGemmOutPitch] = reinterpret_cast<uint16_t(*)[kGemmOutPitch]>(&s_ab[0][0][0][0]);
+    static_assert(kGemmLds >= sizeof(uint16_t) * kGemmM * kGemmOutPitch, "output tile fits");
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                s_out[wm * 64 + mt * 16 + 4 * grp + r][wn * 64 + nt * 16 + col] =
+                    (uint16_t)f32_to_bf16_bits(c[mt][nt][r]);
+    __syncthreads();
+    // whole rows out: 16 pieces of 16 bytes per row, 8 rows per pass of 128 threads
+    const int piece = tid & 15;
+    int dst_kind, width, fo;  // 0: index query, 1: index key, 2: K, 3: V
+    if (f0 < 256) { dst_kind = 0; width = 256; fo = f0; }
+    else if (f0 < 512) { dst_kind = 1; width = 256; fo = f0 - 256; }
+    else if (f0 < 512 + a.kvw) { dst_kind = 2; width = a.kvw; fo = f0 - 512; }
+    else { dst_kind = 3; width = a.kvw; fo = f0 - 512 - a.kvw; }
+    for (int rr = tid >> 4; rr < kGemmM; rr += 16) {
+        const int r = r0 + rr;
+        if (r >= a.rows) break;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(&s_out[rr][piece * 8]);
+        uint16_t *dst;
+        if (dst_kind == 0) {
+            dst = a.q_idx + (size_t)r * 256;
+        } else {
+            const int p = a.pos[r];
+            if (p < 0 || p >= a.max_len) continue;
+            const int b = r / a.n_q;
+            size_t row;
+            if (PAGED) {
+                const int page = a.page_table[(size_t)b * a.max_pages + (p >> a.page_shift)];
+                row = ((size_t)page << a.page_shift) + (p & ((1 << a.page_shift) - 1));
+            } else {
+                row = (size_t)b * a.max_len + p;
+            }
+            dst = (dst_kind == 1 ? a.k_idx : dst_kind == 2 ? a.k_cache : a.v_cache) + row * width;
+        }
+        *reinterpret_cast<u32x4 *>(dst + fo + piece * 8) = v;
+    }
 }
 
 bool project_supported(int d_model) {
@@ -175,7 +279,7 @@ hipError_t launch_project(const Geometry &g, int d_model, const void *h, const v
     a.max_pages = g.max_pages;
     a.kvw = g.kv_heads * 128;
     if (g.rows == 0) return hipSuccess;
-    const int n_feat = 512 + 2 * a.kvw;  // a multiple of 64
+    const int n_feat = 512 + 2 * a.kvw;  // a multiple of 256 (kv_heads * 128 per K and V)
     const bool paged = g.page_shift >= 0;
     if (g.rows <= 64 && d_model <= kSplitMaxD) {
         const dim3 grid(n_feat / 16, div_up(g.rows, 16));
@@ -190,11 +294,21 @@ hipError_t launch_project(const Geometry &g, int d_model, const void *h, const v
         }
         return hipGetLastError();
     }
-    const long row_groups = (g.rows + 63) / 64;
-    if (row_groups > 65535) return hipErrorInvalidConfiguration;
-    const dim3 grid(n_feat / kProjFeat, (unsigned)row_groups);
-    if (paged) project_rows_kernel<true><<<grid, dim3(256), 0, stream>>>(a);
-    else project_rows_kernel<false><<<grid, dim3(256), 0, stream>>>(a);
+    a.rtiles = div_up(g.rows, kGemmM);
+    a.ftiles = n_feat / kGemmN;
+    // bands of up to 8 row tiles, dealt to the 8 XCDs in turn (the last round
+    // padded); fewer row tiles per band when that still leaves XCDs idle
+    a.band = a.rtiles >= 64 ? 8 : div_up(a.rtiles, 8);
+    const long bands = div_up(a.rtiles, a.band);
+    const long blocks = div_up((int)bands, 8) * 8 * (long)a.band * a.ftiles;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)blocks);
+    const void *fn = paged ? reinterpret_cast<const void *>(&project_gemm_kernel<true>)
+                           : reinterpret_cast<const void *>(&project_gemm_kernel<false>);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGemmLds);
+    if (e != hipSuccess) return e;
+    if (paged) project_gemm_kernel<true><<<grid, dim3(256), kGemmLds, stream>>>(a);
+    else project_gemm_kernel<false><<<grid, dim3(256), kGemmLds, stream>>>(a);
     return hipGetLastError();
 }
 

@@ -92,3 +92,16 @@ def test_many_rows_chunk():
                               q_pos0=(500, 600), n_layers=1, wid=105)
     pos = np.concatenate([np.arange(500, 600), np.arange(600, 700)]).astype(np.int32)
     _case(w, 1024, pos, 15, "200 rows")
+
+
+def test_many_rows_tiles_ragged_paged():
+    """The tiled kernel: 600 rows (four 128-row tiles and a tail of 88), paged
+    caches, d_model 2560; every 50th position past the cache and one negative,
+    so those rows write their index query only."""
+    T = 300
+    w = inputs.small_workload(batch=2, lens=(2000, 2400), n_q=T, causal=True,
+                              q_pos0=(1700, 2100), page_size=64, n_layers=1, wid=106)
+    pos = np.concatenate([np.arange(1700, 2000), np.arange(2100, 2400)]).astype(np.int32)
+    pos[::50] = w.max_len
+    pos[7] = -1
+    _case(w, 2560, pos, 16, "600 rows, tiles + tail, paged")
