@@ -173,6 +173,7 @@ struct DecodeWs {
     uint32_t *cand_count = nullptr;  // [rows, key blocks]
     uint32_t *cands = nullptr;     // [rows, key blocks, kTopkBlockSlots, 2]
     uint32_t *slow = nullptr;      // [1 + rows]: rows selected the slow way
+    uint32_t *tickets = nullptr;   // [rows, kv_heads]: split arrivals of the in-kernel merge
 };
 
 // Every layer gathers its K/V rows from the cache through the shared index set.
@@ -192,6 +193,7 @@ size_t carve_decode(const Geometry &g, void *base, DecodeWs &w) {
         w.topk.counts = c.take<uint32_t>(L.count_u32);
     }
     w.partials = c.take<float>(clsa::attn_partial_floats(g));
+    w.tickets = c.take<uint32_t>((size_t)g.rows * g.kv_heads);
     if (clsa::topk_uses_two_pass(g)) {
         w.samples = c.take<float>((size_t)g.rows * clsa::topk_sample_cols(g));
         w.thresh = c.take<uint32_t>(g.rows);
@@ -273,7 +275,7 @@ clsa_status clsa_index_scores(const clsa_shape *shape, const void *q_idx, const 
         return from_hip(clsa::launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos,
                                                    scores, st));
     return from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, scores,
-                                              nullptr, st));
+                                              nullptr, nullptr, st));
 }
 
 clsa_status clsa_topk(const clsa_shape *shape, const float *scores, const int32_t *seq_lens,
@@ -317,7 +319,8 @@ clsa_status clsa_sparse_attn(const clsa_shape *shape, const void *q, const void 
     AttnWs w;
     carve_attn(g, c, w);
     return from_hip(clsa::launch_sparse_attn(g, q, k_cache, v_cache, page_table, idx, n_sel, out,
-                                             lse, w.partials, static_cast<hipStream_t>(stream)));
+                                             lse, w.partials, nullptr,
+                                             static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"
@@ -371,6 +374,9 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
     const size_t lse_stride = (size_t)g.rows * g.q_heads;
     const size_t set_stride = (size_t)g.rows * g.top_k;         // index entries per set
     const int n_sets = n_layers > 0 ? (n_layers + group - 1) / group : 1;
+    // The decode indexer clears the attention's arrival counters, so only steps
+    // that run it merge the splits inside the attention kernel.
+    uint32_t *tickets = !two_pass && !mfma ? w.tickets : nullptr;
     for (int s = 0; s < n_sets; ++s) {
         const uint16_t *qi = static_cast<const uint16_t *>(q_idx) + (size_t)s * q_idx_stride;
         const uint16_t *ki = static_cast<const uint16_t *>(k_idx) + (size_t)s * k_idx_stride;
@@ -403,7 +409,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
             else
                 CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
                                                             w.scores, idx_hist ? w.topk.hist : nullptr,
-                                                            st)));
+                                                            w.tickets, st)));
             if (first && hook && hipEventRecord(t_hook.ev[1], st) != hipSuccess) return CLSA_ERR_HIP;
             CLSA_TRY(from_hip(clsa::launch_topk(g, w.scores, seq_lens, q_pos, w.topk, idx_hist, is,
                                                 ns, st)));
@@ -418,7 +424,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
             if (mark && hipEventRecord(t_hook.ev[4 + 2 * l], st) != hipSuccess)
                 return CLSA_ERR_HIP;
             CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, is,
-                                                       ns, ol, lsel, w.partials, st,
+                                                       ns, ol, lsel, w.partials, tickets, st,
                                                        mark ? t_hook.ev[5 + 2 * l] : nullptr)));
         }
     }

@@ -60,10 +60,12 @@ hipError_t take_device_error_kd(uint32_t *bits);
 
 // ---- index_decode.hip ----
 // coarse_hist: [rows, kCoarseBins], zero on entry, or NULL for no histogram.
+// attn_tickets: [rows, kv_heads] counters of the attention that follows, set to
+// zero by this launch, or NULL.
 hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void *k_idx,
                                const int32_t *page_table, const int32_t *seq_lens,
                                const int32_t *q_pos, float *scores, uint32_t *coarse_hist,
-                               hipStream_t stream);
+                               uint32_t *attn_tickets, hipStream_t stream);
 
 // ---- index_prefill.hip ----
 // Query rows per sequence from which the indexer runs on the matrix cores.
@@ -140,11 +142,13 @@ hipError_t launch_zero_u32(uint32_t *p, size_t n, hipStream_t stream);
 size_t attn_partial_floats(const Geometry &g, bool dense = false);
 // Attention gathering K/V rows from the cache through idx (and the page table).
 // split_done, if not null, is recorded right after the attention kernel, before
-// the split merge.
+// the split merge.  tickets: [rows, kv_heads] arrival counters, zero on entry and
+// zero again on return, or NULL; with them, decode grids of at most
+// kFusedMaxSplits splits merge the splits inside the attention kernel.
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
-                              float *partials, hipStream_t stream,
+                              float *partials, uint32_t *tickets, hipStream_t stream,
                               hipEvent_t split_done = nullptr);
 // Dense attention of every row over all of its valid keys (seq_lens, and q_pos
 // when causal), same layouts as the sparse call.

@@ -31,6 +31,8 @@ struct IndexArgs {
     float *scores;
     uint32_t *hist;
     int n_q, max_len, page_shift, max_pages, causal, groups_per_row, tiles_per_group;
+    uint32_t *attn_tickets;  // [rows, kv_heads], cleared here, or NULL
+    int kv_heads;
 };
 
 constexpr int kIdxWidth = 256;  // d_idx in bf16 elements (512 bytes per token)
@@ -85,6 +87,8 @@ __global__ __launch_bounds__(256) void index_decode_kernel(IndexArgs a) {
     const int row = blockIdx.x / a.groups_per_row;
     const int grp = blockIdx.x - row * a.groups_per_row;
     const int b = row / a.n_q;
+    if (a.attn_tickets && grp == 0 && (int)threadIdx.x < a.kv_heads)
+        a.attn_tickets[(size_t)row * a.kv_heads + threadIdx.x] = 0u;
     const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
     const int tile_first = grp * a.tiles_per_group;
     if (tile_first * kIndexTile >= n) return;  // uniform over the workgroup
@@ -111,8 +115,10 @@ __global__ __launch_bounds__(256) void index_decode_kernel(IndexArgs a) {
 hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void *k_idx,
                                const int32_t *page_table, const int32_t *seq_lens,
                                const int32_t *q_pos, float *scores, uint32_t *coarse_hist,
-                               hipStream_t stream) {
+                               uint32_t *attn_tickets, hipStream_t stream) {
     IndexArgs a;
+    a.attn_tickets = attn_tickets;
+    a.kv_heads = g.kv_heads;
     a.q_idx = static_cast<const uint16_t *>(q_idx);
     a.k_idx = static_cast<const uint16_t *>(k_idx);
     a.page_table = page_table;

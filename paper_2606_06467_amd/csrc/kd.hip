@@ -883,7 +883,7 @@ hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_id
                        ? launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
                                               stream)
                        : launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
-                                             nullptr, stream);
+                                             nullptr, nullptr, stream);
     if (e != hipSuccess) return e;
     if (after_scores && hipEventRecord(after_scores, stream) != hipSuccess) return hipErrorUnknown;
     kd_rows_kernel<<<dim3(g.rows), dim3(256), 0, stream>>>(a);

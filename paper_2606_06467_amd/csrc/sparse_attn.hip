@@ -34,10 +34,11 @@
 //     and G heads.
 // The accumulators are then reduced over lanes and waves in LDS.  With one
 // split the workgroup writes the bf16 output and lse itself.  Otherwise it
-// writes fp32 partials (o, m, l) and attn_merge_kernel combines the splits with
-// the exact log-sum-exp rule.  The merge is a second launch rather than a
-// "last workgroup merges" ticket: the agent-scope release fence such a ticket
-// needs writes back the whole L2 of the XCD from every workgroup on this chip.
+// writes fp32 partials (o, m, l), combined by the exact log-sum-exp rule: inside
+// the kernel by the last split of each (row, KV head) to arrive (decode grids in
+// a step, see split_merge: write-through partials and a relaxed ticket, since an
+// agent-scope release fence writes back the whole L2 of the XCD from every
+// workgroup on this chip), else by attn_merge_kernel as a second launch.
 // The same kernels serve dense attention over every valid key (Eq. 1, the
 // attention that Eq. 4 restricts), used as the reference point for the cost of
 // sparse attention: token positions then come straight from the chunk, with no
@@ -80,6 +81,10 @@ struct AttnArgs {
     const int32_t *seq_lens; // dense: [batch]
     const int32_t *q_pos;    // dense, causal: [rows]
     int causal;
+    // decode grids inside a step: one arrival counter per (row, KV head), zero on
+    // entry; the last split to arrive combines the splits (no merge launch).
+    // NULL: attn_merge_kernel runs as a second launch.
+    uint32_t *tickets;
 };
 
 __host__ __device__ constexpr int pow2_at_least(int x) {
@@ -119,6 +124,82 @@ __device__ __forceinline__ float rows4_sum(float x) {
 __device__ __forceinline__ int sel_at(const int32_t *sel, int pos) {
     return *reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(sel) +
                                               (uint32_t)pos * 4u);
+}
+
+__device__ __forceinline__ uint64_t pack2f(float x, float y) {
+    return (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32);
+}
+
+// In-kernel split merge.  Every split of a (row, KV head) stores its partials
+// (o, m, l) with device-scope stores (written through the XCD's L2, so other
+// XCDs can read them without a cache write-back), waits until they are
+// complete, and takes a ticket from the unit's counter; the split that draws the
+// last ticket resets the counter and combines every split by the log-sum-exp
+// rule, reading the partials with device-scope loads (one wave per query head,
+// lane l owning dimensions 2l and 2l + 1, all loads issued before the first
+// wait).  The ticket is a relaxed atomic: ordering comes from the completed
+// write-through stores, not from an agent-scope release, whose L2 write-back
+// costs about a microsecond per workgroup.  At most kFusedMaxSplits splits.
+constexpr int kFusedMaxSplits = 8;
+
+template <int G, bool DENSE, typename Combine>
+__device__ __forceinline__ void split_merge(const AttnArgs &a, int row, int g, int split,
+                                            int nsplit, size_t base, Combine combine) {
+    __shared__ uint32_t s_ticket;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    for (int e = 2 * tid; e < G * kHeadDim; e += 512) {
+        const int h = e / kHeadDim, dim = e - h * kHeadDim;
+        float m, l, s0, s1;
+        combine(h, e, m, l, s0);
+        combine(h, e + 1, m, l, s1);
+        const size_t slot = base + (size_t)h * a.splits + split;
+        __hip_atomic_store(reinterpret_cast<uint64_t *>(a.part_o + slot * kHeadDim + dim),
+                           pack2f(s0, s1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (dim == 0)
+            __hip_atomic_store(reinterpret_cast<uint64_t *>(a.part_ml + slot * 2), pack2f(m, l),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's partials are complete
+    __syncthreads();                                   // ... and every wave's
+    uint32_t *ticket = a.tickets + (size_t)row * a.kv_heads + g;
+    if (tid == 0) s_ticket = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (s_ticket != (uint32_t)(nsplit - 1)) return;  // uniform
+    if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int Hq = a.q_heads;
+    for (int h = wave; h < G; h += 4) {
+        const size_t hb = base + (size_t)h * a.splits;
+        uint64_t o[kFusedMaxSplits], ml[kFusedMaxSplits];
+#pragma unroll
+        for (int s = 0; s < kFusedMaxSplits; ++s) {
+            const size_t slot = hb + min(s, nsplit - 1);
+            o[s] = __hip_atomic_load(reinterpret_cast<const uint64_t *>(a.part_o + slot * kHeadDim + 2 * lane),
+                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ml[s] = __hip_atomic_load(reinterpret_cast<const uint64_t *>(a.part_ml + slot * 2),
+                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        auto lo = [](uint64_t x) { return __uint_as_float((uint32_t)x); };
+        auto hi = [](uint64_t x) { return __uint_as_float((uint32_t)(x >> 32)); };
+        float M = lo(ml[0]);  // finite: split 0 holds tokens
+#pragma unroll
+        for (int s = 1; s < kFusedMaxSplits; ++s)
+            if (s < nsplit) M = fmaxf(M, lo(ml[s]));
+        float l = 0.0f, ox = 0.0f, oy = 0.0f;
+#pragma unroll
+        for (int s = 0; s < kFusedMaxSplits; ++s) {
+            if (s < nsplit) {
+                const float w = exp2f(lo(ml[s]) - M);
+                l = fmaf(w, hi(ml[s]), l);
+                ox = fmaf(w, lo(o[s]), ox);
+                oy = fmaf(w, hi(o[s]), oy);
+            }
+        }
+        const float inv = 1.0f / l;
+        const size_t rh = (size_t)row * Hq + g * G + h;
+        *reinterpret_cast<uint32_t *>(a.out + rh * kHeadDim + lane * 2) =
+            f32_to_bf16_bits(ox * inv) | (f32_to_bf16_bits(oy * inv) << 16);
+        if (a.lse && lane == 0) a.lse[rh] = (M + log2f(l)) * kLn2;
+    }
 }
 
 // MQK: matrix-core logits with per-wave softmax states; PVM (with MQK): the
@@ -491,7 +572,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             sum = red[0][e] + red[1][e] + red[2][e] + red[3][e];
         }
     };
-    if (a.splits == 1) {
+    // one split, or (with the in-kernel merge) the only split that holds tokens
+    if (a.splits == 1 || (a.tickets && nsplit == 1)) {
         for (int e = tid; e < G * kHeadDim; e += 256) {
             const int h = e / kHeadDim, dim = e - h * kHeadDim;
             float m, l, sum;
@@ -504,6 +586,10 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         return;
     }
     const size_t base = ((size_t)row * Hq + g * G) * a.splits;  // slot of (head g*G, split 0)
+    if (a.tickets) {
+        split_merge<G, DENSE>(a, row, g, split, nsplit, base, combine);
+        return;
+    }
     for (int e = tid; e < G * kHeadDim; e += 256) {
         const int h = e / kHeadDim, dim = e - h * kHeadDim;
         float m, l, sum;
@@ -680,7 +766,7 @@ static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int un
     else sparse_attn_kernel<G, false, DENSE, true, true><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
-    if (e != hipSuccess || a.splits == 1) return e;
+    if (e != hipSuccess || a.splits == 1 || a.tickets) return e;
     const dim3 mgrid(units), mblock(256), wblock(64);
     // up to 4 splits: one wave per (row, query head) (32K step layers -1.7 us,
     // 32-sequence ragged batch -6.5 us); 8 splits measured faster on the
@@ -730,6 +816,7 @@ static AttnArgs attn_args(const Geometry &g, const void *q, const void *k_cache,
     a.kv_heads = g.kv_heads;
     a.q_heads = g.q_heads;
     a.causal = g.causal;
+    a.tickets = nullptr;
     plan_splits(g, keys, dense, a.splits, a.chunks_per_split);
     a.scale_log2 = g.softmax_scale * kLog2e;
     const size_t part_o = (size_t)g.rows * g.q_heads * a.splits * kHeadDim;
@@ -741,13 +828,17 @@ static AttnArgs attn_args(const Geometry &g, const void *q, const void *k_cache,
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,
-                              float *partials, hipStream_t stream, hipEvent_t split_done) {
+                              float *partials, uint32_t *tickets, hipStream_t stream,
+                              hipEvent_t split_done) {
     AttnArgs a = attn_args(g, q, k_cache, v_cache, page_table, out, lse, partials, false);
     a.idx = idx;
     a.n_sel = n_sel;
     if (g.rows == 0) return hipSuccess;
     const size_t blocks = (size_t)g.rows * g.kv_heads * a.splits;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
+    if (tickets && a.splits > 1 && a.splits <= kFusedMaxSplits &&
+        (long)g.rows * g.kv_heads < kManyUnits)
+        a.tickets = tickets;
     const int units = g.rows * g.q_heads;  // merge workgroups: one per (row, query head)
     return launch_attn<false>(g, a, g.page_shift >= 0, dim3((unsigned)blocks), units, stream,
                               split_done);
