@@ -273,7 +273,7 @@ clsa_status clsa_index_scores(const clsa_shape *shape, const void *q_idx, const 
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (clsa::index_uses_mfma(g))
         return from_hip(clsa::launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos,
-                                                   scores, st));
+                                                   scores, nullptr, st));
     return from_hip(clsa::launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, scores,
                                               nullptr, nullptr, st));
 }
@@ -374,9 +374,9 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
     const size_t lse_stride = (size_t)g.rows * g.q_heads;
     const size_t set_stride = (size_t)g.rows * g.top_k;         // index entries per set
     const int n_sets = n_layers > 0 ? (n_layers + group - 1) / group : 1;
-    // The decode indexer clears the attention's arrival counters, so only steps
-    // that run it merge the splits inside the attention kernel.
-    uint32_t *tickets = !two_pass && !mfma ? w.tickets : nullptr;
+    // The first index launch of every set clears the attention's arrival
+    // counters, so the attention merges its splits in the kernel.
+    uint32_t *tickets = w.tickets;
     for (int s = 0; s < n_sets; ++s) {
         const uint16_t *qi = static_cast<const uint16_t *>(q_idx) + (size_t)s * q_idx_stride;
         const uint16_t *ki = static_cast<const uint16_t *>(k_idx) + (size_t)s * k_idx_stride;
@@ -386,7 +386,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
         if (two_pass) {
             if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
             CLSA_TRY(from_hip(clsa::launch_index_prefill_sample(g, qi, ki, page_table, seq_lens,
-                                                                q_pos, w.samples, st)));
+                                                                q_pos, w.samples, w.tickets, st)));
             CLSA_TRY(from_hip(clsa::launch_topk_sample_thresh(g, w.samples, seq_lens, q_pos,
                                                               w.thresh, w.slow, st)));
             CLSA_TRY(from_hip(clsa::launch_index_prefill_emit(g, qi, ki, page_table, seq_lens,
@@ -405,7 +405,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
             if (first && hook && hipEventRecord(t_hook.ev[0], st) != hipSuccess) return CLSA_ERR_HIP;
             if (mfma)
                 CLSA_TRY(from_hip(clsa::launch_index_prefill(g, qi, ki, page_table, seq_lens,
-                                                             q_pos, w.scores, st)));
+                                                             q_pos, w.scores, w.tickets, st)));
             else
                 CLSA_TRY(from_hip(clsa::launch_index_scores(g, qi, ki, page_table, seq_lens, q_pos,
                                                             w.scores, idx_hist ? w.topk.hist : nullptr,

@@ -71,10 +71,13 @@ hipError_t launch_index_scores(const Geometry &g, const void *q_idx, const void 
 // Query rows per sequence from which the indexer runs on the matrix cores.
 constexpr int kPrefillMinRows = 32;
 bool index_uses_mfma(const Geometry &g);
-// Scores only (no coarse histogram).
+// Scores only (no coarse histogram).  attn_tickets: [rows, kv_heads] counters
+// of the attention that follows, set to zero by this launch, or NULL (also for
+// the sampled pass below).
 hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void *k_idx,
                                 const int32_t *page_table, const int32_t *seq_lens,
-                                const int32_t *q_pos, float *scores, hipStream_t stream);
+                                const int32_t *q_pos, float *scores, uint32_t *attn_tickets,
+                                hipStream_t stream);
 
 // ---- two-pass chunked-prefill top-k (index_prefill.hip, topk.hip) ----
 // Every kTopkSampleStride-th key of each row is scored first; the threshold of
@@ -95,7 +98,8 @@ int topk_sample_rank(const Geometry &g);
 // Pass 1: sampled scores [rows, topk_sample_cols(g)].
 hipError_t launch_index_prefill_sample(const Geometry &g, const void *q_idx, const void *k_idx,
                                        const int32_t *page_table, const int32_t *seq_lens,
-                                       const int32_t *q_pos, float *samples, hipStream_t stream);
+                                       const int32_t *q_pos, float *samples, uint32_t *attn_tickets,
+                                       hipStream_t stream);
 // Per-row thresholds (order-preserving keys) from the samples; also clears the
 // count of the slow list (slow: [1 + rows]) that the selection fills.
 hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
@@ -143,8 +147,8 @@ size_t attn_partial_floats(const Geometry &g, bool dense = false);
 // Attention gathering K/V rows from the cache through idx (and the page table).
 // split_done, if not null, is recorded right after the attention kernel, before
 // the split merge.  tickets: [rows, kv_heads] arrival counters, zero on entry and
-// zero again on return, or NULL; with them, decode grids of at most
-// kFusedMaxSplits splits merge the splits inside the attention kernel.
+// zero again on return, or NULL; with them, grids of at most kFusedMaxSplits
+// splits per (row, KV head) merge the splits inside the attention kernel.
 hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_cache,
                               const void *v_cache, const int32_t *page_table,
                               const int32_t *idx, const int32_t *n_sel, void *out, float *lse,

@@ -49,6 +49,8 @@ struct PrefillArgs {
     int key_stride;   // 1, or S: a block's keys are positions 0, S, 2S, ... (the sample pass)
     int row_stride;   // floats per score row
     int qsplit;       // query-tile ranges per sequence (workgroups per key block)
+    uint32_t *attn_tickets;  // arrival counters of the attention that follows, cleared here, or NULL
+    int n_tickets;
 };
 
 __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t *p) {
@@ -198,6 +200,9 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int qs = blockIdx.x - b * per_seq - kblk * a.qsplit;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int col = lane & 15, grp = lane >> 4;
+    if (a.attn_tickets)
+        for (int x = blockIdx.x * 256 + threadIdx.x; x < a.n_tickets; x += gridDim.x * 256)
+            a.attn_tickets[x] = 0u;
     const int stride = a.key_stride;
     const int len_pos = clamp_len(a.seq_lens[b], a.max_len);  // positions
     const int len = strided_limit(len_pos, stride);           // keys (of this pass)
@@ -399,6 +404,8 @@ static PrefillArgs prefill_args(const Geometry &g, const void *q_idx, const void
     a.causal = g.causal;
     a.key_stride = 1;
     a.qsplit = 1;
+    a.attn_tickets = nullptr;
+    a.n_tickets = g.rows * g.kv_heads;
     return a;
 }
 
@@ -418,8 +425,10 @@ static hipError_t launch_prefill(const Geometry &g, const PrefillArgs &a, hipStr
 
 hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void *k_idx,
                                 const int32_t *page_table, const int32_t *seq_lens,
-                                const int32_t *q_pos, float *scores, hipStream_t stream) {
+                                const int32_t *q_pos, float *scores, uint32_t *attn_tickets,
+                                hipStream_t stream) {
     PrefillArgs a = prefill_args(g, q_idx, k_idx, page_table, seq_lens, q_pos);
+    a.attn_tickets = attn_tickets;
     a.scores = scores;
     a.row_stride = g.max_len;
     a.kblocks = div_up(g.max_len, kPfKeys);
@@ -438,8 +447,10 @@ static int prefill_qsplit(const Geometry &g, int kblocks) {
 
 hipError_t launch_index_prefill_sample(const Geometry &g, const void *q_idx, const void *k_idx,
                                        const int32_t *page_table, const int32_t *seq_lens,
-                                       const int32_t *q_pos, float *samples, hipStream_t stream) {
+                                       const int32_t *q_pos, float *samples, uint32_t *attn_tickets,
+                                       hipStream_t stream) {
     PrefillArgs a = prefill_args(g, q_idx, k_idx, page_table, seq_lens, q_pos);
+    a.attn_tickets = attn_tickets;
     a.scores = samples;
     a.key_stride = kTopkSampleStride;
     a.row_stride = topk_sample_cols(g);

@@ -881,7 +881,7 @@ hipError_t launch_kd_loss(const Geometry &g, const float *abar, const void *q_id
     // The scores of Eq. 3 for every valid (row, key), then the row terms in place.
     hipError_t e = index_uses_mfma(g)
                        ? launch_index_prefill(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
-                                              stream)
+                                              nullptr, stream)
                        : launch_index_scores(g, q_idx, k_idx, page_table, seq_lens, q_pos, a.dI,
                                              nullptr, nullptr, stream);
     if (e != hipSuccess) return e;

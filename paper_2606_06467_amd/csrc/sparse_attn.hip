@@ -35,10 +35,11 @@
 // The accumulators are then reduced over lanes and waves in LDS.  With one
 // split the workgroup writes the bf16 output and lse itself.  Otherwise it
 // writes fp32 partials (o, m, l), combined by the exact log-sum-exp rule: inside
-// the kernel by the last split of each (row, KV head) to arrive (decode grids in
-// a step, see split_merge: write-through partials and a relaxed ticket, since an
-// agent-scope release fence writes back the whole L2 of the XCD from every
-// workgroup on this chip), else by attn_merge_kernel as a second launch.
+// the kernel by the last split of each (row, KV head) to arrive (inside
+// clsa_decode_step, whose first index launch clears the arrival counters; see
+// split_merge: write-through partials and a relaxed ticket, since an agent-scope
+// release fence writes back the whole L2 of the XCD from every workgroup on this
+// chip), else by attn_merge_kernel as a second launch.
 // The same kernels serve dense attention over every valid key (Eq. 1, the
 // attention that Eq. 4 restricts), used as the reference point for the cost of
 // sparse attention: token positions then come straight from the chunk, with no
@@ -81,8 +82,8 @@ struct AttnArgs {
     const int32_t *seq_lens; // dense: [batch]
     const int32_t *q_pos;    // dense, causal: [rows]
     int causal;
-    // decode grids inside a step: one arrival counter per (row, KV head), zero on
-    // entry; the last split to arrive combines the splits (no merge launch).
+    // inside a step: one arrival counter per (row, KV head), zero on entry; the
+    // last split to arrive combines the splits (no merge launch).
     // NULL: attn_merge_kernel runs as a second launch.
     uint32_t *tickets;
 };
@@ -836,9 +837,7 @@ hipError_t launch_sparse_attn(const Geometry &g, const void *q, const void *k_ca
     if (g.rows == 0) return hipSuccess;
     const size_t blocks = (size_t)g.rows * g.kv_heads * a.splits;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
-    if (tickets && a.splits > 1 && a.splits <= kFusedMaxSplits &&
-        (long)g.rows * g.kv_heads < kManyUnits)
-        a.tickets = tickets;
+    if (tickets && a.splits > 1 && a.splits <= kFusedMaxSplits) a.tickets = tickets;
     const int units = g.rows * g.q_heads;  // merge workgroups: one per (row, query head)
     return launch_attn<false>(g, a, g.page_shift >= 0, dim3((unsigned)blocks), units, stream,
                               split_done);
