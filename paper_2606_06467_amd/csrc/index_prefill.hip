@@ -20,6 +20,8 @@
 // staged in LDS and written as whole 1 KiB row segments (direct 16-byte stores
 // of 64-byte row pieces reached only about 3 TB/s), one tile later, after the
 // next wait, so that waiting for loads never waits for fresh stores.
+#include <type_traits>
+
 #include "clsa_internal.h"
 #include "device_common.h"
 
@@ -40,9 +42,9 @@ struct PrefillArgs {
     const int32_t *seq_lens;
     const int32_t *q_pos;
     float *scores;            // scores: [rows, row_stride]
-    const uint32_t *thresh;   // EMIT: [rows] candidate threshold (order-preserving key)
-    uint32_t *cand_count;     // EMIT: [rows, kblocks] candidates per key block (may exceed the slots)
-    uint2 *cands;             // EMIT: [rows, kblocks, kTopkBlockSlots] (key, position)
+    const uint32_t *thresh;   // candidate pass: [rows] candidate threshold (order-preserving key)
+    uint32_t *cand_count;     // candidate pass: [rows, kblocks] candidates per key block (may exceed the slots)
+    uint2 *cands;             // candidate pass: [rows, kblocks, kTopkBlockSlots] (key, position)
     int n_q, max_len, page_shift, max_pages, causal;
     int kblocks;      // key blocks per sequence (of sampled keys when key_stride > 1)
     int vec_store;    // row_stride % 4 == 0: rows are 16-byte aligned
@@ -187,12 +189,11 @@ __device__ __forceinline__ void score_regs(const bf16x8 (&kv)[4][8], const bf16x
 // before it; issuing a tile's stores only after the next tile's queries have
 // arrived keeps the stores' completion out of the wait.  Tiles whose rows all
 // end before the workgroup's first key (causal) compute and store nothing.
-// EMIT (the second pass of the chunked-prefill top-k): instead of storing the
-// scores, append each row's candidates (scores at or above its threshold) to
-// its list.  With key_stride S > 1 (the first pass) the block's keys are every
-// S-th position and the scores go to a [rows, row_stride] sample matrix.
-// Workgroups of one key block split the query tiles into qsplit ranges.
-template <bool PAGED, bool CAUSAL, bool EMIT>
+// With key_stride S > 1 (the first pass of the chunked-prefill top-k) the
+// block's keys are every S-th position and the scores go to a [rows,
+// row_stride] sample matrix.  Workgroups of one key block split the query
+// tiles into qsplit ranges.
+template <bool PAGED, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int per_seq = a.kblocks * a.qsplit;
     const int b = blockIdx.x / per_seq;
@@ -209,13 +210,8 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     const int jg = kblk * kPfKeys;                       // first key of this workgroup
     const int jw = jg + wave * kPfWaveKeys;              // first key of this wave
     if (jg >= len) return;                               // uniform over the workgroup
-    __shared__ float tile[EMIT ? 1 : 2][EMIT ? 1 : 16][kTileStride];
+    __shared__ float tile[2][16][kTileStride];
     __shared__ __align__(16) uint16_t s_q[2][16][kQStride];  // query tiles (bf16)
-    // EMIT: candidates per (query, wave, lane group) of a tile, two tiles in turn
-    __shared__ __align__(16) uint32_t s_cnt[EMIT ? 2 : 1][16][16];
-    // EMIT: each lane's 16 scores of the last tile (fp32 bits), [wave][key slot]
-    // [lane] (a lane reads back only its own, at any slot: no bank conflicts)
-    __shared__ uint32_t s_ek[EMIT ? 4 : 1][EMIT ? 16 : 1][64];
 
     // the wave's 64 keys as A operands: key tile kt, row col = key jw + 16*kt + col
     bf16x8 kv[4][8];
@@ -254,12 +250,7 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
         *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col]) = qs_v[0];
         *reinterpret_cast<u32x4 *>(&s_q[buf][sq_row][sq_col + 8]) = qs_v[1];
     };
-    // row thresholds (EMIT), a tile ahead like the key limits
-    auto load_thresh = [&](int qt) -> uint32_t {
-        return EMIT ? a.thresh[(size_t)b * a.n_q + min(qt * 16 + col, a.n_q - 1)] : 0u;
-    };
     int p_cur = key_pos<CAUSAL>(qpos, a.n_q, qt0 * 16 + col);  // raw positions, a tile ahead
-    uint32_t th_cur = load_thresh(qt0);
     load_quarter(qt0);
     __builtin_amdgcn_s_waitcnt(kPfWaitVm0);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -267,24 +258,138 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
     if (qt0 + 1 < qt_end) load_quarter(qt0 + 1);
     pf_lds_barrier();
     int n_prev = 0;       // key limits of the tile staged in LDS, not yet stored
-    uint32_t th_prev = 0;
     bool staged = false;
-    // EMIT (the second pass of the chunked-prefill top-k): a key is a candidate
-    // when it is valid for its query and its order-preserving score key is at
-    // least the query's threshold.  The tile's scores stay in registers; each
-    // lane counts its candidates into s_cnt, and after the tile's barrier (in
-    // the next iteration, after its wait, so that no wait covers these stores)
-    // it takes its slots of the (query, key block) list: those of the lanes
-    // before it in (wave, lane group) order.  Each (query, key block) list is
-    // written by this workgroup alone, so no atomics are needed; its count is
-    // written in full (a count past the slots sends the row to the exact
-    // fallback of the top-k).
-    f32x4 e_c[4];
-    uint32_t e_mask = 0u;
-    int e_qt = -1;
-    auto emit_store = [&]() {
-        if (!EMIT || e_qt < 0) return;
-        const uint32_t *cs = &s_cnt[e_qt & 1][col][0];
+    for (int qt = qt0; qt < qt_end; ++qt) {
+        int p_next = 0;
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(kPfWaitVm0);                         // (a)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_sched_barrier(0);
+        const int n_cur = strided_limit(key_limit<CAUSAL>(p_cur, len_pos, a.n_q, qt * 16 + col), stride);
+        if (qt + 1 < qt_end) stage_quarter((qt + 1) & 1);               // tile qt+1's queries
+        if (staged)                                                     // (b)
+            store_tile(a, tile[(qt - 1) & 1], n_prev, b, qt - 1, jg, wave, lane);
+        if (qt + 1 < qt_end) {                                          // (c)
+            p_next = key_pos<CAUSAL>(qpos, a.n_q, (qt + 1) * 16 + col);
+        }
+        if (qt + 2 < qt_end) load_quarter(qt + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        staged = tile_limit(n_cur) > jg;                                // uniform
+        if (staged) {                                                   // (d)
+            bf16x8 qv[8];
+#pragma unroll
+            for (int kb = 0; kb < 8; ++kb)
+                qv[kb] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4 *>(&s_q[qt & 1][col][kb * 32 + grp * 8]));
+            score_tile(kv, qv, wave, lane, tile[qt & 1]);
+        }
+        n_prev = n_cur;
+        p_cur = p_next;
+        pf_lds_barrier();                                               // (e)
+    }
+    if (staged) store_tile(a, tile[(qt_end - 1) & 1], n_prev, b, qt_end - 1, jg, wave, lane);
+}
+
+// The candidate pass (the second pass of the chunked-prefill top-k): the
+// products of index_prefill_kernel, but instead of storing the scores each
+// row's candidates (valid keys whose score is at least the row's threshold)
+// go to its (row, key block) list.  Each lane decides its 16 keys of a tile in
+// fp32 against the threshold turned back into a float, counts them into s_cnt,
+// and after the tile's barrier takes its slots of the list: those of the
+// (wave, lane group)s before it.  Each (row, key block) list is written by this
+// workgroup alone, so no atomics are needed; its count is written in full (a
+// count past the slots sends the row to the exact fallback of the top-k).  Two
+// query tiles per step: the wait, the barrier and the candidate stores of a
+// step cover 32 queries (one tile per step measured 4% slower).  Per step P (tiles qt, qt + 1): (a) wait
+// for every global access so far (pair P + 1's queries, loaded a step ahead,
+// and the candidate stores of step P - 2); stage pair P + 1's queries in LDS;
+// (b) store pair P - 1's candidates; (c) load pair P + 1's key limits and
+// thresholds and pair P + 2's queries; (d) products and candidate masks of
+// pair P; (e) LDS-only barrier.  The scores of a pair wait in LDS (each lane
+// reads back only its own) until its candidates are stored a step later
+// (picking them out of the registers by a select chain on the slot number
+// measured slower).
+template <bool PAGED, bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void index_emit_kernel(PrefillArgs a) {
+    const int per_seq = a.kblocks * a.qsplit;
+    const int b = blockIdx.x / per_seq;
+    const int kblk = (blockIdx.x - b * per_seq) / a.qsplit;
+    const int qs = blockIdx.x - b * per_seq - kblk * a.qsplit;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int col = lane & 15, grp = lane >> 4;
+    if (a.attn_tickets)
+        for (int x = blockIdx.x * 256 + threadIdx.x; x < a.n_tickets; x += gridDim.x * 256)
+            a.attn_tickets[x] = 0u;
+    const int len = clamp_len(a.seq_lens[b], a.max_len);
+    const int jg = kblk * kPfKeys;
+    const int jw = jg + wave * kPfWaveKeys;
+    if (jg >= len) return;  // uniform
+    __shared__ __align__(16) uint16_t s_q[2][2][16][kQStride];  // [stage][tile of the pair]
+    __shared__ __align__(16) uint32_t s_cnt[2][2][16][16];      // [step parity][tile][query][wave, lane group]
+    __shared__ uint32_t s_ek[2][4][16][64];                      // [tile][wave][key slot][lane]
+
+    bf16x8 kv[4][8];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+        const int j = min(jw + 16 * kt + col, len - 1);  // clamped keys are never candidates
+        size_t off;
+        if (PAGED) {
+            const int page = a.page_table[(size_t)b * a.max_pages + (j >> a.page_shift)];
+            off = (((size_t)page << a.page_shift) + (j & ((1 << a.page_shift) - 1))) * kIdxDim;
+        } else {
+            off = ((size_t)b * a.max_len + j) * kIdxDim;
+        }
+#pragma unroll
+        for (int kb = 0; kb < 8; ++kb) kv[kt][kb] = load_bf16x8(a.k_idx + off + grp * 8 + kb * 32);
+    }
+
+    const int ntiles_all = div_up(a.n_q, 16);
+    const int tpw = div_up(ntiles_all, a.qsplit);
+    const int qt0 = qs * tpw;
+    const int qt_end = min(ntiles_all, qt0 + tpw);
+    if (qt0 >= qt_end) return;  // uniform
+    const int32_t *qpos = CAUSAL ? a.q_pos + (size_t)b * a.n_q : nullptr;
+    const int sq_row = wave * 4 + (lane >> 4), sq_col = (lane & 15) * 16;
+    u32x4 qs_v[2][2];
+    auto load_pair = [&](int qt) {  // wave w: queries 4w .. 4w+3 of tiles qt and qt + 1
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int r = min((qt + t) * 16 + sq_row, a.n_q - 1);  // past the end: never used
+            const uint16_t *p = a.q_idx + ((size_t)b * a.n_q + r) * kIdxDim + sq_col;
+            qs_v[t][0] = *reinterpret_cast<const u32x4 *>(p);
+            qs_v[t][1] = *reinterpret_cast<const u32x4 *>(p + 8);
+        }
+    };
+    auto stage_pair = [&](int st) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            *reinterpret_cast<u32x4 *>(&s_q[st][t][sq_row][sq_col]) = qs_v[t][0];
+            *reinterpret_cast<u32x4 *>(&s_q[st][t][sq_row][sq_col + 8]) = qs_v[t][1];
+        }
+    };
+    auto row_of = [&](int qt, int t) { return min((qt + t) * 16 + col, a.n_q - 1); };
+    int p_cur[2], p_next[2] = {0, 0};
+    uint32_t th_cur[2], th_next[2] = {0u, 0u};
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        p_cur[t] = key_pos<CAUSAL>(qpos, a.n_q, qt0 * 16 + 16 * t + col);
+        th_cur[t] = a.thresh[(size_t)b * a.n_q + row_of(qt0, t)];
+    }
+    load_pair(qt0);
+    __builtin_amdgcn_s_waitcnt(kPfWaitVm0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    stage_pair(0);
+    if (qt0 + 2 < qt_end) load_pair(qt0 + 2);
+    pf_lds_barrier();
+
+    f32x4 e_c[2][4];
+    uint32_t e_mask[2] = {0u, 0u};
+    int e_qt[2] = {-1, -1};  // tiles whose candidates are still to be stored
+    int e_par = 0;           // their step's parity (s_cnt buffer)
+    auto emit_store = [&](auto tile) {  // tile: std::integral_constant (keeps e_c indices static)
+        constexpr int t = decltype(tile)::value;
+        if (e_qt[t] < 0) return;
+        const uint32_t *cs = &s_cnt[e_par][t][col][0];
         const u32x4 c0 = *reinterpret_cast<const u32x4 *>(cs);
         const u32x4 c1 = *reinterpret_cast<const u32x4 *>(cs + 4);
         const u32x4 c2 = *reinterpret_cast<const u32x4 *>(cs + 8);
@@ -298,92 +403,87 @@ __global__ __launch_bounds__(256, 2) void index_prefill_kernel(PrefillArgs a) {
             before += i < me ? cnt[i] : 0u;
             total += cnt[i];
         }
-        const int t = e_qt * 16 + col;
-        if (t < a.n_q) {
-            const size_t blk = (size_t)(b * a.n_q + t) * a.kblocks + kblk;
+        const int r = e_qt[t] * 16 + col;
+        if (r < a.n_q) {
+            const size_t blk = (size_t)(b * a.n_q + r) * a.kblocks + kblk;
             uint2 *dst = a.cands + blk * kTopkBlockSlots;
-            // one store per candidate of the lane, in slot order: the wave
-            // issues as many stores as its busiest lane has candidates (about
-            // one), not one per key slot
-            uint32_t slot = before, m = e_mask;
+            uint32_t slot = before, m = e_mask[t];
             while (m) {
                 const int j = __builtin_ctz(m);
                 m &= m - 1u;
                 if (slot < (uint32_t)kTopkBlockSlots)
-                    dst[slot] = make_uint2(score_key(__uint_as_float(s_ek[wave][j][lane])),
+                    dst[slot] = make_uint2(score_key(__uint_as_float(s_ek[t][wave][j][lane])),
                                            (uint32_t)(jw + 16 * (j >> 2) + 4 * grp + (j & 3)));
                 ++slot;
             }
             if (me == 0) a.cand_count[blk] = total;
         }
-        e_qt = -1;
+        e_qt[t] = -1;
     };
-    for (int qt = qt0; qt < qt_end; ++qt) {
-        int p_next = 0;
-        uint32_t th_next = 0;
+    for (int qt = qt0, par = 0; qt < qt_end; qt += 2, par ^= 1) {
         __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(kPfWaitVm0);                         // (a)
+        __builtin_amdgcn_s_waitcnt(kPfWaitVm0);                          // (a)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_sched_barrier(0);
-        const int n_cur = strided_limit(key_limit<CAUSAL>(p_cur, len_pos, a.n_q, qt * 16 + col), stride);
-        if (qt + 1 < qt_end) stage_quarter((qt + 1) & 1);               // tile qt+1's queries
-        if (EMIT) {                                                     // (b)
-            emit_store();
-        } else if (staged) {
-            store_tile(a, tile[(qt - 1) & 1], n_prev, b, qt - 1, jg, wave, lane);
+        int n_cur[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+            n_cur[t] = qt + t < qt_end ? key_limit<CAUSAL>(p_cur[t], len, a.n_q, (qt + t) * 16 + col) : 0;
+        if (qt + 2 < qt_end) stage_pair(par ^ 1);                        // pair P + 1's queries
+        emit_store(std::integral_constant<int, 0>{});                     // (b)
+        emit_store(std::integral_constant<int, 1>{});
+        if (qt + 2 < qt_end) {                                           // (c)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                p_next[t] = key_pos<CAUSAL>(qpos, a.n_q, (qt + 2 + t) * 16 + col);
+                th_next[t] = a.thresh[(size_t)b * a.n_q + row_of(qt + 2, t)];
+            }
         }
-        if (qt + 1 < qt_end) {                                          // (c)
-            p_next = key_pos<CAUSAL>(qpos, a.n_q, (qt + 1) * 16 + col);
-            th_next = load_thresh(qt + 1);
-        }
-        if (qt + 2 < qt_end) load_quarter(qt + 2);
+        if (qt + 4 < qt_end) load_pair(qt + 4);
         __builtin_amdgcn_sched_barrier(0);
-        staged = tile_limit(n_cur) > jg;                                // uniform
-        if (staged) {                                                   // (d)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {                                    // (d)
+            if (tile_limit(n_cur[t]) <= jg) continue;  // uniform: no query of the tile sees this block
             bf16x8 qv[8];
 #pragma unroll
             for (int kb = 0; kb < 8; ++kb)
                 qv[kb] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4 *>(&s_q[qt & 1][col][kb * 32 + grp * 8]));
-            if (EMIT) {
-                score_regs(kv, qv, e_c);
-                // candidates decided in fp32 against the row's threshold; the
-                // per-key causal test only on tiles where some query of the
-                // tile does not see all of this wave's keys (uniform)
-                const float thf = thresh_float(th_cur);
-                e_mask = 0u;
-                if (tile_limit_min(n_cur) >= jw + kPfWaveKeys) {
+                    bf16x8, *reinterpret_cast<const u32x4 *>(&s_q[par][t][col][kb * 32 + grp * 8]));
+            score_regs(kv, qv, e_c[t]);
+            const float thf = thresh_float(th_cur[t]);
+            uint32_t m = 0u;
+            if (tile_limit_min(n_cur[t]) >= jw + kPfWaveKeys) {
 #pragma unroll
-                    for (int kt = 0; kt < 4; ++kt)
+                for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            e_mask |= (e_c[kt][r] >= thf ? 1u : 0u) << (4 * kt + r);
-                            s_ek[wave][4 * kt + r][lane] = __float_as_uint(e_c[kt][r]);
-                        }
-                } else {
-#pragma unroll
-                    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const bool cand = jw + 16 * kt + 4 * grp + r < n_cur && e_c[kt][r] >= thf;
-                            e_mask |= (cand ? 1u : 0u) << (4 * kt + r);
-                            s_ek[wave][4 * kt + r][lane] = __float_as_uint(e_c[kt][r]);
-                        }
-                }
-                s_cnt[qt & 1][col][wave * 4 + grp] = (uint32_t)__popc(e_mask);
-                e_qt = qt;
+                    for (int r = 0; r < 4; ++r) {
+                        m |= (e_c[t][kt][r] >= thf ? 1u : 0u) << (4 * kt + r);
+                        s_ek[t][wave][4 * kt + r][lane] = __float_as_uint(e_c[t][kt][r]);
+                    }
             } else {
-                score_tile(kv, qv, wave, lane, tile[qt & 1]);
+#pragma unroll
+                for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const bool cand = jw + 16 * kt + 4 * grp + r < n_cur[t] && e_c[t][kt][r] >= thf;
+                        m |= (cand ? 1u : 0u) << (4 * kt + r);
+                        s_ek[t][wave][4 * kt + r][lane] = __float_as_uint(e_c[t][kt][r]);
+                    }
             }
+            e_mask[t] = m;
+            s_cnt[par][t][col][wave * 4 + grp] = (uint32_t)__popc(m);
+            e_qt[t] = qt + t;
         }
-        n_prev = n_cur;
-        th_prev = th_cur;
-        p_cur = p_next;
-        th_cur = th_next;
-        pf_lds_barrier();                                               // (e)
+        e_par = par;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            p_cur[t] = p_next[t];
+            th_cur[t] = th_next[t];
+        }
+        pf_lds_barrier();                                                // (e)
     }
-    if (EMIT) emit_store();
-    else if (staged) store_tile(a, tile[(qt_end - 1) & 1], n_prev, b, qt_end - 1, jg, wave, lane);
+    emit_store(std::integral_constant<int, 0>{});
+    emit_store(std::integral_constant<int, 1>{});
 }
 
 bool index_uses_mfma(const Geometry &g) { return g.n_q >= kPrefillMinRows; }
@@ -409,17 +509,16 @@ static PrefillArgs prefill_args(const Geometry &g, const void *q_idx, const void
     return a;
 }
 
-template <bool EMIT>
 static hipError_t launch_prefill(const Geometry &g, const PrefillArgs &a, hipStream_t stream) {
     const size_t blocks = (size_t)g.batch * a.kblocks * a.qsplit;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
     const dim3 grid((unsigned)blocks), block(256);
     const bool paged = g.page_shift >= 0;
-    if (paged && g.causal) index_prefill_kernel<true, true, EMIT><<<grid, block, 0, stream>>>(a);
-    else if (paged) index_prefill_kernel<true, false, EMIT><<<grid, block, 0, stream>>>(a);
-    else if (g.causal) index_prefill_kernel<false, true, EMIT><<<grid, block, 0, stream>>>(a);
-    else index_prefill_kernel<false, false, EMIT><<<grid, block, 0, stream>>>(a);
+    if (paged && g.causal) index_prefill_kernel<true, true><<<grid, block, 0, stream>>>(a);
+    else if (paged) index_prefill_kernel<true, false><<<grid, block, 0, stream>>>(a);
+    else if (g.causal) index_prefill_kernel<false, true><<<grid, block, 0, stream>>>(a);
+    else index_prefill_kernel<false, false><<<grid, block, 0, stream>>>(a);
     return hipGetLastError();
 }
 
@@ -433,7 +532,7 @@ hipError_t launch_index_prefill(const Geometry &g, const void *q_idx, const void
     a.row_stride = g.max_len;
     a.kblocks = div_up(g.max_len, kPfKeys);
     a.vec_store = (g.max_len % 4) == 0;
-    return launch_prefill<false>(g, a, stream);
+    return launch_prefill(g, a, stream);
 }
 
 // Enough workgroups for the chip when a pass has few key blocks: split the
@@ -457,7 +556,7 @@ hipError_t launch_index_prefill_sample(const Geometry &g, const void *q_idx, con
     a.kblocks = div_up(a.row_stride, kPfKeys);
     a.vec_store = (a.row_stride % 4) == 0;
     a.qsplit = prefill_qsplit(g, a.kblocks);
-    return launch_prefill<false>(g, a, stream);
+    return launch_prefill(g, a, stream);
 }
 
 hipError_t launch_index_prefill_emit(const Geometry &g, const void *q_idx, const void *k_idx,
@@ -471,7 +570,16 @@ hipError_t launch_index_prefill_emit(const Geometry &g, const void *q_idx, const
     a.row_stride = g.max_len;
     a.kblocks = div_up(g.max_len, kPfKeys);
     a.qsplit = prefill_qsplit(g, a.kblocks);
-    return launch_prefill<true>(g, a, stream);
+    const size_t blocks = (size_t)g.batch * a.kblocks * a.qsplit;
+    if (blocks == 0) return hipSuccess;
+    if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
+    const dim3 grid((unsigned)blocks), block(256);
+    const bool paged = g.page_shift >= 0;
+    if (paged && g.causal) index_emit_kernel<true, true><<<grid, block, 0, stream>>>(a);
+    else if (paged) index_emit_kernel<true, false><<<grid, block, 0, stream>>>(a);
+    else if (g.causal) index_emit_kernel<false, true><<<grid, block, 0, stream>>>(a);
+    else index_emit_kernel<false, false><<<grid, block, 0, stream>>>(a);
+    return hipGetLastError();
 }
 
 hipError_t take_device_error_index_prefill(uint32_t *bits) { return take_source_device_error(bits); }
