@@ -81,6 +81,7 @@ KERNEL_SOURCES = {
     "sparse_attn_kernel": ["sparse_attn.hip", "device_common.h", "clsa_internal.h"],
     "index_decode_kernel": ["index_decode.hip", "device_common.h", "clsa_internal.h"],
     "index_prefill_kernel": ["index_prefill.hip", "device_common.h", "clsa_internal.h"],
+    "index_emit_kernel": ["index_prefill.hip", "device_common.h", "clsa_internal.h"],
 }
 
 
@@ -737,7 +738,10 @@ def main() -> int:
         # the caches, so it is priced by its matrix FLOPs
         "roofline": (roofline_mfma("sparse_attn_kernel", w, ab["attn_flops"], attn_ms)
                      if prefill else roofline("sparse_attn_kernel", w, ab["attn"], attn_ms)),
-        "roofline_index": (roofline_mfma("index_prefill_kernel", w, ab["index_flops"], index_ms)
+        # chunked prefill: the index phase (sampled pass, threshold, candidate
+        # pass) priced by the causal block's FLOPs; its traffic record is the
+        # candidate pass's, the phase's largest kernel
+        "roofline_index": (roofline_mfma("index_emit_kernel", w, ab["index_flops"], index_ms)
                            if w.n_q >= PREFILL_MIN_ROWS else
                            roofline("index_decode_kernel", w, ab["index"], index_ms)),
     }
