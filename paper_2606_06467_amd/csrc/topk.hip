@@ -730,15 +730,22 @@ static_assert(kMaxLen / kTopkKeyBlock <= 2 * kCandThreads, "at most two key bloc
 static_assert(kTopkKeyBlock == 8 * 32, "a block's positions are 8 bitmap words");
 
 template <int BPT>  // key blocks per thread
-__global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a) {
+// one key block per thread: at most 80 registers, so that three workgroups
+// (six waves per SIMD) fit a CU beside their LDS
+__global__ __launch_bounds__(kCandThreads) __attribute__((amdgpu_waves_per_eu(BPT == 1 ? 6 : 1)))
+void topk_cand_fast_kernel(CandArgs a) {
     constexpr int NT = kCandThreads;
     constexpr int NW = NT / 64;
     constexpr int NWD = 8 * BPT;  // bitmap words per thread
     constexpr int kFirst = 24;    // entries of a block loaded in the first batch (about 8 expected)
-    extern __shared__ __align__(16) uint32_t lds[];  // [kCandCap] keys, then [kCandCap] positions
+    // [kCandCap] keys, then [kCandCap] 16-bit positions relative to the first
+    // key of the owning thread's blocks (48 KiB: three workgroups per CU)
+    extern __shared__ __align__(16) uint32_t lds[];
     __shared__ ShortSelectLds<NT> sm;
     __shared__ uint32_t s_andor[2][NW];
-    uint32_t *s_key = lds, *s_pos = lds + kCandCap;
+    uint32_t *s_key = lds;
+    uint16_t *s_pos = reinterpret_cast<uint16_t *>(lds + kCandCap);
+    static_assert(BPT * kTopkKeyBlock <= 65536, "relative positions fit 16 bits");
 
     const int row = blockIdx.x, b = row / a.n_q, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -751,24 +758,26 @@ __global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a
         return;
     }
     const int nblk = div_up(n, kTopkKeyBlock);
-    // block counts, then at once the first kFirst entries of each of this
-    // thread's blocks (before the workgroup prefix that places them)
-    uint32_t kept[BPT], mine = 0u, lost_mine = 0u;
-#pragma unroll
-    for (int u = 0; u < BPT; ++u) {
-        const int kb = BPT * tid + u;
-        const uint32_t cb = kb < nblk ? a.cand_count[(size_t)row * a.kblocks + kb] : 0u;
-        kept[u] = min(cb, (uint32_t)kTopkBlockSlots);
-        mine += kept[u];
-        lost_mine += cb - kept[u];
-    }
+    // block counts and the first kFirst entries of each of this thread's
+    // blocks in one batch (the slots exist whatever the count: entries past it
+    // are read and never used), before the workgroup prefix that places them
+    uint32_t cbr[BPT];
     uint2 e[BPT][kFirst];
 #pragma unroll
     for (int u = 0; u < BPT; ++u) {
-        const uint2 *src = a.cands + ((size_t)row * a.kblocks + BPT * tid + u) * kTopkBlockSlots;
+        const int kb = min(BPT * tid + u, a.kblocks - 1);
+        cbr[u] = a.cand_count[(size_t)row * a.kblocks + kb];
+        const uint2 *src = a.cands + ((size_t)row * a.kblocks + kb) * kTopkBlockSlots;
 #pragma unroll
-        for (int v = 0; v < kFirst; ++v)
-            if ((uint32_t)v < kept[u]) e[u][v] = src[v];
+        for (int v = 0; v < kFirst; ++v) e[u][v] = src[v];
+    }
+    uint32_t kept[BPT], mine = 0u, lost_mine = 0u;
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) {
+        const uint32_t cb = BPT * tid + u < nblk ? cbr[u] : 0u;
+        kept[u] = min(cb, (uint32_t)kTopkBlockSlots);
+        mine += kept[u];
+        lost_mine += cb - kept[u];
     }
     uint32_t before, unused0, cnt, lost;
     block_excl_scan2<NT>(mine, lost_mine, sm.wave, before, unused0, cnt, lost);
@@ -776,6 +785,7 @@ __global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a
         if (tid == 0) a.slow[1 + atomicAdd(&a.slow[0], 1u)] = (uint32_t)row;
         return;
     }
+    const uint32_t p_first = (uint32_t)tid * BPT * kTopkKeyBlock;  // first key of this thread's blocks
     {
         uint32_t at = before;
 #pragma unroll
@@ -784,7 +794,7 @@ __global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a
             for (int v = 0; v < kFirst; ++v)
                 if ((uint32_t)v < kept[u]) {
                     s_key[at + v] = e[u][v].x;
-                    s_pos[at + v] = e[u][v].y;
+                    s_pos[at + v] = (uint16_t)(e[u][v].y - p_first);
                 }
             const uint2 *src = a.cands + ((size_t)row * a.kblocks + BPT * tid + u) * kTopkBlockSlots;
             for (uint32_t q0 = kFirst; q0 < kept[u]; q0 += 8) {  // rare: more than kFirst candidates
@@ -796,7 +806,7 @@ __global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a
                 for (int v = 0; v < 8; ++v)
                     if (q0 + v < kept[u]) {
                         s_key[at + q0 + v] = x[v].x;
-                        s_pos[at + q0 + v] = x[v].y;
+                        s_pos[at + q0 + v] = (uint16_t)(x[v].y - p_first);
                     }
             }
             at += kept[u];
@@ -845,13 +855,12 @@ __global__ __launch_bounds__(kCandThreads) void topk_cand_fast_kernel(CandArgs a
     }
 
     // this thread's blocks (positions 256 BPT tid ..): keys above / equal to tau
-    const uint32_t p_first = (uint32_t)tid * BPT * kTopkKeyBlock;
     uint32_t sw[NWD], tw[NWD];
 #pragma unroll
     for (int i = 0; i < NWD; ++i) sw[i] = tw[i] = 0u;
     for (uint32_t q = 0; q < mine; ++q) {
         const uint32_t kk = s_key[before + q];
-        const uint32_t p = s_pos[before + q] - p_first;  // 0 .. 256 BPT - 1
+        const uint32_t p = s_pos[before + q];  // 0 .. 256 BPT - 1
         const uint32_t bit = 1u << (p & 31u), wi = p >> 5;
         const uint32_t sb = kk > tau ? bit : 0u, tb = kk == tau ? bit : 0u;
 #pragma unroll
@@ -1230,7 +1239,7 @@ hipError_t launch_topk_cands(const Geometry &g, const uint32_t *cand_count, cons
     a.max_pages = g.max_pages;
     a.kblocks = topk_key_blocks(g);
     a.slow = slow;
-    const size_t fast_lds = sizeof(uint32_t) * 2 * (size_t)kCandCap;
+    const size_t fast_lds = (sizeof(uint32_t) + sizeof(uint16_t)) * (size_t)kCandCap;
     const bool two = a.kblocks > kCandThreads;  // more key blocks than threads
     const void *fast = two ? reinterpret_cast<const void *>(&topk_cand_fast_kernel<2>)
                            : reinterpret_cast<const void *>(&topk_cand_fast_kernel<1>);
