@@ -644,58 +644,36 @@ struct SampleArgs {
     int n_q, max_len, causal, top_k, cols, rank;
 };
 
-constexpr int kSampleThreads = 256;
-constexpr int kSamplePerThread = kMaxLen / kTopkSampleStride / kSampleThreads;  // 32
-
 // One workgroup per row: the rank-th largest of the row's valid sampled keys,
-// by three radix levels (11, 11 and 10 bits) over keys held in registers.
-// Rows with no more than k valid keys select them all and get the largest
-// threshold (no candidates); rows with no more than `rank` valid samples get 0
-// (every key a candidate).
-__global__ __launch_bounds__(kSampleThreads) void topk_sample_thresh_kernel(SampleArgs a) {
-    __shared__ __align__(16) uint32_t hist[kHistWords];
-    __shared__ uint32_t s_res[2];
+// found by short_select over 16 keys per thread in registers (NT = 256 for up
+// to 4096 samples, 512 for up to 8192; which thread holds which key does not
+// matter, so the loads are strided and coalesced).  Rows with no more than k
+// valid keys select them all and get the largest threshold (no candidates);
+// rows with no more than `rank` valid samples get 0 (every key a candidate).
+static_assert(kMaxLen / kTopkSampleStride <= 512 * kShortKeys, "samples of a row fit 512 threads");
+
+template <int NT>
+__global__ __launch_bounds__(NT) void topk_sample_thresh_kernel(SampleArgs a) {
+    __shared__ ShortSelectLds<NT> sm;
     const int row = blockIdx.x, b = row / a.n_q, tid = threadIdx.x;
     if (row == 0 && tid == 0) a.slow[0] = 0u;
     const int n = valid_keys(a.seq_lens, a.q_pos, a.causal, b, row, a.max_len);
-    const int m = div_up(n, kTopkSampleStride);  // valid samples
+    const int m = div_up(n, kTopkSampleStride);  // valid samples, at most a.cols <= NT * kShortKeys
     if (n <= a.top_k || m <= a.rank) {
         if (tid == 0) a.thresh[row] = n <= a.top_k ? 0xffffffffu : 0u;
         return;
     }
     const float *srow = a.samples + (size_t)row * a.cols;
-    uint32_t key[kSamplePerThread];
+    uint32_t key[kShortKeys], vmask = 0u;
 #pragma unroll
-    for (int u = 0; u < kSamplePerThread; ++u) {
-        const int i = u * kSampleThreads + tid;
-        key[u] = i < m ? score_key(srow[i]) : 0u;
+    for (int j = 0; j < kShortKeys; ++j) {
+        const int i = j * NT + tid;
+        key[j] = score_key(srow[min(i, m - 1)]);
+        vmask |= (i < m ? 1u : 0u) << j;
     }
-    uint32_t need = (uint32_t)a.rank, prefix = 0u;
-    // level: bits [lo, hi) of keys whose bits above hi equal prefix
-    auto level = [&](int hi, int lo, int nbins) {
-        for (int x = tid; x < nbins; x += kSampleThreads) hist[x] = 0u;
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < kSamplePerThread; ++u) {
-            const int i = u * kSampleThreads + tid;
-            if (i < m && (hi == 32 || (key[u] >> hi) == prefix))
-                atomicAdd(&hist[(key[u] >> lo) & (uint32_t)(nbins - 1)], 1u);
-        }
-        __syncthreads();
-    };
-    level(32, kCoarseShift, kCoarseBins);
-    find_threshold_bin<kCoarseBins>(hist, need, s_res);
-    prefix = s_res[0];
-    need -= s_res[1];
-    __syncthreads();
-    level(kCoarseShift, kMidShift, kMidBins);
-    find_threshold_bin<kMidBins>(hist, need, s_res);
-    prefix = (prefix << (kCoarseShift - kMidShift)) | s_res[0];
-    need -= s_res[1];
-    __syncthreads();
-    level(kMidShift, 0, kLowBins);
-    find_threshold_bin<kLowBins>(hist, need, s_res);
-    if (tid == 0) a.thresh[row] = (prefix << kMidShift) | s_res[0];
+    uint32_t tau, r;
+    short_select<NT>(key, vmask, (uint32_t)a.rank, sm, tau, r);
+    if (tid == 0) a.thresh[row] = tau;
 }
 
 struct CandArgs {
@@ -1209,7 +1187,10 @@ hipError_t launch_topk_sample_thresh(const Geometry &g, const float *samples,
     a.top_k = g.top_k;
     a.cols = topk_sample_cols(g);
     a.rank = topk_sample_rank(g);
-    topk_sample_thresh_kernel<<<dim3(g.rows), dim3(kSampleThreads), 0, stream>>>(a);
+    if (a.cols <= 256 * kShortKeys)
+        topk_sample_thresh_kernel<256><<<dim3(g.rows), dim3(256), 0, stream>>>(a);
+    else
+        topk_sample_thresh_kernel<512><<<dim3(g.rows), dim3(512), 0, stream>>>(a);
     return hipGetLastError();
 }
 

@@ -168,12 +168,15 @@ def test_chunked_prefill_many_rows_chain():
 
 
 @pytest.mark.parametrize("page_size,top_k,length", [(64, 256, 20000), (0, 40, 20000),
-                                                    (0, 256, 20000), (0, 4096, 9000)])
+                                                    (0, 256, 20000), (0, 4096, 9000),
+                                                    (0, 512, 140000)])
 def test_chunked_prefill_many_rows_shapes(page_size, top_k, length):
     """More than 128 causal rows: the two-pass top-k (long rows next to short
     ones, whose dense candidates send them to the exact fallback) with paged
-    and contiguous caches and small k, and a k above 2048 (the top-k over full
-    score rows); every row and layer compared."""
+    and contiguous caches and small k, a k above 2048 (the top-k over full
+    score rows), and a cache above 131072 tokens (more than 4096 samples per
+    row: the 512-thread sampled-threshold workgroup); every row and layer
+    compared."""
     w = inputs.small_workload(batch=2, lens=(length, length - 2000), n_q=96, causal=True,
                               q_pos0=(length - 96, 1500), top_k=top_k, n_layers=1,
                               page_size=page_size, wid=86)
