@@ -103,15 +103,25 @@ __device__ __forceinline__ void pf_lds_barrier() {
 
 // Largest / smallest key limit over the 16 queries of a tile (every lane gets
 // it; the same in every wave of the workgroup, which holds the same queries).
+// A butterfly inside each 16-lane row with DPP operand permutes (lane ^ 1,
+// lane ^ 2, then the half-row and row mirrors, which pair the quads and the
+// halves), four dependent VALU steps instead of four LDS permutes.  Called
+// with every lane active.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int x) {
+    return __builtin_amdgcn_mov_dpp(x, CTRL, 0xf, 0xf, false);
+}
 __device__ __forceinline__ int tile_limit(int n) {
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) n = max(n, __shfl_xor(n, m));
-    return n;
+    n = max(n, dpp_i32<0xB1>(n));
+    n = max(n, dpp_i32<0x4E>(n));
+    n = max(n, dpp_i32<0x141>(n));
+    return max(n, dpp_i32<0x140>(n));
 }
 __device__ __forceinline__ int tile_limit_min(int n) {
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) n = min(n, __shfl_xor(n, m));
-    return n;
+    n = min(n, dpp_i32<0xB1>(n));
+    n = min(n, dpp_i32<0x4E>(n));
+    n = min(n, dpp_i32<0x141>(n));
+    return min(n, dpp_i32<0x140>(n));
 }
 
 // The fp32 threshold equivalent to an order-preserving key threshold th:
