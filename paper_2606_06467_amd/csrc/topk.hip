@@ -338,7 +338,7 @@ __device__ void row_topk(const float *srow, const uint32_t *ghist, int n, int k,
             filter_classify_1024(key, c * 1024, n, b1, sure + c * 32, tie + c * 32, cmask);
         uint32_t slot = 0;
         if (lane == 0 && cnt) slot = atomicAdd(s_cand_count, cnt);
-        filter_append_1024(key, c * 1024, cmask, __shfl(slot, 0),
+        filter_append_1024(key, c * 1024, cmask, __builtin_amdgcn_readfirstlane(slot),
                            [&](uint32_t at, uint32_t kv, uint32_t j) {
                                if (at < cap) {
                                    ckey[at] = kv;
@@ -411,6 +411,25 @@ static_assert(1024 * kShortKeys >= kTopkRowMaxLen, "one 1024-thread workgroup ho
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xf, 0xf, false);
+}
+
+// AND and OR over the 64 lanes of a wave (every lane active): a butterfly
+// inside each 16-lane row with DPP (lane ^ 1, lane ^ 2, half-row and row
+// mirrors), then across rows with the permlane16 / permlane32 swaps; VALU
+// steps only, no LDS permutes.
+__device__ __forceinline__ void wave_and_or(uint32_t &a, uint32_t &o) {
+    a &= dpp_u32<0xB1>(a);  o |= dpp_u32<0xB1>(o);
+    a &= dpp_u32<0x4E>(a);  o |= dpp_u32<0x4E>(o);
+    a &= dpp_u32<0x141>(a); o |= dpp_u32<0x141>(o);
+    a &= dpp_u32<0x140>(a); o |= dpp_u32<0x140>(o);
+    auto ra = __builtin_amdgcn_permlane16_swap(a, a, false, false);
+    auto ro = __builtin_amdgcn_permlane16_swap(o, o, false, false);
+    a = ra[0] & ra[1];
+    o = ro[0] | ro[1];
+    ra = __builtin_amdgcn_permlane32_swap(a, a, false, false);
+    ro = __builtin_amdgcn_permlane32_swap(o, o, false, false);
+    a = ra[0] & ra[1];
+    o = ro[0] | ro[1];
 }
 
 // Each of 8 values summed over the 64 lanes; lane L ends with the total of
@@ -805,11 +824,7 @@ void topk_cand_fast_kernel(CandArgs a) {
             kand &= key[j];
             kor |= key[j];
         }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        kand &= (uint32_t)__shfl_xor((int)kand, m);
-        kor |= (uint32_t)__shfl_xor((int)kor, m);
-    }
+    wave_and_or(kand, kor);
     if (lane == 0) {
         s_andor[0][wave] = kand;
         s_andor[1][wave] = kor;
