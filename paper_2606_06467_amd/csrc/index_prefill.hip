@@ -20,6 +20,11 @@
 // staged in LDS and written as whole 1 KiB row segments (direct 16-byte stores
 // of 64-byte row pieces reached only about 3 TB/s), one tile later, after the
 // next wait, so that waiting for loads never waits for fresh stores.
+// Three kernels share this mapping: index_prefill_kernel writes the scores
+// (clsa_index_scores, the distillation loss, the top-k over full score rows)
+// or, with a key stride, the sampled scores of the two-pass chunked-prefill
+// top-k; index_emit_kernel is that top-k's second pass, which writes only each
+// row's candidates.
 #include <type_traits>
 
 #include "clsa_internal.h"

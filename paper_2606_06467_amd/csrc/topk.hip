@@ -24,9 +24,10 @@
 //     and, per wave, its candidates into a region of its own) and a second
 //     launch with one workgroup per row (topk_finish_kernel) does steps 3-5
 //     with the bitmaps in LDS and the candidates in registers.  The hand-off
-//     goes through the kernel boundary: a ticket taken by the last filter
-//     workgroup would need an agent-scope release fence, which on this chip
-//     writes back the whole L2 of the XCD from every workgroup.
+//     goes through the kernel boundary: the finish works with 1024 threads per
+//     row, the filter with 256-thread workgroups, so a last-arriver finish (as
+//     the attention kernel merges its splits) would run on a quarter of the
+//     threads.
 // If the per-row kernel's candidate list overflows (very flat score rows),
 // steps 3-4 re-read the row instead: slower, same result.  The regions of the
 // wide path hold every key of their wave, so they never overflow.
