@@ -735,7 +735,7 @@ void topk_cand_fast_kernel(CandArgs a) {
     constexpr int NT = kCandThreads;
     constexpr int NW = NT / 64;
     constexpr int NWD = 8 * BPT;  // bitmap words per thread
-    constexpr int kFirst = 24;    // entries of a block loaded in the first batch (about 8 expected)
+    constexpr int kFirst = 16;    // entries of a block loaded in the first batch (one 128-byte line; about 8 expected)
     // [kCandCap] keys, then [kCandCap] 16-bit positions relative to the first
     // key of the owning thread's blocks (48 KiB: three workgroups per CU)
     extern __shared__ __align__(16) uint32_t lds[];
