@@ -173,7 +173,8 @@ struct DecodeWs {
     uint32_t *cand_count = nullptr;  // [rows, key blocks]
     uint32_t *cands = nullptr;     // [rows, key blocks, kTopkBlockSlots, 2]
     uint32_t *slow = nullptr;      // [1 + rows]: rows selected the slow way
-    uint32_t *tickets = nullptr;   // [rows, kv_heads]: split arrivals of the in-kernel merge
+    uint32_t *tickets = nullptr;   // [rows, kv_heads]: split arrivals of the in-kernel merge,
+                                   // cleared by the first index launch of every index set
 };
 
 // Every layer gathers its K/V rows from the cache through the shared index set.
@@ -374,9 +375,6 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
     const size_t lse_stride = (size_t)g.rows * g.q_heads;
     const size_t set_stride = (size_t)g.rows * g.top_k;         // index entries per set
     const int n_sets = n_layers > 0 ? (n_layers + group - 1) / group : 1;
-    // The first index launch of every set clears the attention's arrival
-    // counters, so the attention merges its splits in the kernel.
-    uint32_t *tickets = w.tickets;
     for (int s = 0; s < n_sets; ++s) {
         const uint16_t *qi = static_cast<const uint16_t *>(q_idx) + (size_t)s * q_idx_stride;
         const uint16_t *ki = static_cast<const uint16_t *>(k_idx) + (size_t)s * k_idx_stride;
@@ -424,7 +422,7 @@ clsa_status decode_step_impl(const clsa_shape *shape, const void *q_idx, int64_t
             if (mark && hipEventRecord(t_hook.ev[4 + 2 * l], st) != hipSuccess)
                 return CLSA_ERR_HIP;
             CLSA_TRY(from_hip(clsa::launch_sparse_attn(g, ql, k_cache, v_cache, page_table, is,
-                                                       ns, ol, lsel, w.partials, tickets, st,
+                                                       ns, ol, lsel, w.partials, w.tickets, st,
                                                        mark ? t_hook.ev[5 + 2 * l] : nullptr)));
         }
     }
