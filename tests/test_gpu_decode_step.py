@@ -69,6 +69,25 @@ def test_small_ragged_with_short_rows():
     _check_step(w, x, range(3), "ragged small")
 
 
+@pytest.mark.parametrize("q_heads,kv_heads,page_size", [(8, 8, 0), (16, 8, 0), (40, 8, 0),
+                                                    (64, 8, 0), (32, 4, 0), (40, 8, 64)])
+def test_step_group_sizes_in_kernel_merge(q_heads, kv_heads, page_size):
+    """Every GQA group size through the step, whose attention merges its splits
+    inside the kernel (the last split of each (row, KV head) to arrive): one
+    wave per query head for G <= 4, several heads per wave for G = 5 and 8;
+    rows with every split holding tokens next to rows whose short index sets
+    fill only some of the splits, and an empty row; every layer compared."""
+    # paged caches take at most 8 splits (the in-kernel merge) from 128 (row, KV
+    # head) units on: 16 sequences; (32, 4) plans 16 splits and merges in a
+    # second launch
+    lens = (9000, 700, 0, 5000) if page_size == 0 else (
+        9000, 700, 0, 5000, 3100, 8100, 1024, 1025, 6000, 2047, 4500, 7777, 300, 9999, 2600, 5100)
+    w = inputs.small_workload(batch=len(lens), lens=lens, top_k=1024, n_layers=2,
+                              q_heads=q_heads, kv_heads=kv_heads, page_size=page_size, wid=97)
+    x = inputs.make_inputs(w)
+    _check_step(w, x, range(w.n_layers), f"group {q_heads // kv_heads} kv {kv_heads} page {page_size}")
+
+
 def test_single_layer_gathers_from_the_cache():
     """With one layer the step attends straight from the cache (no compact copy)."""
     w = inputs.small_workload(batch=3, lens=(9000, 2500, 4000), top_k=1024, n_layers=1, wid=94)
