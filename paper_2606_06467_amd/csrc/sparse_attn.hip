@@ -61,6 +61,8 @@ constexpr int kMaxSplits = 128;  // splits per (row, KV head): the merge's large
 constexpr int kManyUnits = 4096; // (row, KV head) units from which splits go by key range
 constexpr int kKtPitch = 17;     // 16-byte pieces per staged K row (one of padding)
 constexpr int kManySplits = 8;   // splits per unit then (measured best of 1, 2, 4, 8, 16)
+constexpr int kResidentWgs = 1024;  // many units: workgroups resident on the chip (4 per CU),
+                                    // the chunk-order period's base
 
 // The fields every workgroup reads first come first: the kernel's prologue
 // then fetches them in one batch of scalar loads (a field pushed past them
@@ -234,6 +236,18 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     const int qq = lane >> 4, sub = lane & 15;
     const int span = a.chunks_per_split * 64;
     const int tok_begin = split * span;
+    // Chunk order of the many-unit form (MQK && !PVM): a workgroup starts at
+    // chunk (blockIdx / P) mod chunks_per_split, P = kResidentWgs /
+    // chunks_per_split, and wraps around.  Workgroups start in grid order, about
+    // P per chunk time once the chip is full, so the resident ones tend to be on
+    // the same chunk of their stretch at the same time; as the index lists are
+    // ascending and all rows' stretches span about the same keys, the K/V rows
+    // gathered at any moment come from about one chunk's share of the stretch
+    // instead of all of it.  The online softmax does not depend on the order of
+    // the chunks (only the order of its fp32 roundings does).
+    constexpr bool ROT = MQK && !PVM;
+    const unsigned rot_period = max(1, kResidentWgs / a.chunks_per_split);
+    const int rot = ROT && split_major ? (int)((blockIdx.x / rot_period) % (unsigned)a.chunks_per_split) : 0;
     const int row_elems = a.kv_heads * kHeadDim;
     const char *kseq = reinterpret_cast<const char *>(
         a.k + ((size_t)b * a.max_len * a.kv_heads + g) * kHeadDim);
@@ -246,8 +260,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     int jpre[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        jpre[i] = DENSE ? tok_begin + i * 16 + wave * 4 + qq
-                        : sel_at(sel, min(tok_begin + i * 16 + wave * 4 + qq, a.top_k - 1));
+        jpre[i] = DENSE ? tok_begin + rot * 64 + i * 16 + wave * 4 + qq
+                        : sel_at(sel, min(tok_begin + rot * 64 + i * 16 + wave * 4 + qq, a.top_k - 1));
     const int n = row_keys<DENSE>(a, row);
     const int nsplit = div_up(n, span);  // splits that hold tokens
 
@@ -261,6 +275,15 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     }
     if (split >= nsplit) return;  // uniform; the merge masks splits past the last one
     const int tok_end = min(n, tok_begin + span);
+    const int nch = div_up(tok_end - tok_begin, 64);  // chunks of this split (>= 1)
+    int cfirst = rot;
+    if (ROT && cfirst >= nch) {  // a short split (the row's last): start from a chunk it has
+        cfirst = rot % nch;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            jpre[i] = DENSE ? tok_begin + cfirst * 64 + i * 16 + wave * 4 + qq
+                            : sel_at(sel, min(tok_begin + cfirst * 64 + i * 16 + wave * 4 + qq, a.top_k - 1));
+    }
 
     uint4 qv[MQK ? 1 : G];
     bf16x8 qb[4];  // MQK: B operands, Q^T (32 dims x 16 head columns, heads >= G zero)
@@ -293,7 +316,13 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < (PVM ? 8 : 1); ++i) pacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int c0 = tok_begin; c0 < tok_end; c0 += 64) {
+    for (int ci = 0, c = cfirst, c0 = tok_begin; ROT ? ci < nch : c0 < tok_end; ++ci, c0 += 64) {
+        int c0_next = c0 + 64;
+        if constexpr (ROT) {
+            c0 = tok_begin + c * 64;
+            c = c + 1 < nch ? c + 1 : 0;  // the next chunk in this workgroup's order
+            c0_next = tok_begin + c * 64;
+        }
         int jr[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)  // -1 padding -> row 0; dense positions past n -> row n-1
@@ -330,8 +359,8 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
         // prefetch the next chunk's indices (clamped, so always readable)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            jpre[i] = DENSE ? c0 + 64 + i * 16 + wave * 4 + qq
-                            : sel_at(sel, min(c0 + 64 + i * 16 + wave * 4 + qq, a.top_k - 1));
+            jpre[i] = DENSE ? c0_next + i * 16 + wave * 4 + qq
+                            : sel_at(sel, min(c0_next + i * 16 + wave * 4 + qq, a.top_k - 1));
         // All K and V gathers of the chunk are in flight before any math (without
         // this the scheduler sinks the V loads below the logits, which costs a
         // second memory round trip per chunk).
@@ -726,7 +755,9 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 // the chip anyway; there each list is cut into kManySplits stretches, issued
 // stretch by stretch over all rows, so that the K/V rows gathered at any time
 // come from one key range (the lists are ascending) and stay in the Infinity
-// Cache (8192 rows x 2048 of 131072 keys: 8.8 -> 7.2 ms per layer).  keys: the
+// Cache (8192 rows x 2048 of 131072 keys: 8.8 -> 7.2 ms per layer); within a
+// stretch the kernel rotates each workgroup's chunk order so that the resident
+// workgroups gather from about one chunk's share of it.  keys: the
 // most keys a row can have (top_k, or max_len for dense attention).
 static void plan_splits(const Geometry &g, int keys, bool dense, int &splits,
                         int &chunks_per_split) {
