@@ -61,8 +61,8 @@ constexpr int kMaxSplits = 128;  // splits per (row, KV head): the merge's large
 constexpr int kManyUnits = 4096; // (row, KV head) units from which splits go by key range
 constexpr int kKtPitch = 17;     // 16-byte pieces per staged K row (one of padding)
 constexpr int kManySplits = 8;   // splits per unit then (measured best of 1, 2, 4, 8, 16)
-constexpr int kResidentWgs = 1024;  // many units: workgroups resident on the chip (4 per CU),
-                                    // the chunk-order period's base
+constexpr int kResidentWgs = 1280;  // many units: workgroups resident on the chip (5 per CU),
+                                    // the chunk-order period's base (1024..1536 measured alike)
 
 // The fields every workgroup reads first come first: the kernel's prologue
 // then fetches them in one batch of scalar loads (a field pushed past them
@@ -208,7 +208,15 @@ __device__ __forceinline__ void split_merge(const AttnArgs &a, int row, int g, i
 // MQK: matrix-core logits with per-wave softmax states; PVM (with MQK): the
 // weighted V on the matrix cores as well.
 template <int G, bool PAGED, bool DENSE, bool MQK, bool PVM>
-__global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MQK && !PVM ? 5 : 1)))
+void sparse_attn_kernel(AttnArgs a) {
+    // Many-unit form (MQK && !PVM): five workgroups per CU (G <= 5; G = 8 keeps
+    // four, its accumulators need the registers), so the query operands wait in
+    // LDS instead of 16 registers: the G query rows, which every wave writes in
+    // full (the same values) and each lane reads back only where it wrote them
+    // itself, so no barrier is needed.
+    constexpr bool QLDS = MQK && !PVM;
+    __shared__ __align__(16) u32x4 s_qb[QLDS ? G : 1][QLDS ? 16 : 1];  // [head][16-byte piece]
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
     constexpr int NO = pow2_at_least(8 * G);   // accumulators per lane before the reduction
     __shared__ float zs[G][64];                // logits -> weights of the current chunk
@@ -298,7 +306,11 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int s4 = 0; s4 < 4; ++s4) {
             const u32x4 v = *reinterpret_cast<const u32x4 *>(qp + 32 * s4);
-            qb[s4] = __builtin_bit_cast(bf16x8, sub < G ? v : u32x4{0u, 0u, 0u, 0u});
+            if (QLDS) {
+                if (sub < G) s_qb[sub][qq + 4 * s4] = v;
+            } else {
+                qb[s4] = __builtin_bit_cast(bf16x8, sub < G ? v : u32x4{0u, 0u, 0u, 0u});
+            }
         }
     }
     if (tid < G) {
@@ -412,7 +424,10 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
             for (int s4 = 0; s4 < 4; ++s4) {
                 const int arow = PVM ? 4 * (sub & 3) + (sub >> 2) : sub;
                 const bf16x8 ka = __builtin_bit_cast(bf16x8, sk[arow * kKtPitch + qq + 4 * s4]);
-                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb[s4], c, 0, 0, 0);
+                const bf16x8 qop = QLDS ? __builtin_bit_cast(bf16x8, sub < G ? s_qb[min(sub, G - 1)][qq + 4 * s4]
+                                                                              : u32x4{0u, 0u, 0u, 0u})
+                                        : qb[s4];
+                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop, c, 0, 0, 0);
             }
             // Online softmax per wave over its own 16 slots (no workgroup barrier):
             // lane (qq, sub) keeps the running maximum and sum of head sub; the
