@@ -2,11 +2,12 @@
 // O_t = Attn(Q_t, K_{S_t}, V_{S_t}); softmax attention as in Eq. 1; no
 // positional encoding on this path).
 //
-// One workgroup (4 waves) = one (query row, KV head g, split of S).  A split is
-// a run of 64-token chunks of the row's index list.  Per chunk:
+// One workgroup (NW waves: 4, or 1 in the chunked-prefill form) = one (query
+// row, KV head g, split of S).  A split is a run of chunks of 16 NW tokens of
+// the row's index list.  Per chunk:
 //   * each 16-lane quarter-wave gathers one selected token's 256-byte K row and
-//     256-byte V row of head g (16 bytes per lane); 4 rounds x 4 waves x 4
-//     quarters = 64 tokens.  Index loads, page-table loads and the K/V loads
+//     256-byte V row of head g (16 bytes per lane); 4 rounds x NW waves x 4
+//     quarters = 16 NW tokens.  Index loads, page-table loads and the K/V loads
 //     are each issued as one unconditional batch (positions past the end are
 //     clamped and masked afterwards), so a workgroup waits for memory about
 //     three times instead of once per token;
@@ -16,7 +17,7 @@
 //       into v_mfma_f32_16x16x32_bf16 against Q^T (heads padded to 16), and
 //       each wave keeps its own online softmax per head (base-2 exponentials;
 //       the four lanes of a head combine with permlane swaps) and its own
-//       weighted-V accumulators: no workgroup barrier per chunk; the four wave
+//       weighted-V accumulators: no workgroup barrier per chunk; the wave
 //       states are merged by the log-sum-exp rule at the end.  On decode grids
 //       (PVM) the weighted V is a v_mfma_f32_16x16x16_bf16 product whose
 //       operands are the lane's own weights and V rows (the logits tile is
@@ -61,8 +62,9 @@ constexpr int kMaxSplits = 128;  // splits per (row, KV head): the merge's large
 constexpr int kManyUnits = 4096; // (row, KV head) units from which splits go by key range
 constexpr int kKtPitch = 17;     // 16-byte pieces per staged K row (one of padding)
 constexpr int kManySplits = 8;   // splits per unit then (measured best of 1, 2, 4, 8, 16)
-constexpr int kResidentWgs = 1280;  // many units: workgroups resident on the chip (5 per CU),
-                                    // the chunk-order period's base (1024..1536 measured alike)
+constexpr int kManyUnitWaves = 1;    // waves per workgroup of the many-unit form (measured 1, 2, 4)
+constexpr int kResidentWaves = 5120; // many units: waves resident on the chip (5 per SIMD), the
+                                     // base of the chunk-order period (4096..5120 measured alike)
 
 // The fields every workgroup reads first come first: the kernel's prologue
 // then fetches them in one batch of scalar loads (a field pushed past them
@@ -145,12 +147,12 @@ __device__ __forceinline__ uint64_t pack2f(float x, float y) {
 // costs about a microsecond per workgroup.  At most kFusedMaxSplits splits.
 constexpr int kFusedMaxSplits = 8;
 
-template <int G, bool DENSE, typename Combine>
+template <int G, bool DENSE, int NW, typename Combine>
 __device__ __forceinline__ void split_merge(const AttnArgs &a, int row, int g, int split,
                                             int nsplit, size_t base, Combine combine) {
     __shared__ uint32_t s_ticket;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    for (int e = 2 * tid; e < G * kHeadDim; e += 512) {
+    for (int e = 2 * tid; e < G * kHeadDim; e += 128 * NW) {
         const int h = e / kHeadDim, dim = e - h * kHeadDim;
         float m, l, s0, s1;
         combine(h, e, m, l, s0);
@@ -170,7 +172,7 @@ __device__ __forceinline__ void split_merge(const AttnArgs &a, int row, int g, i
     if (s_ticket != (uint32_t)(nsplit - 1)) return;  // uniform
     if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int Hq = a.q_heads;
-    for (int h = wave; h < G; h += 4) {
+    for (int h = wave; h < G; h += NW) {
         const size_t hb = base + (size_t)h * a.splits;
         uint64_t o[kFusedMaxSplits], ml[kFusedMaxSplits];
 #pragma unroll
@@ -207,14 +209,18 @@ __device__ __forceinline__ void split_merge(const AttnArgs &a, int row, int g, i
 
 // MQK: matrix-core logits with per-wave softmax states; PVM (with MQK): the
 // weighted V on the matrix cores as well.
-template <int G, bool PAGED, bool DENSE, bool MQK, bool PVM>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MQK && !PVM ? 5 : 1)))
+template <int G, bool PAGED, bool DENSE, bool MQK, bool PVM, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(MQK && !PVM && G <= 5 ? 5 : 1)))
 void sparse_attn_kernel(AttnArgs a) {
-    // Many-unit form (MQK && !PVM): five workgroups per CU (G <= 5; G = 8 keeps
-    // four, its accumulators need the registers), so the query operands wait in
-    // LDS instead of 16 registers: the G query rows, which every wave writes in
-    // full (the same values) and each lane reads back only where it wrote them
-    // itself, so no barrier is needed.
+    static_assert(NW == 4 || (MQK && !PVM), "fewer waves per workgroup: the many-unit form only");
+    constexpr int CH = 16 * NW;  // tokens per chunk: 16 per wave
+    // Many-unit form (MQK && !PVM): one wave per workgroup and five waves per
+    // SIMD (G <= 5; G = 8 keeps four, its accumulators need the registers), so
+    // that as many rows as possible are resident at once (see the chunk order
+    // below); the query operands therefore wait in LDS instead of 16 registers:
+    // the G query rows, which every wave writes in full (the same values) and
+    // each lane reads back only where it wrote them itself, so no barrier is
+    // needed.
     constexpr bool QLDS = MQK && !PVM;
     __shared__ __align__(16) u32x4 s_qb[QLDS ? G : 1][QLDS ? 16 : 1];  // [head][16-byte piece]
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
@@ -222,11 +228,11 @@ void sparse_attn_kernel(AttnArgs a) {
     __shared__ float zs[G][64];                // logits -> weights of the current chunk
     __shared__ float s_scale[G];               // per-head rescale factor of this chunk
     __shared__ float s_ml[G][2];               // running max (log2 domain) and denominator
-    __shared__ __align__(16) float red[4][G * kHeadDim];  // cross-wave reduction of the accumulators
+    __shared__ __align__(16) float red[NW][G * kHeadDim];  // cross-wave reduction of the accumulators
     // MQK: per wave, its 16 gathered K rows (16 x 16 pieces of 16 bytes, padded)
-    __shared__ __align__(16) u32x4 s_kt[MQK ? 4 : 1][MQK ? 16 : 1][MQK ? kKtPitch : 1];
-    __shared__ __align__(16) float zw[MQK && !PVM ? 4 : 1][MQK && !PVM ? G : 1][16];  // MQK: weights per wave
-    __shared__ float s_wml[MQK ? 4 : 1][G][2];  // MQK: each wave's (max, sum) per head
+    __shared__ __align__(16) u32x4 s_kt[MQK ? NW : 1][MQK ? 16 : 1][MQK ? kKtPitch : 1];
+    __shared__ __align__(16) float zw[MQK && !PVM ? NW : 1][MQK && !PVM ? G : 1][16];  // MQK: weights per wave
+    __shared__ float s_wml[MQK ? NW : 1][G][2];  // MQK: each wave's (max, sum) per head
 
     // flattened grid, few (row, KV head) units: (row * kv_heads + g) * splits + split;
     // many units (kManyUnits or more): split * units + (row * kv_heads + g), so that
@@ -245,17 +251,20 @@ void sparse_attn_kernel(AttnArgs a) {
     const int span = a.chunks_per_split * 64;
     const int tok_begin = split * span;
     // Chunk order of the many-unit form (MQK && !PVM): a workgroup starts at
-    // chunk (blockIdx / P) mod chunks_per_split, P = kResidentWgs /
-    // chunks_per_split, and wraps around.  Workgroups start in grid order, about
-    // P per chunk time once the chip is full, so the resident ones tend to be on
-    // the same chunk of their stretch at the same time; as the index lists are
-    // ascending and all rows' stretches span about the same keys, the K/V rows
-    // gathered at any moment come from about one chunk's share of the stretch
-    // instead of all of it.  The online softmax does not depend on the order of
-    // the chunks (only the order of its fp32 roundings does).
+    // chunk (blockIdx / P) mod cps of its cps chunks and wraps around, P being
+    // the resident workgroups (kResidentWaves / NW) over cps.  Workgroups start
+    // in grid order, about P per chunk time once the chip is full, so the
+    // resident ones tend to be on the same chunk of their stretch at the same
+    // time; as the index lists are ascending and all rows' stretches span about
+    // the same keys, the K/V rows gathered at any moment come from about one
+    // chunk's share of the stretch instead of all of it, and each of them is
+    // gathered by more of the resident rows while the L2 still holds it, the
+    // more rows are resident.  The online softmax does not depend on the order
+    // of the chunks (only the order of its fp32 roundings does).
     constexpr bool ROT = MQK && !PVM;
-    const unsigned rot_period = max(1, kResidentWgs / a.chunks_per_split);
-    const int rot = ROT && split_major ? (int)((blockIdx.x / rot_period) % (unsigned)a.chunks_per_split) : 0;
+    const int cps = span / CH;  // chunks per split
+    const unsigned rot_period = max(1, kResidentWaves / NW / cps);
+    const int rot = ROT && split_major ? (int)((blockIdx.x / rot_period) % (unsigned)cps) : 0;
     const int row_elems = a.kv_heads * kHeadDim;
     const char *kseq = reinterpret_cast<const char *>(
         a.k + ((size_t)b * a.max_len * a.kv_heads + g) * kHeadDim);
@@ -268,14 +277,14 @@ void sparse_attn_kernel(AttnArgs a) {
     int jpre[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        jpre[i] = DENSE ? tok_begin + rot * 64 + i * 16 + wave * 4 + qq
-                        : sel_at(sel, min(tok_begin + rot * 64 + i * 16 + wave * 4 + qq, a.top_k - 1));
+        jpre[i] = DENSE ? tok_begin + rot * CH + i * 4 * NW + wave * 4 + qq
+                        : sel_at(sel, min(tok_begin + rot * CH + i * 4 * NW + wave * 4 + qq, a.top_k - 1));
     const int n = row_keys<DENSE>(a, row);
     const int nsplit = div_up(n, span);  // splits that hold tokens
 
     if (n == 0) {  // empty index set: output 0, lse -inf
         if (split == 0) {
-            for (int e = tid; e < G * kHeadDim; e += 256)
+            for (int e = tid; e < G * kHeadDim; e += 64 * NW)
                 a.out[((size_t)row * Hq + g * G) * kHeadDim + e] = 0;
             if (a.lse && tid < G) a.lse[(size_t)row * Hq + g * G + tid] = -INFINITY;
         }
@@ -283,14 +292,14 @@ void sparse_attn_kernel(AttnArgs a) {
     }
     if (split >= nsplit) return;  // uniform; the merge masks splits past the last one
     const int tok_end = min(n, tok_begin + span);
-    const int nch = div_up(tok_end - tok_begin, 64);  // chunks of this split (>= 1)
+    const int nch = div_up(tok_end - tok_begin, CH);  // chunks of this split (>= 1)
     int cfirst = rot;
     if (ROT && cfirst >= nch) {  // a short split (the row's last): start from a chunk it has
         cfirst = rot % nch;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            jpre[i] = DENSE ? tok_begin + cfirst * 64 + i * 16 + wave * 4 + qq
-                            : sel_at(sel, min(tok_begin + cfirst * 64 + i * 16 + wave * 4 + qq, a.top_k - 1));
+            jpre[i] = DENSE ? tok_begin + cfirst * CH + i * 4 * NW + wave * 4 + qq
+                            : sel_at(sel, min(tok_begin + cfirst * CH + i * 4 * NW + wave * 4 + qq, a.top_k - 1));
     }
 
     uint4 qv[MQK ? 1 : G];
@@ -328,12 +337,12 @@ void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < (PVM ? 8 : 1); ++i) pacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int ci = 0, c = cfirst, c0 = tok_begin; ROT ? ci < nch : c0 < tok_end; ++ci, c0 += 64) {
-        int c0_next = c0 + 64;
+    for (int ci = 0, c = cfirst, c0 = tok_begin; ROT ? ci < nch : c0 < tok_end; ++ci, c0 += CH) {
+        int c0_next = c0 + CH;
         if constexpr (ROT) {
-            c0 = tok_begin + c * 64;
+            c0 = tok_begin + c * CH;
             c = c + 1 < nch ? c + 1 : 0;  // the next chunk in this workgroup's order
-            c0_next = tok_begin + c * 64;
+            c0_next = tok_begin + c * CH;
         }
         int jr[4];
 #pragma unroll
@@ -371,8 +380,8 @@ void sparse_attn_kernel(AttnArgs a) {
         // prefetch the next chunk's indices (clamped, so always readable)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            jpre[i] = DENSE ? c0_next + i * 16 + wave * 4 + qq
-                            : sel_at(sel, min(c0_next + i * 16 + wave * 4 + qq, a.top_k - 1));
+            jpre[i] = DENSE ? c0_next + i * 4 * NW + wave * 4 + qq
+                            : sel_at(sel, min(c0_next + i * 4 * NW + wave * 4 + qq, a.top_k - 1));
         // All K and V gathers of the chunk are in flight before any math (without
         // this the scheduler sinks the V loads below the logits, which costs a
         // second memory round trip per chunk).
@@ -410,7 +419,7 @@ void sparse_attn_kernel(AttnArgs a) {
         if (MQK) {
             // Logits on the matrix cores: C = K_w (16 tokens x 128) x Q^T (128 x 16
             // head columns).  The wave's 16 K rows (gathered as above: token slot
-            // r = 4i + qq is chunk token 16i + 4w + qq) go through this wave's LDS
+            // r = 4i + qq is chunk token 4 NW i + 4w + qq) go through this wave's LDS
             // rows to reach the operand layout: lane (qq, sub) supplies A row sub,
             // dims 8qq + 32s of step s, and receives C rows 4qq + r of head sub.
             // A row m holds slot m, or with PVM slot 4(m & 3) + (m >> 2), so that
@@ -435,8 +444,8 @@ void sparse_attn_kernel(AttnArgs a) {
             float z[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int tl = PVM ? r * 16 + wave * 4 + qq    // slot 4r + qq
-                                   : qq * 16 + wave * 4 + r;   // slot 4qq + r
+                const int tl = PVM ? r * 4 * NW + wave * 4 + qq    // slot 4r + qq
+                                   : qq * 4 * NW + wave * 4 + r;   // slot 4qq + r
                 z[r] = sub < G && c0 + tl < tok_end ? c[r] * a.scale_log2 : -INFINITY;
             }
             const float mx = rows4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
@@ -504,7 +513,7 @@ void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
                     for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
                 }
-                // this lane's tokens 16i + 4w + qq are slots 4i + qq of the wave
+                // this lane's tokens 4 NW i + 4w + qq are slots 4i + qq of the wave
                 weighted_v([&](int h, int i) { return zw[wave][h][4 * i + qq]; });
             }
         } else {
@@ -598,14 +607,20 @@ void sparse_attn_kernel(AttnArgs a) {
     }
     __syncthreads();
     // (max, sum, weighted V) of head h over the workgroup: with per-wave softmax
-    // states (MQK) the four waves combine by the log-sum-exp rule
+    // states (MQK) the NW waves combine by the log-sum-exp rule
     auto combine = [&](int h, int e, float &m, float &l, float &sum) {
-        if (MQK) {
-            m = fmaxf(fmaxf(s_wml[0][h][0], s_wml[1][h][0]), fmaxf(s_wml[2][h][0], s_wml[3][h][0]));
+        if constexpr (MQK) {
+            if constexpr (NW == 4) {
+                m = fmaxf(fmaxf(s_wml[0][h][0], s_wml[1][h][0]), fmaxf(s_wml[2][h][0], s_wml[3][h][0]));
+            } else {
+                m = s_wml[0][h][0];
+#pragma unroll
+                for (int w4 = 1; w4 < NW; ++w4) m = fmaxf(m, s_wml[w4][h][0]);
+            }
             l = 0.0f;
             sum = 0.0f;
 #pragma unroll
-            for (int w4 = 0; w4 < 4; ++w4) {
+            for (int w4 = 0; w4 < NW; ++w4) {
                 const float mw = s_wml[w4][h][0];
                 const float f = mw == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mw - m);
                 l = fmaf(f, s_wml[w4][h][1], l);
@@ -619,7 +634,7 @@ void sparse_attn_kernel(AttnArgs a) {
     };
     // one split, or (with the in-kernel merge) the only split that holds tokens
     if (a.splits == 1 || (a.tickets && nsplit == 1)) {
-        for (int e = tid; e < G * kHeadDim; e += 256) {
+        for (int e = tid; e < G * kHeadDim; e += 64 * NW) {
             const int h = e / kHeadDim, dim = e - h * kHeadDim;
             float m, l, sum;
             combine(h, e, m, l, sum);
@@ -632,10 +647,10 @@ void sparse_attn_kernel(AttnArgs a) {
     }
     const size_t base = ((size_t)row * Hq + g * G) * a.splits;  // slot of (head g*G, split 0)
     if (a.tickets) {
-        split_merge<G, DENSE>(a, row, g, split, nsplit, base, combine);
+        split_merge<G, DENSE, NW>(a, row, g, split, nsplit, base, combine);
         return;
     }
-    for (int e = tid; e < G * kHeadDim; e += 256) {
+    for (int e = tid; e < G * kHeadDim; e += 64 * NW) {
         const int h = e / kHeadDim, dim = e - h * kHeadDim;
         float m, l, sum;
         combine(h, e, m, l, sum);
@@ -772,7 +787,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 // come from one key range (the lists are ascending) and stay in the Infinity
 // Cache (8192 rows x 2048 of 131072 keys: 8.8 -> 7.2 ms per layer); within a
 // stretch the kernel rotates each workgroup's chunk order so that the resident
-// workgroups gather from about one chunk's share of it.  keys: the
+// workgroups gather from about one chunk's share of it, with one wave per
+// workgroup so that many rows are resident.  keys: the
 // most keys a row can have (top_k, or max_len for dense attention).
 static void plan_splits(const Geometry &g, int keys, bool dense, int &splits,
                         int &chunks_per_split) {
@@ -804,13 +820,13 @@ static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int un
     // caches and for many units (chunked prefill); paged decode grids keep the
     // vector-unit logits and the shared softmax, which measured faster there.
     const bool many = grid.x / a.splits >= (unsigned)kManyUnits;
-    const bool mqk = !paged || many;
     // The weighted V goes to the matrix cores as well on decode grids; chunked
     // prefill (held by its gathers) measured faster with it on bf16 dot2.
-    if (paged && mqk) sparse_attn_kernel<G, true, DENSE, true, false><<<grid, dim3(256), 0, stream>>>(a);
-    else if (paged) sparse_attn_kernel<G, true, DENSE, false, false><<<grid, dim3(256), 0, stream>>>(a);
-    else if (many) sparse_attn_kernel<G, false, DENSE, true, false><<<grid, dim3(256), 0, stream>>>(a);
-    else sparse_attn_kernel<G, false, DENSE, true, true><<<grid, dim3(256), 0, stream>>>(a);
+    constexpr int NWM = kManyUnitWaves;
+    if (paged && many) sparse_attn_kernel<G, true, DENSE, true, false, NWM><<<grid, dim3(64 * NWM), 0, stream>>>(a);
+    else if (paged) sparse_attn_kernel<G, true, DENSE, false, false, 4><<<grid, dim3(256), 0, stream>>>(a);
+    else if (many) sparse_attn_kernel<G, false, DENSE, true, false, NWM><<<grid, dim3(64 * NWM), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false, DENSE, true, true, 4><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1 || a.tickets) return e;
