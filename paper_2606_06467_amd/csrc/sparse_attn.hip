@@ -18,12 +18,9 @@
 //       each wave keeps its own online softmax per head (base-2 exponentials;
 //       the four lanes of a head combine with permlane swaps) and its own
 //       weighted-V accumulators: no workgroup barrier per chunk; the wave
-//       states are merged by the log-sum-exp rule at the end.  On decode grids
-//       (PVM) the weighted V is a v_mfma_f32_16x16x16_bf16 product whose
-//       operands are the lane's own weights and V rows (the logits tile is
-//       ordered for that); in chunked prefill the weights reach the lanes
-//       holding the matching V rows through the wave's LDS rows and the
-//       weighted V is a bf16 dot2 product;
+//       states are merged by the log-sum-exp rule at the end.  The weighted V
+//       is a v_mfma_f32_16x16x16_bf16 product whose operands are the lane's
+//       own weights and V rows (the logits tile is ordered for that);
 //     - vector form (paged decode grids): each lane dots its 8 key values with
 //       the matching 8 values of every head (v_dot2_f32_bf16), a
 //       transpose-reduction over the 16 lanes leaves one (head, token) logit
@@ -31,8 +28,8 @@
 //       maximum and sum, updates the running max / denominator and rescales
 //       (online softmax, shared by the workgroup);
 //     so a split of any length needs one pass;
-//   * in the dot2 forms each lane accumulates weight x V for its 8 dimensions
-//     and G heads.
+//   * in the vector form each lane accumulates weight x V for its 8 dimensions
+//     and G heads (v_dot2_f32_bf16).
 // The accumulators are then reduced over lanes and waves in LDS.  With one
 // split the workgroup writes the bf16 output and lse itself.  Otherwise it
 // writes fp32 partials (o, m, l), combined by the exact log-sum-exp rule: inside
@@ -207,21 +204,21 @@ __device__ __forceinline__ void split_merge(const AttnArgs &a, int row, int g, i
     }
 }
 
-// MQK: matrix-core logits with per-wave softmax states; PVM (with MQK): the
-// weighted V on the matrix cores as well.
-template <int G, bool PAGED, bool DENSE, bool MQK, bool PVM, int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(MQK && !PVM && G <= 5 ? 5 : 1)))
+// MQK: matrix-core logits and weighted V with per-wave softmax states.  NW:
+// waves per workgroup (4; 1 in the many-unit form).
+template <int G, bool PAGED, bool DENSE, bool MQK, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW < 4 && G <= 5 ? 5 : 1)))
 void sparse_attn_kernel(AttnArgs a) {
-    static_assert(NW == 4 || (MQK && !PVM), "fewer waves per workgroup: the many-unit form only");
+    static_assert(NW == 4 || MQK, "fewer waves per workgroup: the matrix-core form only");
     constexpr int CH = 16 * NW;  // tokens per chunk: 16 per wave
-    // Many-unit form (MQK && !PVM): one wave per workgroup and five waves per
+    // Many-unit form (NW < 4): one wave per workgroup and five waves per
     // SIMD (G <= 5; G = 8 keeps four, its accumulators need the registers), so
     // that as many rows as possible are resident at once (see the chunk order
     // below); the query operands therefore wait in LDS instead of 16 registers:
     // the G query rows, which every wave writes in full (the same values) and
     // each lane reads back only where it wrote them itself, so no barrier is
     // needed.
-    constexpr bool QLDS = MQK && !PVM;
+    constexpr bool QLDS = NW < 4;
     __shared__ __align__(16) u32x4 s_qb[QLDS ? G : 1][QLDS ? 16 : 1];  // [head][16-byte piece]
     constexpr int NV = pow2_at_least(4 * G);   // logits per lane before the reduction
     constexpr int NO = pow2_at_least(8 * G);   // accumulators per lane before the reduction
@@ -231,7 +228,6 @@ void sparse_attn_kernel(AttnArgs a) {
     __shared__ __align__(16) float red[NW][G * kHeadDim];  // cross-wave reduction of the accumulators
     // MQK: per wave, its 16 gathered K rows (16 x 16 pieces of 16 bytes, padded)
     __shared__ __align__(16) u32x4 s_kt[MQK ? NW : 1][MQK ? 16 : 1][MQK ? kKtPitch : 1];
-    __shared__ __align__(16) float zw[MQK && !PVM ? NW : 1][MQK && !PVM ? G : 1][16];  // MQK: weights per wave
     __shared__ float s_wml[MQK ? NW : 1][G][2];  // MQK: each wave's (max, sum) per head
 
     // flattened grid, few (row, KV head) units: (row * kv_heads + g) * splits + split;
@@ -250,7 +246,7 @@ void sparse_attn_kernel(AttnArgs a) {
     const int qq = lane >> 4, sub = lane & 15;
     const int span = a.chunks_per_split * 64;
     const int tok_begin = split * span;
-    // Chunk order of the many-unit form (MQK && !PVM): a workgroup starts at
+    // Chunk order of the many-unit form (NW < 4): a workgroup starts at
     // chunk (blockIdx / P) mod cps of its cps chunks and wraps around, P being
     // the resident workgroups (kResidentWaves / NW) over cps.  Workgroups start
     // in grid order, about P per chunk time once the chip is full, so the
@@ -261,7 +257,7 @@ void sparse_attn_kernel(AttnArgs a) {
     // gathered by more of the resident rows while the L2 still holds it, the
     // more rows are resident.  The online softmax does not depend on the order
     // of the chunks (only the order of its fp32 roundings does).
-    constexpr bool ROT = MQK && !PVM;
+    constexpr bool ROT = NW < 4;
     const int cps = span / CH;  // chunks per split
     const unsigned rot_period = max(1, kResidentWaves / NW / cps);
     const int rot = ROT && split_major ? (int)((blockIdx.x / rot_period) % (unsigned)cps) : 0;
@@ -332,10 +328,10 @@ void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int d = 0; d < 8; ++d) acc[h][d] = 0.0f;
     float m_run = -INFINITY, l_run = 0.0f;  // MQK: head sub's running max / sum (this wave)
-    // PVM: weighted V per 16-dim block blk, lane (qq, sub): heads 4qq + r, dim 8sub + blk
-    f32x4 pacc[PVM ? 8 : 1];
+    // MQK: weighted V per 16-dim block blk, lane (qq, sub): heads 4qq + r, dim 8sub + blk
+    f32x4 pacc[MQK ? 8 : 1];
 #pragma unroll
-    for (int i = 0; i < (PVM ? 8 : 1); ++i) pacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < (MQK ? 8 : 1); ++i) pacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int ci = 0, c = cfirst, c0 = tok_begin; ROT ? ci < nch : c0 < tok_end; ++ci, c0 += CH) {
         int c0_next = c0 + CH;
@@ -422,7 +418,7 @@ void sparse_attn_kernel(AttnArgs a) {
             // r = 4i + qq is chunk token 4 NW i + 4w + qq) go through this wave's LDS
             // rows to reach the operand layout: lane (qq, sub) supplies A row sub,
             // dims 8qq + 32s of step s, and receives C rows 4qq + r of head sub.
-            // A row m holds slot m, or with PVM slot 4(m & 3) + (m >> 2), so that
+            // A row m holds slot 4(m & 3) + (m >> 2), so that
             // C row 4qq + r is slot 4r + qq: this lane's own gathered row of round r.
             u32x4 *sk = &s_kt[wave][0][0];
 #pragma unroll
@@ -431,7 +427,7 @@ void sparse_attn_kernel(AttnArgs a) {
             f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) {
-                const int arow = PVM ? 4 * (sub & 3) + (sub >> 2) : sub;
+                const int arow = 4 * (sub & 3) + (sub >> 2);
                 const bf16x8 ka = __builtin_bit_cast(bf16x8, sk[arow * kKtPitch + qq + 4 * s4]);
                 const bf16x8 qop = QLDS ? __builtin_bit_cast(bf16x8, sub < G ? s_qb[min(sub, G - 1)][qq + 4 * s4]
                                                                               : u32x4{0u, 0u, 0u, 0u})
@@ -444,8 +440,7 @@ void sparse_attn_kernel(AttnArgs a) {
             float z[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int tl = PVM ? r * 4 * NW + wave * 4 + qq    // slot 4r + qq
-                                   : qq * 4 * NW + wave * 4 + r;   // slot 4qq + r
+                const int tl = r * 4 * NW + wave * 4 + qq;  // slot 4r + qq
                 z[r] = sub < G && c0 + tl < tok_end ? c[r] * a.scale_log2 : -INFINITY;
             }
             const float mx = rows4_max(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])));
@@ -457,64 +452,48 @@ void sparse_attn_kernel(AttnArgs a) {
             const float scl = __builtin_amdgcn_exp2f(m_run - base);  // m_run = -inf -> 0
             l_run = l_run * scl + rows4_sum((w[0] + w[1]) + (w[2] + w[3]));
             m_run = m_new;
-            if constexpr (PVM) {
-                // Weighted V on the matrix cores with no data movement: contraction
-                // index k = 4qq + j stands for slot 4j + qq, so the A operand (P,
-                // heads x slots) is this lane's own weights w[0..3] (bf16) and the
-                // B operand of 16-dim block blk (slots x dims 8n + blk) is element
-                // blk of this lane's own four V rows.
-                const s16x4 pa = __builtin_bit_cast(
-                    s16x4, u32x2{__builtin_bit_cast(uint32_t, bf16x2{(__bf16)w[0], (__bf16)w[1]}),
-                                 __builtin_bit_cast(uint32_t, bf16x2{(__bf16)w[2], (__bf16)w[3]})});
-                // rescale: C row 4qq + r is head 4qq + r, whose factor every lane
-                // (*, head) holds
-                float f[4];
+            // Weighted V on the matrix cores with no data movement: contraction
+            // index k = 4qq + j stands for slot 4j + qq, so the A operand (P,
+            // heads x slots) is this lane's own weights w[0..3] (bf16) and the
+            // B operand of 16-dim block blk (slots x dims 8n + blk) is element
+            // blk of this lane's own four V rows.
+            const s16x4 pa = __builtin_bit_cast(
+                s16x4, u32x2{__builtin_bit_cast(uint32_t, bf16x2{(__bf16)w[0], (__bf16)w[1]}),
+                             __builtin_bit_cast(uint32_t, bf16x2{(__bf16)w[2], (__bf16)w[3]})});
+            // rescale: C row 4qq + r is head 4qq + r, whose factor every lane
+            // (*, head) holds
+            float f[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    f[r] = r < G ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                                 __builtin_bit_cast(int, scl), r))
-                                 : 1.0f;
-                    if (4 + r < G)
-                        f[r] = qq == 1 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                                       __builtin_bit_cast(int, scl), 4 + r))
-                                       : f[r];
-                }
+            for (int r = 0; r < 4; ++r) {
+                f[r] = r < G ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                             __builtin_bit_cast(int, scl), r))
+                             : 1.0f;
+                if (4 + r < G)
+                    f[r] = qq == 1 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                                   __builtin_bit_cast(int, scl), 4 + r))
+                                   : f[r];
+            }
 #pragma unroll
-                for (int blk = 0; blk < 8; ++blk)
+            for (int blk = 0; blk < 8; ++blk)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) pacc[blk][r] *= f[r];
-                const uint32_t v0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-                const uint32_t v1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
-                const uint32_t v2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
-                const uint32_t v3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
+                for (int r = 0; r < 4; ++r) pacc[blk][r] *= f[r];
+            const uint32_t v0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
+            const uint32_t v1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+            const uint32_t v2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
+            const uint32_t v3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
 #pragma unroll
-                for (int c2 = 0; c2 < 4; ++c2) {
-                    // dims 2c2 (low halves) and 2c2 + 1 (high halves) of rounds 0..3
-                    const s16x4 blo = __builtin_bit_cast(
-                        s16x4, u32x2{__builtin_amdgcn_perm(v1[c2], v0[c2], 0x05040100u),
-                                     __builtin_amdgcn_perm(v3[c2], v2[c2], 0x05040100u)});
-                    const s16x4 bhi = __builtin_bit_cast(
-                        s16x4, u32x2{__builtin_amdgcn_perm(v1[c2], v0[c2], 0x07060302u),
-                                     __builtin_amdgcn_perm(v3[c2], v2[c2], 0x07060302u)});
-                    pacc[2 * c2] =
-                        __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, blo, pacc[2 * c2], 0, 0, 0);
-                    pacc[2 * c2 + 1] =
-                        __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, bhi, pacc[2 * c2 + 1], 0, 0, 0);
-                }
-            } else {
-                if (sub < G)
-                    *reinterpret_cast<float4 *>(&zw[wave][sub][4 * qq]) =
-                        make_float4(w[0], w[1], w[2], w[3]);
-                // head h's rescale factor is held by lane h (row 0)
-#pragma unroll
-                for (int h = 0; h < G; ++h) {
-                    const float sc = __builtin_bit_cast(
-                        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, scl), h));
-#pragma unroll
-                    for (int d = 0; d < 8; ++d) acc[h][d] *= sc;
-                }
-                // this lane's tokens 4 NW i + 4w + qq are slots 4i + qq of the wave
-                weighted_v([&](int h, int i) { return zw[wave][h][4 * i + qq]; });
+            for (int c2 = 0; c2 < 4; ++c2) {
+                // dims 2c2 (low halves) and 2c2 + 1 (high halves) of rounds 0..3
+                const s16x4 blo = __builtin_bit_cast(
+                    s16x4, u32x2{__builtin_amdgcn_perm(v1[c2], v0[c2], 0x05040100u),
+                                 __builtin_amdgcn_perm(v3[c2], v2[c2], 0x05040100u)});
+                const s16x4 bhi = __builtin_bit_cast(
+                    s16x4, u32x2{__builtin_amdgcn_perm(v1[c2], v0[c2], 0x07060302u),
+                                 __builtin_amdgcn_perm(v3[c2], v2[c2], 0x07060302u)});
+                pacc[2 * c2] =
+                    __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, blo, pacc[2 * c2], 0, 0, 0);
+                pacc[2 * c2 + 1] =
+                    __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, bhi, pacc[2 * c2 + 1], 0, 0, 0);
             }
         } else {
             // logits: value index i*G + h, transpose-reduced over the 16 lanes of the quarter
@@ -569,7 +548,7 @@ void sparse_attn_kernel(AttnArgs a) {
         }
     }
 
-    if constexpr (PVM) {
+    if constexpr (MQK) {
         // the wave's weighted V is complete in the C tiles: head 4qq + r, dims 8sub..8sub+7
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -820,13 +799,11 @@ static hipError_t launch_attn_g(const AttnArgs &a, bool paged, dim3 grid, int un
     // caches and for many units (chunked prefill); paged decode grids keep the
     // vector-unit logits and the shared softmax, which measured faster there.
     const bool many = grid.x / a.splits >= (unsigned)kManyUnits;
-    // The weighted V goes to the matrix cores as well on decode grids; chunked
-    // prefill (held by its gathers) measured faster with it on bf16 dot2.
     constexpr int NWM = kManyUnitWaves;
-    if (paged && many) sparse_attn_kernel<G, true, DENSE, true, false, NWM><<<grid, dim3(64 * NWM), 0, stream>>>(a);
-    else if (paged) sparse_attn_kernel<G, true, DENSE, false, false, 4><<<grid, dim3(256), 0, stream>>>(a);
-    else if (many) sparse_attn_kernel<G, false, DENSE, true, false, NWM><<<grid, dim3(64 * NWM), 0, stream>>>(a);
-    else sparse_attn_kernel<G, false, DENSE, true, true, 4><<<grid, dim3(256), 0, stream>>>(a);
+    if (paged && many) sparse_attn_kernel<G, true, DENSE, true, NWM><<<grid, dim3(64 * NWM), 0, stream>>>(a);
+    else if (paged) sparse_attn_kernel<G, true, DENSE, false, 4><<<grid, dim3(256), 0, stream>>>(a);
+    else if (many) sparse_attn_kernel<G, false, DENSE, true, NWM><<<grid, dim3(64 * NWM), 0, stream>>>(a);
+    else sparse_attn_kernel<G, false, DENSE, true, 4><<<grid, dim3(256), 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && split_done) e = hipEventRecord(split_done, stream);
     if (e != hipSuccess || a.splits == 1 || a.tickets) return e;

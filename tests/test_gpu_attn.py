@@ -84,11 +84,13 @@ def test_many_rows_split_by_key_range():
 
 
 @pytest.mark.parametrize("qh,kvh,nq,k,ps", [(16, 4, 1030, 256, 0), (16, 2, 2050, 128, 64),
-                                            (20, 4, 1030, 320, 64)])
+                                            (20, 4, 1030, 320, 64), (16, 8, 600, 512, 64)])
 def test_matrix_core_logits_form(qh, kvh, nq, k, ps):
-    """Over 4096 (row, KV head) units the logits run on the matrix cores and each
-    wave keeps its own softmax state: groups of 4, 8 and 5 heads, one split
-    (k = 128) and several, contiguous and paged, ragged counts (0, 1, 37, 63, 65)."""
+    """Over 4096 (row, KV head) units the chunked-prefill form runs (one wave per
+    workgroup, rotated chunk order, logits and weighted V on the matrix cores,
+    per-wave softmax states): groups of 4, 8, 5 and 2 heads, one split (k = 128)
+    and several, contiguous and paged, ragged counts (0, 1, 37, 63, 65) that
+    leave splits shorter than the chunk they would start from."""
     w = inputs.small_workload(batch=1, lens=(4000,), n_q=nq, causal=True, q_pos0=(4000 - nq,),
                               top_k=k, q_heads=qh, kv_heads=kvh, page_size=ps, n_layers=1,
                               wid=88)
