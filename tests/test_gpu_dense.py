@@ -59,11 +59,14 @@ def test_causal_rows():
     _case(w, "dense causal rows")
 
 
-def test_many_rows_split_by_key_range():
-    """Dense attention over 4096+ (row, KV head) units, split by key range."""
-    w = inputs.small_workload(batch=1, lens=(1500,), n_q=520, causal=True, q_pos0=(980,),
-                              q_heads=8, kv_heads=8, n_layers=1, wid=75)
-    _case(w, "dense 520 causal rows x 8 KV heads")
+@pytest.mark.parametrize("qh,kvh,nq,ps", [(8, 8, 520, 0), (32, 8, 520, 64), (20, 4, 1030, 0)])
+def test_many_rows_split_by_key_range(qh, kvh, nq, ps):
+    """Dense attention over 4096+ (row, KV head) units (the one-wave chunked-prefill
+    form with its rotated chunk order), split by key range: groups of 1, 4 and 5
+    heads, contiguous and paged caches."""
+    w = inputs.small_workload(batch=1, lens=(1500,), n_q=nq, causal=True, q_pos0=(1500 - nq,),
+                              q_heads=qh, kv_heads=kvh, page_size=ps, n_layers=1, wid=75)
+    _case(w, f"dense {nq} causal rows Hq={qh} Hkv={kvh} page={ps}")
 
 
 def test_many_splits_one_row():
