@@ -212,7 +212,7 @@ void sparse_attn_kernel(AttnArgs a) {
     static_assert(NW == 4 || MQK, "fewer waves per workgroup: the matrix-core form only");
     constexpr int CH = 16 * NW;  // tokens per chunk: 16 per wave
     // Many-unit form (NW < 4): one wave per workgroup and five waves per
-    // SIMD (G <= 5; G = 8 keeps four, its accumulators need the registers), so
+    // SIMD (G <= 5; G = 8 needs 97 registers and 10.6 KB of LDS, so four), so
     // that as many rows as possible are resident at once (see the chunk order
     // below); the query operands therefore wait in LDS instead of 16 registers:
     // the G query rows, which every wave writes in full (the same values) and
