@@ -107,3 +107,32 @@ def test_paged():
 def test_without_lse():
     w = inputs.small_workload(batch=2, lens=(3000, 1700), top_k=512, n_layers=1, wid=86)
     _case(w, 6, with_lse=False, what="no lse")
+
+
+@pytest.mark.parametrize("case", range(10))
+def test_many_unit_shape_sweep(case):
+    """Seeded shapes over 4096 (row, KV head) units, where the kernel runs one
+    wave per workgroup and walks each workgroup's chunks in a rotated order:
+    KV heads 2, 4 or 8, groups of 1, 2, 4, 5 or 8 query heads, contiguous or
+    paged caches, top-k values that are not multiples of the 16-token chunk,
+    sequences shorter than k, and some rows' counts overridden (0, 1, a
+    random count) so that splits end inside a chunk or hold fewer chunks than
+    the one they would start from."""
+    g = np.random.default_rng(9100 + case)
+    kvh = (2, 4, 8)[case % 3]
+    grp = (1, 2, 4, 5, 8)[case % 5]
+    k = int(g.integers(17, 700))
+    batch = int(g.choice([1, 2]))
+    nq = -(-4096 // (kvh * batch)) + int(g.integers(0, 64))
+    lens = tuple(int(v) for v in g.integers(max(k // 2, 8), 5000, size=batch))
+    ps = int(g.choice([0, 64]))
+    w = inputs.small_workload(batch=batch, lens=lens, n_q=nq, top_k=k, q_heads=kvh * grp,
+                              kv_heads=kvh, page_size=ps, n_layers=1, wid=90 + case)
+    over = {}
+    for t in g.choice(nq, size=6, replace=False):
+        b = int(g.integers(0, batch))
+        over[(b, int(t))] = int(g.choice([0, 1, int(g.integers(0, min(k, lens[b]) + 1))]))
+    what = (f"sweep {case}: B={batch} rows={nq} Hkv={kvh} G={grp} k={k} lens={lens} "
+            f"page={ps}")
+    U.log("  " + what)
+    _case(w, 40 + case, nsel_override=over, what=what)
