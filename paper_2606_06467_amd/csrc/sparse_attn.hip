@@ -60,8 +60,8 @@ constexpr int kManyUnits = 4096; // (row, KV head) units from which splits go by
 constexpr int kKtPitch = 17;     // 16-byte pieces per staged K row (one of padding)
 constexpr int kManySplits = 8;   // splits per unit then (measured best of 1, 2, 4, 8, 16)
 constexpr int kManyUnitWaves = 1;    // waves per workgroup of the many-unit form (measured 1, 2, 4)
-constexpr int kResidentWaves = 5120; // many units: waves resident on the chip (5 per SIMD), the
-                                     // base of the chunk-order period (4096..5120 measured alike)
+constexpr int kRotationWaves = 4352; // many units: base of the chunk-order period, a little under
+                                     // the 5120 waves resident (5 per SIMD); 3584..5632 measured
 
 // The fields every workgroup reads first come first: the kernel's prologue
 // then fetches them in one batch of scalar loads (a field pushed past them
@@ -248,10 +248,10 @@ void sparse_attn_kernel(AttnArgs a) {
     const int tok_begin = split * span;
     // Chunk order of the many-unit form (NW < 4): a workgroup starts at
     // chunk (blockIdx / P) mod cps of its cps chunks and wraps around, P being
-    // the resident workgroups (kResidentWaves / NW) over cps.  Workgroups start
-    // in grid order, about P per chunk time once the chip is full, so the
-    // resident ones tend to be on the same chunk of their stretch at the same
-    // time; as the index lists are ascending and all rows' stretches span about
+    // about the resident workgroups (kRotationWaves / NW) over cps.  Workgroups
+    // start in grid order, about P per chunk time once the chip is full, so
+    // the resident ones tend to be on the same chunk of their stretch at the
+    // same time; as the index lists are ascending and all rows' stretches span about
     // the same keys, the K/V rows gathered at any moment come from about one
     // chunk's share of the stretch instead of all of it, and each of them is
     // gathered by more of the resident rows while the L2 still holds it, the
@@ -259,7 +259,7 @@ void sparse_attn_kernel(AttnArgs a) {
     // of the chunks (only the order of its fp32 roundings does).
     constexpr bool ROT = NW < 4;
     const int cps = span / CH;  // chunks per split
-    const unsigned rot_period = max(1, kResidentWaves / NW / cps);
+    const unsigned rot_period = max(1, kRotationWaves / NW / cps);
     const int rot = ROT && split_major ? (int)((blockIdx.x / rot_period) % (unsigned)cps) : 0;
     const int row_elems = a.kv_heads * kHeadDim;
     const char *kseq = reinterpret_cast<const char *>(
