@@ -17,7 +17,9 @@ from tests import gpu_util as U
 pytestmark = pytest.mark.gpu
 
 
-def _gpu_step(w, x, n_layers):
+def _gpu_step(w, x, n_layers, ws_fill=None):
+    """One step through clsa_decode_step; ws_fill: a byte the workspace is
+    filled with first (None: whatever the allocator hands out)."""
     import torch
     from paper_2606_06467_amd import binding as B
     d = U.to_dev(x)
@@ -29,6 +31,8 @@ def _gpu_step(w, x, n_layers):
     idx = torch.full((w.batch, w.n_q, w.top_k), -7, dtype=torch.int32, device="cuda")
     ns = torch.full((w.batch, w.n_q), -7, dtype=torch.int32, device="cuda")
     ws = B.workspace(sh, B.CLSA_OP_DECODE, L)
+    if ws is not None and ws_fill is not None:
+        ws.fill_(ws_fill)
     B.clsa_decode_step(sh, d["q_idx"], d["k_idx"], d["k_cache"], d["v_cache"], d["page_table"],
                        d["seq_lens"], d["q_pos"], d["q_layers"], out, lse, idx, ns, ws)
     torch.cuda.synchronize()
@@ -119,6 +123,33 @@ def test_deterministic_bits():
     b = _gpu_step(w, x, w.n_layers)
     for u, v in zip(a, b):
         np.testing.assert_array_equal(u, v)
+
+
+@pytest.mark.parametrize("kind", ["prefill", "decode"])
+def test_workspace_contents_do_not_matter(kind):
+    """The workspace carries nothing from one call to the next: filled with one
+    bits (NaN scores, counts and counters at their maximum) or with zero bits
+    before the step, it gives the same bits as a freshly allocated one.  prefill:
+    600 causal rows through the two-pass top-k (forty rows with a zero index
+    query finish the slow way) and the many-unit attention with its in-kernel
+    merge; decode: four long rows through the coarse histogram and the wide
+    top-k."""
+    if kind == "prefill":
+        w = inputs.small_workload(batch=2, lens=(20000, 20000), n_q=300, causal=True,
+                                  q_pos0=(19700, 19700), top_k=256, n_layers=2, wid=87)
+        x = inputs.make_inputs(w)
+        x["q_idx"][0, :40] = 0
+        assert w.batch * w.n_q > 128 and w.batch * w.n_q * w.kv_heads >= 4096
+    else:
+        w = inputs.small_workload(batch=4, lens=(60000, 45000, 30001, 52000), top_k=2048,
+                                  n_layers=2, wid=88)
+        x = inputs.make_inputs(w)
+    ref = _gpu_step(w, x, w.n_layers)
+    for fill in (0xFF, 0x00):
+        U.log(f"  {kind}: workspace filled with {fill:#04x}")
+        got = _gpu_step(w, x, w.n_layers, ws_fill=fill)
+        for u, v in zip(ref, got):
+            np.testing.assert_array_equal(u, v)
 
 
 def test_full_decode_b4_n128k_planted():
